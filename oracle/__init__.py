@@ -1,0 +1,164 @@
+"""CPU oracle (fp64) for the pooled embedding-bag lookup and its sparse gradient.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg, never by the GPU product path.  The arithmetic
+lives in ``tbe_oracle.c`` (plain C, binary64); this module only marshals
+numpy arrays into it through ctypes.  See ``tbe_oracle.c`` for the definition
+that is computed and for what pins it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+from .build import LIB_PATH, build
+
+F32, F16, BF16 = 0, 1, 2
+DTYPE_CODES = {"f32": F32, "f16": F16, "bf16": BF16}
+
+_lib = None
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        lib = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        i32, i64 = ctypes.c_int32, ctypes.c_int64
+        lib.oracle_forward.restype = ctypes.c_int
+        lib.oracle_forward.argtypes = [i32, i64, P, P, i32, P, P, P, i64, P, P, P]
+        lib.oracle_backward_segments.restype = ctypes.c_int
+        lib.oracle_backward_segments.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, P, P]
+        lib.oracle_backward_rows.restype = ctypes.c_int
+        lib.oracle_backward_rows.argtypes = [i32, i64, P, P, P, P, P, P, P, P, i64, P, P, P]
+        lib.oracle_decode.restype = ctypes.c_double
+        lib.oracle_decode.argtypes = [P, i32, i64]
+        _lib = lib
+    return _lib
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _c(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a), dtype=dtype)
+
+
+def _raw16(t: np.ndarray) -> np.ndarray:
+    """Table storage as 16-bit words (fp16 / bf16 payloads)."""
+    return np.ascontiguousarray(t).view(np.uint16)
+
+
+def decode(words: np.ndarray, dtype: str) -> np.ndarray:
+    """Decode stored elements to float64 with the oracle's own format decoder."""
+    lib = _load()
+    w = np.ascontiguousarray(words)
+    return np.array([lib.oracle_decode(_p(w), DTYPE_CODES[dtype], i) for i in range(w.size)])
+
+
+def forward(rows: Sequence[int], dims: Sequence[int], dtype: str, tables: Sequence[np.ndarray],
+            indices, offsets, B: int, weights=None):
+    """Pooled lookup in binary64.
+
+    tables[t] is table t as a [R_t, D_t] array of raw element storage: float32
+    for "f32", and 16-bit words (uint16 / float16 / any 2-byte dtype, read as
+    the raw bit pattern) for "f16" and "bf16".  Returns (out, absout), each
+    [B, total_dim] float64.
+    """
+    lib = _load()
+    T = len(rows)
+    rows_a, dims_a = _c(rows, np.int64), _c(dims, np.int32)
+    tabs = [np.ascontiguousarray(t) for t in tables]
+    ptrs = (ctypes.c_void_p * T)(*[t.ctypes.data for t in tabs])
+    idx, off = _c(indices, np.int64), _c(offsets, np.int64)
+    w = None if weights is None else _c(weights, np.float32)
+    total_dim = int(dims_a.astype(np.int64).sum())
+    out = np.zeros((B, total_dim), np.float64)
+    absout = np.zeros((B, total_dim), np.float64)
+    rc = lib.oracle_forward(T, B, _p(rows_a), _p(dims_a), DTYPE_CODES[dtype], ptrs, _p(idx), _p(off),
+                            idx.size, _p(w), _p(out), _p(absout))
+    if rc != 0:
+        raise OracleError(f"oracle_forward returned {rc}")
+    return out, absout
+
+
+def backward_segments(rows, dims, indices, offsets, B: int):
+    """Integer part of the sparse gradient.
+
+    Returns a dict with perm, sorted_keys, grad_idx, seg_offsets and
+    grad_row_offsets (trimmed to U and U+1 entries) and U.
+    """
+    lib = _load()
+    T = len(rows)
+    rows_a, dims_a = _c(rows, np.int64), _c(dims, np.int32)
+    idx, off = _c(indices, np.int64), _c(offsets, np.int64)
+    N = idx.size
+    perm = np.empty(max(N, 1), np.int64)
+    keys = np.empty(max(N, 1), np.int64)
+    gidx = np.empty(max(N, 1), np.int64)
+    seg = np.empty(N + 1, np.int64)
+    gro = np.empty(N + 1, np.int64)
+    U = np.zeros(1, np.int64)
+    rc = lib.oracle_backward_segments(T, B, _p(rows_a), _p(dims_a), _p(idx), _p(off), N, _p(perm),
+                                      _p(keys), _p(gidx), _p(seg), _p(gro), _p(U))
+    if rc != 0:
+        raise OracleError(f"oracle_backward_segments returned {rc}")
+    u = int(U[0])
+    return {"perm": perm[:N], "sorted_keys": keys[:N], "grad_idx": gidx[:u],
+            "seg_offsets": seg[: u + 1], "grad_row_offsets": gro[: u + 1], "U": u}
+
+
+def backward_rows(rows, dims, offsets, B: int, grad_out, seg: dict, weights=None, sel=None):
+    """Gradient rows (binary64) of the selected unique ids (default: all).
+
+    Returns (rows_packed, abs_packed, row_offsets) where row s of the
+    selection occupies rows_packed[row_offsets[s]:row_offsets[s+1]].
+    """
+    lib = _load()
+    T = len(rows)
+    rows_a, dims_a = _c(rows, np.int64), _c(dims, np.int32)
+    off = _c(offsets, np.int64)
+    g = _c(grad_out, np.float32)
+    w = None if weights is None else _c(weights, np.float32)
+    gidx = _c(seg["grad_idx"], np.int64)
+    if sel is None:
+        sel_a, n_sel = None, int(seg["U"])
+        lens = np.diff(seg["grad_row_offsets"])
+    else:
+        sel_a = _c(sel, np.int64)
+        n_sel = sel_a.size
+        lens = np.diff(seg["grad_row_offsets"])[sel_a]
+    ro = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    total = int(ro[-1])
+    out = np.zeros(max(total, 1), np.float64)
+    absout = np.zeros(max(total, 1), np.float64)
+    rc = lib.oracle_backward_rows(T, B, _p(rows_a), _p(dims_a), _p(off), _p(w), _p(g),
+                                  _p(_c(seg["perm"], np.int64)), _p(gidx), _p(_c(seg["seg_offsets"], np.int64)),
+                                  n_sel, _p(sel_a), _p(out), _p(absout))
+    if rc != 0:
+        raise OracleError(f"oracle_backward_rows returned {rc}")
+    return out[:total], absout[:total], ro
+
+
+def summation_error(y, y_ref, abs_ref) -> np.ndarray:
+    """|y - y_ref| / sum|terms| elementwise, with 0/0 taken as 0.
+
+    The scale is the sum of the absolute values of the summed terms, the
+    backward-error scale for floating-point summation; a plain relative error
+    is unbounded where the terms cancel.
+    """
+    y = np.asarray(y, np.float64)
+    diff = np.abs(y - y_ref)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        e = np.where(abs_ref > 0, diff / np.where(abs_ref > 0, abs_ref, 1.0), np.where(diff > 0, np.inf, 0.0))
+    return e

@@ -1,0 +1,356 @@
+/*
+ * CPU oracle for the batched, multi-table pooled embedding-bag lookup and its
+ * sparse (row-wise) gradient.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously correct
+ * definition that the GPU path is checked against.  Only the test suite, the
+ * smoke check and the benchmark's CPU-baseline leg load it; the product path
+ * never links, calls or falls back to it.  It shares no code, header, table or
+ * helper with the GPU library.
+ *
+ * What it computes.  The paper motivates the operator but does not write it
+ * down: DLRM models hold very large embedding tables whose lookup-and-pool
+ * kernels are bound by memory bandwidth and irregular access (Introduction,
+ * "Model Diversity Across Ranking Stages"; Background, "DLRM Architecture"),
+ * sparse features are variable-length int64 id lists and weighted sparse
+ * features pair each id with an fp32 score (Background, "Feature Types and
+ * Memory Layout"), and a training operator also supplies its backward
+ * (Evaluation and Tooling Framework, "Kernel Output Format", footnote).  The
+ * definition written out here is the standard pooled lookup: with bag
+ * k = t*B + b holding lookups j in [offsets[k], offsets[k+1]),
+ *
+ *     out[b, dim_off[t] + d] = sum_j w_j * W_t[idx_j, d],    d < D_t,
+ *
+ * (w_j = per-sample weight, or 1), i.e. out_t = A_t W_t with the multi-hot
+ * matrix A_t[b, r] = sum of w_j over the lookups of bag (t, b) that hit row r.
+ * Its gradient with respect to the tables is A_t^T G_t, nonzero only on the
+ * rows that were looked up; the sparse form lists those rows once each, in
+ * ascending global row id (row_base[t] + r), with their gradient rows.
+ *
+ * Arithmetic.  Every table element is widened to double exactly (fp16, bf16
+ * and fp32 all fit in binary64), every product of an fp32 weight or gradient
+ * with such an element is exact in binary64, and sums run in lookup order in
+ * binary64.  Alongside each output the oracle returns sum_j |w_j * x_j|, the
+ * scale against which a lower-precision result is judged.
+ *
+ * Parity is pinned (in the CPU tests) by: brute-force dense one-hot products
+ * A_t W_t and A_t^T G_t in numpy; torch's embedding_bag on the CPU; numpy's
+ * unique / stable argsort for the integer outputs; hand-worked fixtures; and
+ * the invariants of the definition (empty bag = 0, permutation within a bag,
+ * additivity, duplicate = weight 2, exact scaling by powers of two, the
+ * backward column-sum and adjoint identities).
+ *
+ * Build: gcc -O2 -fopenmp -ffp-contract=off -shared -fPIC (no fast-math).
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_F32 0
+#define ORC_F16 1
+#define ORC_BF16 2
+
+#define ORC_OK 0
+#define ORC_ERR_ARG (-1)
+#define ORC_ERR_INDEX (-2)
+#define ORC_ERR_OFFSETS (-3)
+#define ORC_ERR_CAPACITY (-4)
+
+/* IEEE 754 binary16 -> binary64, from the format's definition:
+ * value = (-1)^s * 2^(e-15) * (1 + m/1024) for 0 < e < 31,
+ *         (-1)^s * 2^-14 * (m/1024) for e = 0, inf/nan for e = 31. */
+static double half_to_double(uint16_t h)
+{
+    int s = (h >> 15) & 1;
+    int e = (h >> 10) & 0x1f;
+    int m = h & 0x3ff;
+    double v;
+    if (e == 0) {
+        v = (double)m * (1.0 / 16777216.0); /* m * 2^-24 */
+    } else if (e == 31) {
+        v = m ? (0.0 / 0.0) : (1.0 / 0.0);
+    } else {
+        double p = 1.0;
+        int k;
+        if (e >= 15)
+            for (k = 15; k < e; k++) p *= 2.0;
+        else
+            for (k = e; k < 15; k++) p *= 0.5;
+        v = p * (1.0 + (double)m / 1024.0);
+    }
+    return s ? -v : v;
+}
+
+/* bfloat16 is the upper half of an IEEE binary32 word. */
+static double bf16_to_double(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+static double table_elem(const void *table, int32_t dtype, int64_t i)
+{
+    if (dtype == ORC_F32) return (double)((const float *)table)[i];
+    if (dtype == ORC_F16) return half_to_double(((const uint16_t *)table)[i]);
+    return bf16_to_double(((const uint16_t *)table)[i]);
+}
+
+static int check_offsets(int64_t nbags, const int64_t *offsets, int64_t n)
+{
+    int64_t k;
+    if (offsets[0] != 0 || offsets[nbags] != n) return ORC_ERR_OFFSETS;
+    for (k = 0; k < nbags; k++)
+        if (offsets[k + 1] < offsets[k]) return ORC_ERR_OFFSETS;
+    return ORC_OK;
+}
+
+/* Decode one element so the tests can pin the format conversion itself. */
+double oracle_decode(const void *table, int32_t dtype, int64_t i)
+{
+    return table_elem(table, dtype, i);
+}
+
+/*
+ * Forward pooled lookup.
+ *   T, B            number of tables, batch size
+ *   rows[T], dims[T] table shapes R_t x D_t
+ *   dtype           element type of every table (ORC_F32 / ORC_F16 / ORC_BF16)
+ *   tables[T]       host pointer to table t, row-major R_t x D_t
+ *   indices[N]      lookup indices, local to their table
+ *   offsets[T*B+1]  CSR bag boundaries, bag k = t*B + b
+ *   weights[N]      per-sample weights, or NULL for plain sum pooling
+ *   out, absout     [B x total_dim] binary64: the pooled sums and sum |w x|
+ * Returns ORC_OK, or an error (nothing guaranteed written) for an index out of
+ * range or offsets that are not a monotone CSR array ending at N.
+ */
+int oracle_forward(int32_t T, int64_t B, const int64_t *rows, const int32_t *dims, int32_t dtype,
+                   const void *const *tables, const int64_t *indices, const int64_t *offsets,
+                   int64_t N, const float *weights, double *out, double *absout)
+{
+    int64_t total_dim = 0, *dim_off;
+    int64_t k;
+    int t, rc;
+    if (T <= 0 || B < 0 || N < 0) return ORC_ERR_ARG;
+    rc = check_offsets((int64_t)T * B, offsets, N);
+    if (rc) return rc;
+    dim_off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
+    if (!dim_off) return ORC_ERR_ARG;
+    for (t = 0; t < T; t++) {
+        dim_off[t] = total_dim;
+        total_dim += dims[t];
+    }
+    dim_off[T] = total_dim;
+
+    /* every lookup must address a row of its own table */
+    for (t = 0; t < T; t++) {
+        int64_t j;
+        for (j = offsets[(int64_t)t * B]; j < offsets[(int64_t)(t + 1) * B]; j++)
+            if (indices[j] < 0 || indices[j] >= rows[t]) {
+                free(dim_off);
+                return ORC_ERR_INDEX;
+            }
+    }
+
+#pragma omp parallel for schedule(dynamic, 64)
+    for (k = 0; k < (int64_t)T * B; k++) {
+        int64_t tt = k / B, b = k % B, j;
+        int64_t D = dims[tt];
+        double *o = out + b * total_dim + dim_off[tt];
+        double *a = absout + b * total_dim + dim_off[tt];
+        int64_t d;
+        for (d = 0; d < D; d++) {
+            o[d] = 0.0;
+            a[d] = 0.0;
+        }
+        for (j = offsets[k]; j < offsets[k + 1]; j++) {
+            double w = weights ? (double)weights[j] : 1.0;
+            for (d = 0; d < D; d++) {
+                double term = w * table_elem(tables[tt], dtype, indices[j] * D + d);
+                o[d] += term;
+                a[d] += term < 0 ? -term : term;
+            }
+        }
+    }
+    free(dim_off);
+    return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Backward                                                                 */
+
+typedef struct {
+    int64_t key;
+    int64_t pos;
+} orc_pair;
+
+/* Order by key, then by lookup position: a total order, so the library sort
+ * below yields exactly the stable order of the keys. */
+static int pair_cmp(const void *pa, const void *pb)
+{
+    const orc_pair *a = (const orc_pair *)pa, *b = (const orc_pair *)pb;
+    if (a->key != b->key) return a->key < b->key ? -1 : 1;
+    if (a->pos != b->pos) return a->pos < b->pos ? -1 : 1;
+    return 0;
+}
+
+/* Table that owns global row id g: the t with row_base[t] <= g < row_base[t+1]. */
+static int table_of_row(int32_t T, const int64_t *row_base, int64_t g)
+{
+    int lo = 0, hi = T; /* invariant: row_base[lo] <= g < row_base[hi] */
+    while (hi - lo > 1) {
+        int mid = (lo + hi) / 2;
+        if (row_base[mid] <= g) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+/* Bag that holds lookup j: the last k with offsets[k] <= j (empty bags have
+ * offsets[k] == offsets[k+1] and are skipped by taking the last one). */
+static int64_t bag_of_lookup(int64_t nbags, const int64_t *offsets, int64_t j)
+{
+    int64_t lo = 0, hi = nbags; /* offsets[lo] <= j < offsets[hi] */
+    while (hi - lo > 1) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (offsets[mid] <= j) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+/*
+ * Integer part of the sparse gradient: which rows, in which order, with which
+ * lookups.
+ *   key_j  = row_base[t(j)] + indices[j]          (global row id of lookup j)
+ *   perm   = the lookup positions sorted stably by key
+ *   sorted_keys[i] = key[perm[i]]                  (optional, may be NULL)
+ *   grad_idx[u]    = the distinct keys, ascending  (U = *num_unique of them)
+ *   seg_offsets[u] = first position in perm of row u; seg_offsets[U] = N
+ *   grad_row_offsets[u] = sum_{u' < u} D_{t(u')}; grad_row_offsets[U] = total
+ * Arrays are sized by the caller for the worst case U = N.
+ */
+int oracle_backward_segments(int32_t T, int64_t B, const int64_t *rows, const int32_t *dims,
+                             const int64_t *indices, const int64_t *offsets, int64_t N,
+                             int64_t *perm, int64_t *sorted_keys, int64_t *grad_idx,
+                             int64_t *seg_offsets, int64_t *grad_row_offsets, int64_t *num_unique)
+{
+    int64_t *row_base;
+    orc_pair *pairs;
+    int64_t j, i, U;
+    int t, rc;
+    if (T <= 0 || B < 0 || N < 0) return ORC_ERR_ARG;
+    rc = check_offsets((int64_t)T * B, offsets, N);
+    if (rc) return rc;
+    row_base = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
+    pairs = (orc_pair *)malloc(sizeof(orc_pair) * (size_t)(N > 0 ? N : 1));
+    if (!row_base || !pairs) {
+        free(row_base);
+        free(pairs);
+        return ORC_ERR_ARG;
+    }
+    row_base[0] = 0;
+    for (t = 0; t < T; t++) row_base[t + 1] = row_base[t] + rows[t];
+
+    for (t = 0; t < T; t++) {
+        for (j = offsets[(int64_t)t * B]; j < offsets[(int64_t)(t + 1) * B]; j++) {
+            if (indices[j] < 0 || indices[j] >= rows[t]) {
+                free(row_base);
+                free(pairs);
+                return ORC_ERR_INDEX;
+            }
+            pairs[j].key = row_base[t] + indices[j];
+            pairs[j].pos = j;
+        }
+    }
+    qsort(pairs, (size_t)N, sizeof(orc_pair), pair_cmp);
+
+    U = 0;
+    for (i = 0; i < N; i++) {
+        perm[i] = pairs[i].pos;
+        if (sorted_keys) sorted_keys[i] = pairs[i].key;
+        if (i == 0 || pairs[i].key != pairs[i - 1].key) {
+            grad_idx[U] = pairs[i].key;
+            seg_offsets[U] = i;
+            U++;
+        }
+    }
+    seg_offsets[U] = N;
+    grad_row_offsets[0] = 0;
+    for (i = 0; i < U; i++)
+        grad_row_offsets[i + 1] = grad_row_offsets[i] + dims[table_of_row(T, row_base, grad_idx[i])];
+    *num_unique = U;
+    free(row_base);
+    free(pairs);
+    return ORC_OK;
+}
+
+/*
+ * Gradient rows of selected unique rows (all of them when sel == NULL):
+ *   g_u[d] = sum over i in [seg_offsets[u], seg_offsets[u+1]) of
+ *            w_{perm[i]} * grad_out[b(perm[i]), dim_off[t_u] + d],
+ * summed in sorted (= lookup position) order, in binary64.
+ *   grad_out  [B x total_dim] fp32;  weights [N] or NULL
+ *   perm, grad_idx, seg_offsets  from oracle_backward_segments
+ *   n_sel, sel    unique ids u to compute (or sel == NULL: u = 0..n_sel-1)
+ *   out, absout   the selected rows packed one after another (row s starts
+ *                 at sum_{s' < s} D_{t(sel[s'])}), and sum |w g| per element
+ */
+int oracle_backward_rows(int32_t T, int64_t B, const int64_t *rows, const int32_t *dims,
+                         const int64_t *offsets, const float *weights, const float *grad_out,
+                         const int64_t *perm, const int64_t *grad_idx, const int64_t *seg_offsets,
+                         int64_t n_sel, const int64_t *sel, double *out, double *absout)
+{
+    int64_t *row_base, *dim_off, *out_off;
+    int64_t s, total_dim;
+    int t;
+    if (T <= 0 || B < 0 || n_sel < 0) return ORC_ERR_ARG;
+    row_base = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
+    dim_off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
+    out_off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n_sel + 1));
+    if (!row_base || !dim_off || !out_off) {
+        free(row_base);
+        free(dim_off);
+        free(out_off);
+        return ORC_ERR_ARG;
+    }
+    row_base[0] = 0;
+    dim_off[0] = 0;
+    for (t = 0; t < T; t++) {
+        row_base[t + 1] = row_base[t] + rows[t];
+        dim_off[t + 1] = dim_off[t] + dims[t];
+    }
+    total_dim = dim_off[T];
+    out_off[0] = 0;
+    for (s = 0; s < n_sel; s++) {
+        int64_t u = sel ? sel[s] : s;
+        out_off[s + 1] = out_off[s] + dims[table_of_row(T, row_base, grad_idx[u])];
+    }
+
+#pragma omp parallel for schedule(dynamic, 16)
+    for (s = 0; s < n_sel; s++) {
+        int64_t u = sel ? sel[s] : s;
+        int tu = table_of_row(T, row_base, grad_idx[u]);
+        int64_t D = dims[tu], d, i;
+        double *o = out + out_off[s], *a = absout + out_off[s];
+        for (d = 0; d < D; d++) {
+            o[d] = 0.0;
+            a[d] = 0.0;
+        }
+        for (i = seg_offsets[u]; i < seg_offsets[u + 1]; i++) {
+            int64_t j = perm[i];
+            int64_t k = bag_of_lookup((int64_t)T * B, offsets, j);
+            int64_t b = k % B;
+            double w = weights ? (double)weights[j] : 1.0;
+            const float *g = grad_out + b * total_dim + dim_off[tu];
+            for (d = 0; d < D; d++) {
+                double term = w * (double)g[d];
+                o[d] += term;
+                a[d] += term < 0 ? -term : term;
+            }
+        }
+    }
+    free(row_base);
+    free(dim_off);
+    free(out_off);
+    return ORC_OK;
+}
