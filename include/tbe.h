@@ -1,0 +1,173 @@
+/*
+ * tbe.h -- C ABI of the MI355X (gfx950) batched multi-table pooled
+ * embedding-bag library: forward lookup-and-pool and its sparse, row-wise
+ * gradient.
+ *
+ * The operator.  The paper motivates it without writing it down: DLRM models
+ * hold embedding tables large enough to be bound by memory capacity and
+ * bandwidth, served by lookup-and-aggregation kernels built for irregular
+ * access (Introduction, "Model Diversity Across Ranking Stages"; Background,
+ * "DLRM Architecture"); sparse features are variable-length int64 id lists and
+ * weighted sparse features pair each id with an fp32 score (Background,
+ * "Feature Types and Memory Layout"); a training operator also provides its
+ * backward (Evaluation and Tooling Framework, "Kernel Output Format",
+ * footnote).  With T tables (table t: R_t rows of D_t elements), batch B, and
+ * bag k = t*B + b holding lookups j in [offsets[k], offsets[k+1]):
+ *
+ *   forward   out[b, dim_off[t] + d] = sum_j w_j * W_t[indices[j], d]
+ *             (w_j = per_sample_weights[j], or 1), accumulated in fp32;
+ *   backward  for every distinct global row id g = row_base[t] + indices[j]
+ *             that occurs, in ascending order, the row
+ *             grad[g][d] = sum over lookups j of g, in lookup order,
+ *                          of w_j * grad_out[b(j), dim_off[t] + d].
+ *
+ * Conventions shared by every entry point.
+ *   - "host" pointers are CPU memory read during the call; "device" pointers
+ *     are GPU memory (hipMalloc'd or equivalent) on the current HIP device.
+ *   - The caller owns every buffer.  The library allocates only the small
+ *     per-plan metadata (tbe_plan_create), never frees caller memory, and
+ *     never synchronises: all work is queued on `stream` (a hipStream_t;
+ *     NULL = the default stream) and is complete once that stream is.
+ *   - Return value: TBE_OK (0), or a negative TBE_ERR_* code.  Every
+ *     TBE_ERR_* except TBE_ERR_HIP is detected on the host before anything
+ *     is queued.
+ *   - Errors that only the GPU can see (bad index, bad offsets, too small an
+ *     output) are OR-ed into the caller's device int32 `*status` as
+ *     TBE_STATUS_* bits, readable after the stream completes.  With bounds
+ *     checking on, an out-of-range lookup contributes nothing and is never
+ *     dereferenced, and a malformed bag is treated as empty.
+ *   - Entry points are reentrant; no C++ type or exception crosses the ABI.
+ */
+#ifndef TBE_H
+#define TBE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TBE_ABI_VERSION 1
+
+/* Element type of every table. */
+enum tbe_dtype { TBE_F32 = 0, TBE_F16 = 1, TBE_BF16 = 2 };
+
+/* Host-detected errors (return values). */
+enum tbe_error {
+    TBE_OK = 0,
+    TBE_ERR_NULL = -1,      /* a required pointer is NULL                        */
+    TBE_ERR_SHAPE = -2,     /* a count, size or shape is out of range           */
+    TBE_ERR_DTYPE = -3,     /* unknown element type                             */
+    TBE_ERR_ALIGN = -4,     /* D_t * elem_size not a multiple of 16 bytes, or a
+                               table / output / buffer not 16-byte aligned       */
+    TBE_ERR_WORKSPACE = -5, /* backward workspace smaller than required          */
+    TBE_ERR_HIP = -6,       /* a HIP runtime call failed                         */
+    TBE_ERR_NOMEM = -7      /* host allocation failed                            */
+};
+
+/* Device-detected errors (bits OR-ed into *status). */
+enum tbe_status_bits {
+    TBE_STATUS_INDEX_OOB = 1, /* some lookup index < 0 or >= R_t                 */
+    TBE_STATUS_OFFSETS = 2,   /* offsets[0] != 0, offsets decreasing, or last != N */
+    TBE_STATUS_CAPACITY = 4   /* backward output longer than grad_rows_capacity */
+};
+
+/* Description of the tables; read during tbe_plan_create only. */
+typedef struct tbe_desc {
+    int32_t num_tables;           /* T >= 1                                       */
+    int32_t dtype;                /* enum tbe_dtype                               */
+    int64_t batch_size;           /* B >= 0                                       */
+    const int64_t *rows;          /* host [T]: R_t >= 1                           */
+    const int32_t *dims;          /* host [T]: D_t >= 1, D_t*elem_size % 16 == 0  */
+    const int64_t *table_offsets; /* host [T]: element offset of table t in the
+                                     flat tables buffer (row-major R_t x D_t,
+                                     16-byte aligned); NULL = tables packed in
+                                     order with no gaps                          */
+    int64_t table_elems;          /* elements in the flat tables buffer; every
+                                     table must lie inside it                    */
+    int32_t bounds_check;         /* 1 = check indices and offsets on the GPU,
+                                     0 = trust them                              */
+} tbe_desc;
+
+/* Validated description plus its per-table metadata on the device
+ * (element offset, rows, global row base, dim, output column offset). */
+typedef struct tbe_plan tbe_plan;
+
+/* TBE_ABI_VERSION of the built library. */
+int32_t tbe_abi_version(void);
+
+/* Static text for a tbe_error code. */
+const char *tbe_error_string(int32_t code);
+
+/*
+ * Validates `desc` and builds a plan for the current HIP device: dim_off[t]
+ * (output column of table t), row_base[t] (first global row id of table t),
+ * total_dim and the table placement, uploaded once to a small device array.
+ * On success *plan owns that array until tbe_plan_destroy.  On any error
+ * *plan is set to NULL and nothing is allocated.
+ */
+int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan);
+
+/* Frees a plan (NULL is accepted).  The plan must not be in use on a stream. */
+int32_t tbe_plan_destroy(tbe_plan *plan);
+
+/* Read-only facts about a plan (any pointer may be NULL). */
+int32_t tbe_plan_info(const tbe_plan *plan, int64_t *total_dim, int64_t *total_rows,
+                      int32_t *key_bits);
+
+/*
+ * Forward pooled lookup.
+ *   tables              device, the flat buffer described by the plan
+ *   indices             device int64 [num_indices], local to each bag's table
+ *   offsets             device int64 [T*B + 1], CSR bag boundaries, k = t*B + b
+ *   num_indices         N = offsets[T*B]
+ *   per_sample_weights  device fp32 [N], or NULL for plain sum pooling
+ *   out                 device fp32 [B x total_dim] row-major, 16-byte aligned;
+ *                       every element is written (an empty bag gives +0.0)
+ *   status              device int32, OR-ed with TBE_STATUS_* bits; may be NULL
+ *                       only when the plan does not check bounds
+ * One wavefront pools one (bag, table); the output has exactly one writer
+ * per element, so results are bitwise reproducible.
+ */
+int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *indices,
+                    const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+                    float *out, int32_t *status, void *stream);
+
+/* Bytes of device workspace tbe_backward needs for num_indices lookups. */
+int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, size_t *bytes);
+
+/*
+ * Sparse gradient of the tables.
+ *   grad_out            device fp32 [B x total_dim], the gradient of `out`
+ *   indices, offsets, num_indices, per_sample_weights   as in tbe_forward
+ *   workspace           device, >= tbe_backward_workspace_bytes, 256-byte aligned;
+ *                       scratch only, its contents are not part of the result
+ *   grad_rows           device fp32, capacity grad_rows_capacity floats: the
+ *                       gradient rows one after another, row u at
+ *                       grad_row_offsets[u], D_{t(u)} floats long
+ *   grad_idx            device int64 [N]: the U distinct global row ids
+ *                       (row_base[t] + index), ascending
+ *   seg_offsets         device int64 [N+1]: lookups of row u are positions
+ *                       seg_offsets[u] .. seg_offsets[u+1]-1 of the stable
+ *                       sort of the lookups by global row id; seg_offsets[U] = N
+ *   grad_row_offsets    device int64 [N+1]: prefix sums of D_{t(u)}
+ *   num_unique          device int64 scalar: U
+ *   status              as in tbe_forward; TBE_STATUS_CAPACITY is set (and no
+ *                       gradient row written) if grad_row_offsets[U] exceeds
+ *                       grad_rows_capacity
+ * Entries past U of grad_idx / seg_offsets / grad_row_offsets are unspecified.
+ * Every gradient row has a single writer and a fixed summation order, so the
+ * result is bitwise reproducible.
+ */
+int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t *indices,
+                     const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+                     void *workspace, size_t workspace_bytes, float *grad_rows,
+                     int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
+                     int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TBE_H */

@@ -1,0 +1,206 @@
+// C ABI of the embedding-bag library: host-side validation, plan metadata,
+// and dispatch to the kernels.  Every check that the host can make is made
+// before anything is queued on the stream.
+
+#include <new>
+
+#include "tbe_internal.h"
+
+struct tbe_plan {
+    tbe::Plan p;
+};
+
+namespace {
+
+bool aligned16(const void *ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+int32_t validate_desc(const tbe_desc *d) {
+    if (!d || !d->rows || !d->dims) return TBE_ERR_NULL;
+    if (d->dtype != TBE_F32 && d->dtype != TBE_F16 && d->dtype != TBE_BF16) return TBE_ERR_DTYPE;
+    if (d->num_tables < 1 || d->batch_size < 0 || d->table_elems < 0) return TBE_ERR_SHAPE;
+    if (d->bounds_check != 0 && d->bounds_check != 1) return TBE_ERR_SHAPE;
+    // bag ids and output columns are kept in 32 bits on the device
+    if (static_cast<int64_t>(d->num_tables) * d->batch_size >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
+    const int es = tbe::elem_size(d->dtype);
+    int64_t packed = 0, total_dim = 0, total_rows = 0;
+    for (int32_t t = 0; t < d->num_tables; ++t) {
+        const int64_t R = d->rows[t];
+        const int32_t D = d->dims[t];
+        if (R < 1 || D < 1) return TBE_ERR_SHAPE;
+        if ((static_cast<int64_t>(D) * es) % 16 != 0) return TBE_ERR_ALIGN;
+        if (R > (int64_t(1) << 40) || D > (1 << 20)) return TBE_ERR_SHAPE;
+        const int64_t off = d->table_offsets ? d->table_offsets[t] : packed;
+        if (off < 0 || (off * es) % 16 != 0) return TBE_ERR_ALIGN;
+        if (off > d->table_elems || R * D > d->table_elems - off) return TBE_ERR_SHAPE;
+        packed += R * D;
+        total_dim += D;
+        total_rows += R;
+        if (total_dim >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
+        if (total_rows >= (int64_t(1) << 62)) return TBE_ERR_SHAPE;
+    }
+    return TBE_OK;
+}
+
+const tbe::Plan *plan_of(const tbe_plan *p) { return p ? &p->p : nullptr; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t tbe_abi_version(void) { return TBE_ABI_VERSION; }
+
+const char *tbe_error_string(int32_t code) {
+    switch (code) {
+        case TBE_OK: return "ok";
+        case TBE_ERR_NULL: return "a required pointer is NULL";
+        case TBE_ERR_SHAPE: return "a count, size or shape is out of range";
+        case TBE_ERR_DTYPE: return "unknown element type";
+        case TBE_ERR_ALIGN: return "row width or a buffer is not 16-byte aligned";
+        case TBE_ERR_WORKSPACE: return "workspace smaller than required";
+        case TBE_ERR_HIP: return "a HIP runtime call failed";
+        case TBE_ERR_NOMEM: return "host allocation failed";
+        default: return "unknown error code";
+    }
+}
+
+int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
+    if (!plan) return TBE_ERR_NULL;
+    *plan = nullptr;
+    const int32_t rc = validate_desc(desc);
+    if (rc != TBE_OK) return rc;
+
+    tbe_plan *h = new (std::nothrow) tbe_plan();
+    if (!h) return TBE_ERR_NOMEM;
+    tbe::Plan &p = h->p;
+    p.T = desc->num_tables;
+    p.dtype = desc->dtype;
+    p.B = desc->batch_size;
+    p.bounds_check = desc->bounds_check;
+    p.table_elems = desc->table_elems;
+    p.meta_host = new (std::nothrow) tbe::TableMeta[p.T];
+    if (!p.meta_host) {
+        delete h;
+        return TBE_ERR_NOMEM;
+    }
+    const int es = tbe::elem_size(p.dtype);
+    int64_t packed = 0, dim_off = 0, row_base = 0;
+    for (int32_t t = 0; t < p.T; ++t) {
+        tbe::TableMeta &m = p.meta_host[t];
+        const int64_t R = desc->rows[t];
+        const int32_t D = desc->dims[t];
+        m.elem_offset = desc->table_offsets ? desc->table_offsets[t] : packed;
+        m.rows = R;
+        m.row_base = row_base;
+        m.dim = D;
+        m.dim_off = static_cast<int32_t>(dim_off);
+        m.nvec = static_cast<int32_t>(static_cast<int64_t>(D) * es / 16);
+        int l = 0;
+        while ((1 << l) < m.nvec && l < 6) ++l;
+        m.lpr_log2 = l;
+        m.pad[0] = m.pad[1] = 0;
+        packed += R * D;
+        dim_off += D;
+        row_base += R;
+        if (D > p.max_dim) p.max_dim = D;
+    }
+    p.total_dim = dim_off;
+    p.total_rows = row_base;
+    int bits = 1;
+    while (bits < 63 && (int64_t(1) << bits) < p.total_rows) ++bits;
+    p.key_bits = bits;
+
+    if (hipGetDevice(&p.device) != hipSuccess ||
+        hipMalloc(reinterpret_cast<void **>(&p.meta_dev), sizeof(tbe::TableMeta) * p.T) != hipSuccess ||
+        hipMemcpy(p.meta_dev, p.meta_host, sizeof(tbe::TableMeta) * p.T, hipMemcpyHostToDevice) !=
+            hipSuccess) {
+        if (p.meta_dev) (void)hipFree(p.meta_dev);
+        delete[] p.meta_host;
+        delete h;
+        return TBE_ERR_HIP;
+    }
+    *plan = h;
+    return TBE_OK;
+}
+
+int32_t tbe_plan_destroy(tbe_plan *plan) {
+    if (!plan) return TBE_OK;
+    int32_t rc = TBE_OK;
+    if (plan->p.meta_dev && hipFree(plan->p.meta_dev) != hipSuccess) rc = TBE_ERR_HIP;
+    delete[] plan->p.meta_host;
+    delete plan;
+    return rc;
+}
+
+int32_t tbe_plan_info(const tbe_plan *plan, int64_t *total_dim, int64_t *total_rows, int32_t *key_bits) {
+    if (!plan) return TBE_ERR_NULL;
+    if (total_dim) *total_dim = plan->p.total_dim;
+    if (total_rows) *total_rows = plan->p.total_rows;
+    if (key_bits) *key_bits = plan->p.key_bits;
+    return TBE_OK;
+}
+
+int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *indices,
+                    const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+                    float *out, int32_t *status, void *stream) {
+    const tbe::Plan *p = plan_of(plan);
+    if (!p) return TBE_ERR_NULL;
+    if (num_indices < 0) return TBE_ERR_SHAPE;
+    const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
+    if (!offsets && nbags > 0) return TBE_ERR_NULL;
+    if (nbags == 0) return TBE_OK;  // empty output: nothing to write
+    if (!tables || !out) return TBE_ERR_NULL;
+    if (num_indices > 0 && !indices) return TBE_ERR_NULL;
+    if (p->bounds_check && !status) return TBE_ERR_NULL;
+    if (!aligned16(tables) || !aligned16(out)) return TBE_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(indices) & 7u) || (reinterpret_cast<uintptr_t>(offsets) & 7u) ||
+        (reinterpret_cast<uintptr_t>(per_sample_weights) & 3u))
+        return TBE_ERR_ALIGN;
+    const hipError_t e = tbe::launch_forward(*p, tables, indices, offsets, num_indices,
+                                             per_sample_weights, out, status,
+                                             static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
+int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, size_t *bytes) {
+    const tbe::Plan *p = plan_of(plan);
+    if (!p || !bytes) return TBE_ERR_NULL;
+    if (num_indices < 0 || num_indices >= (int64_t(1) << 32)) return TBE_ERR_SHAPE;
+    *bytes = tbe::backward_workspace_bytes(*p, num_indices);
+    return TBE_OK;
+}
+
+int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t *indices,
+                     const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+                     void *workspace, size_t workspace_bytes, float *grad_rows,
+                     int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
+                     int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream) {
+    const tbe::Plan *p = plan_of(plan);
+    if (!p) return TBE_ERR_NULL;
+    // lookup positions are carried as 32-bit values through the sort
+    if (num_indices < 0 || num_indices >= (int64_t(1) << 32)) return TBE_ERR_SHAPE;
+    if (grad_rows_capacity < 0) return TBE_ERR_SHAPE;
+    const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
+    if ((!offsets && nbags > 0) || !seg_offsets || !grad_row_offsets || !num_unique) return TBE_ERR_NULL;
+    if (num_indices > 0 && (!indices || !grad_idx || !grad_out)) return TBE_ERR_NULL;
+    if (grad_rows_capacity > 0 && !grad_rows) return TBE_ERR_NULL;
+    if (p->bounds_check && !status) return TBE_ERR_NULL;
+    const size_t need = tbe::backward_workspace_bytes(*p, num_indices);
+    if (workspace_bytes < need) return TBE_ERR_WORKSPACE;
+    if (need > 0 && !workspace) return TBE_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) || !aligned16(grad_rows) || !aligned16(grad_out))
+        return TBE_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(indices) & 7u) || (reinterpret_cast<uintptr_t>(offsets) & 7u) ||
+        (reinterpret_cast<uintptr_t>(grad_idx) & 7u) || (reinterpret_cast<uintptr_t>(seg_offsets) & 7u) ||
+        (reinterpret_cast<uintptr_t>(grad_row_offsets) & 7u) ||
+        (reinterpret_cast<uintptr_t>(num_unique) & 7u) ||
+        (reinterpret_cast<uintptr_t>(per_sample_weights) & 3u))
+        return TBE_ERR_ALIGN;
+    const hipError_t e = tbe::launch_backward(*p, grad_out, indices, offsets, num_indices,
+                                              per_sample_weights, workspace, workspace_bytes,
+                                              grad_rows, grad_rows_capacity, grad_idx, seg_offsets,
+                                              grad_row_offsets, num_unique, status,
+                                              static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,68 @@
+// Internal declarations shared by the library's host code and its kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tbe.h"
+
+namespace tbe {
+
+// Per-table facts the kernels need, one 48-byte record per table, uploaded
+// once per plan.  Read wave-uniformly, so they live in scalar registers.
+struct TableMeta {
+    int64_t elem_offset;  // first element of the table in the flat buffer
+    int64_t rows;         // R_t
+    int64_t row_base;     // first global row id: sum of R_t' for t' < t
+    int32_t dim;          // D_t
+    int32_t dim_off;      // first output column: sum of D_t' for t' < t
+    int32_t nvec;         // 16-byte vectors per table row: D_t * elem_size / 16
+    int32_t lpr_log2;     // log2 of lanes per row: smallest power of two >= min(nvec, 64)
+    int32_t pad[2];
+};
+static_assert(sizeof(TableMeta) == 48, "TableMeta layout");
+
+inline int elem_size(int dtype) { return dtype == TBE_F32 ? 4 : 2; }
+
+struct Plan {
+    int32_t T = 0;
+    int32_t dtype = 0;
+    int32_t bounds_check = 0;
+    int32_t key_bits = 0;      // bits of the largest global row id (>= 1)
+    int64_t B = 0;
+    int64_t total_dim = 0;
+    int64_t total_rows = 0;
+    int64_t table_elems = 0;
+    int32_t max_dim = 0;
+    int device = 0;
+    TableMeta *meta_dev = nullptr;
+    TableMeta *meta_host = nullptr;
+};
+
+// Forward: queues the pooled lookup of every (bag, table) on `stream`.
+hipError_t launch_forward(const Plan &p, const void *tables, const int64_t *indices,
+                          const int64_t *offsets, int64_t num_indices, const float *weights,
+                          float *out, int32_t *status, hipStream_t stream);
+
+// Backward: workspace size and the full sort + segmented-reduce pipeline.
+size_t backward_workspace_bytes(const Plan &p, int64_t num_indices);
+hipError_t launch_backward(const Plan &p, const float *grad_out, const int64_t *indices,
+                           const int64_t *offsets, int64_t num_indices, const float *weights,
+                           void *workspace, size_t workspace_bytes, float *grad_rows,
+                           int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
+                           int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status,
+                           hipStream_t stream);
+
+// Logical workgroup id under round-robin dispatch of workgroups over the
+// XCDs: workgroup w runs on XCD w % num_xcd, and the XCDs are given
+// contiguous ranges of logical ids, so neighbouring bags (same table) share
+// one XCD's L2.
+__device__ inline int64_t xcd_remap(int64_t w, int64_t nwg, int num_xcd) {
+    const int64_t q = nwg / num_xcd, r = nwg % num_xcd;
+    const int64_t x = w % num_xcd, local = w / num_xcd;
+    return x < r ? x * (q + 1) + local : r * (q + 1) + (x - r) * q + local;
+}
+
+constexpr int kNumXcd = 8;
+
+}  // namespace tbe

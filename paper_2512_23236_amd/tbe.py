@@ -1,0 +1,238 @@
+"""Python binding of libtbe.so (include/tbe.h): argument marshalling only.
+
+Torch tensors supply device memory and the current HIP stream; every step of
+the lookup and of its gradient runs in the library's own kernels.  There is no
+fallback: if the library is missing or was built for another ABI, loading
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtbe.so")
+ABI_VERSION = 1
+
+F32, F16, BF16 = 0, 1, 2
+DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+
+STATUS_INDEX_OOB, STATUS_OFFSETS, STATUS_CAPACITY = 1, 2, 4
+
+_lib = None
+
+
+class TBEError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        msg = _load().tbe_error_string(code).decode() if _lib is not None else str(code)
+        super().__init__(f"{where}: {msg} (code {code})")
+        self.code = code
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [
+        ("num_tables", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("batch_size", ctypes.c_int64),
+        ("rows", ctypes.c_void_p),
+        ("dims", ctypes.c_void_p),
+        ("table_offsets", ctypes.c_void_p),
+        ("table_elems", ctypes.c_int64),
+        ("bounds_check", ctypes.c_int32),
+    ]
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        lib.tbe_abi_version.restype = i32
+        lib.tbe_error_string.restype = ctypes.c_char_p
+        lib.tbe_error_string.argtypes = [i32]
+        lib.tbe_plan_create.restype = i32
+        lib.tbe_plan_create.argtypes = [ctypes.POINTER(_Desc), ctypes.POINTER(P)]
+        lib.tbe_plan_destroy.restype = i32
+        lib.tbe_plan_destroy.argtypes = [P]
+        lib.tbe_plan_info.restype = i32
+        lib.tbe_plan_info.argtypes = [P, P, P, P]
+        lib.tbe_forward.restype = i32
+        lib.tbe_forward.argtypes = [P, P, P, P, i64, P, P, P, P]
+        lib.tbe_backward_workspace_bytes.restype = i32
+        lib.tbe_backward_workspace_bytes.argtypes = [P, i64, P]
+        lib.tbe_backward.restype = i32
+        lib.tbe_backward.argtypes = [P, P, P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P, P, P]
+        if lib.tbe_abi_version() != ABI_VERSION:
+            raise ImportError(f"libtbe ABI {lib.tbe_abi_version()} != {ABI_VERSION}")
+        _lib = lib
+    return _lib
+
+
+def lib():
+    return _load()
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check(rc: int, where: str):
+    if rc != 0:
+        raise TBEError(rc, where)
+
+
+def _stream(dev: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+class Plan:
+    """A validated table layout with its per-table metadata on the device."""
+
+    def __init__(self, rows: Sequence[int], dims: Sequence[int], dtype: torch.dtype, batch_size: int,
+                 table_offsets: Optional[Sequence[int]] = None, table_elems: Optional[int] = None,
+                 bounds_check: bool = True, device=None):
+        lib_ = _load()
+        self.rows = np.ascontiguousarray(rows, dtype=np.int64)
+        self.dims = np.ascontiguousarray(dims, dtype=np.int32)
+        self.T = int(self.rows.size)
+        self.B = int(batch_size)
+        self.dtype = dtype
+        self.bounds_check = bool(bounds_check)
+        self.table_offsets = None if table_offsets is None else np.ascontiguousarray(table_offsets, dtype=np.int64)
+        if table_elems is None:
+            table_elems = int((self.rows * self.dims.astype(np.int64)).sum())
+        self.table_elems = int(table_elems)
+        if dtype not in DTYPE_CODE:
+            raise TBEError(-3, "Plan")
+        d = _Desc(self.T, DTYPE_CODE[dtype], self.B, self.rows.ctypes.data, self.dims.ctypes.data,
+                  None if self.table_offsets is None else self.table_offsets.ctypes.data,
+                  self.table_elems, int(self.bounds_check))
+        self.device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+        self._h = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(lib_.tbe_plan_create(ctypes.byref(d), ctypes.byref(self._h)), "tbe_plan_create")
+        td, tr, kb = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int32()
+        _check(lib_.tbe_plan_info(self._h, ctypes.byref(td), ctypes.byref(tr), ctypes.byref(kb)), "tbe_plan_info")
+        self.total_dim, self.total_rows, self.key_bits = td.value, tr.value, kb.value
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            _check(_load().tbe_plan_destroy(self._h), "tbe_plan_destroy")
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _dev_tensor(t: torch.Tensor, dtype, name: str, plan: Plan):
+    if t.device != plan.device:
+        raise ValueError(f"{name} is on {t.device}, the plan is on {plan.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def forward(plan: Plan, tables: torch.Tensor, indices: torch.Tensor, offsets: torch.Tensor,
+            per_sample_weights: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+            status: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Pooled lookup: returns out [B, total_dim] fp32 (written on the current stream)."""
+    _dev_tensor(tables, plan.dtype, "tables", plan)
+    _dev_tensor(indices, torch.int64, "indices", plan)
+    _dev_tensor(offsets, torch.int64, "offsets", plan)
+    if offsets.numel() != plan.T * plan.B + 1:
+        raise ValueError(f"offsets has {offsets.numel()} entries, expected T*B+1 = {plan.T * plan.B + 1}")
+    if per_sample_weights is not None:
+        _dev_tensor(per_sample_weights, torch.float32, "per_sample_weights", plan)
+        if per_sample_weights.numel() != indices.numel():
+            raise ValueError("per_sample_weights must have one weight per index")
+    if out is None:
+        out = torch.empty((plan.B, plan.total_dim), dtype=torch.float32, device=plan.device)
+    _dev_tensor(out, torch.float32, "out", plan)
+    if out.numel() != plan.B * plan.total_dim:
+        raise ValueError("out must be [B, total_dim]")
+    if status is not None:
+        _dev_tensor(status, torch.int32, "status", plan)
+    rc = _load().tbe_forward(plan.handle, _ptr(tables), _ptr(indices), _ptr(offsets), indices.numel(),
+                             _ptr(per_sample_weights), _ptr(out), _ptr(status), _stream(plan.device))
+    _check(rc, "tbe_forward")
+    return out
+
+
+def backward_workspace_bytes(plan: Plan, num_indices: int) -> int:
+    n = ctypes.c_size_t()
+    _check(_load().tbe_backward_workspace_bytes(plan.handle, int(num_indices), ctypes.byref(n)),
+           "tbe_backward_workspace_bytes")
+    return n.value
+
+
+class SparseGrad:
+    """Result of backward(): the first num_unique() entries are meaningful."""
+
+    def __init__(self, grad_rows, grad_idx, seg_offsets, grad_row_offsets, num_unique_dev):
+        self.grad_rows = grad_rows
+        self.grad_idx = grad_idx
+        self.seg_offsets = seg_offsets
+        self.grad_row_offsets = grad_row_offsets
+        self.num_unique_dev = num_unique_dev
+
+    def num_unique(self) -> int:
+        return int(self.num_unique_dev.item())
+
+    def trimmed(self):
+        """Host copies trimmed to U: (grad_idx, seg_offsets, grad_row_offsets, grad_rows)."""
+        U = self.num_unique()
+        gro = self.grad_row_offsets[: U + 1].cpu()
+        return (self.grad_idx[:U].cpu(), self.seg_offsets[: U + 1].cpu(), gro,
+                self.grad_rows[: int(gro[-1])].cpu())
+
+
+def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets: torch.Tensor,
+             per_sample_weights: Optional[torch.Tensor] = None, grad_rows_capacity: Optional[int] = None,
+             workspace: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
+             outputs: Optional[SparseGrad] = None) -> SparseGrad:
+    """Sparse gradient of the tables (queued on the current stream)."""
+    N = indices.numel()
+    _dev_tensor(grad_out, torch.float32, "grad_out", plan)
+    _dev_tensor(indices, torch.int64, "indices", plan)
+    _dev_tensor(offsets, torch.int64, "offsets", plan)
+    if grad_out.numel() != plan.B * plan.total_dim:
+        raise ValueError("grad_out must be [B, total_dim]")
+    if offsets.numel() != plan.T * plan.B + 1:
+        raise ValueError("offsets must have T*B+1 entries")
+    if per_sample_weights is not None:
+        _dev_tensor(per_sample_weights, torch.float32, "per_sample_weights", plan)
+    dev = plan.device
+    if outputs is None:
+        if grad_rows_capacity is None:
+            grad_rows_capacity = N * int(plan.dims.max()) if N else 0
+        outputs = SparseGrad(
+            torch.empty(max(grad_rows_capacity, 1), dtype=torch.float32, device=dev),
+            torch.empty(max(N, 1), dtype=torch.int64, device=dev),
+            torch.empty(N + 1, dtype=torch.int64, device=dev),
+            torch.empty(N + 1, dtype=torch.int64, device=dev),
+            torch.zeros(1, dtype=torch.int64, device=dev))
+    cap = outputs.grad_rows.numel() if grad_rows_capacity is None else int(grad_rows_capacity)
+    need = backward_workspace_bytes(plan, N)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = _load().tbe_backward(plan.handle, _ptr(grad_out), _ptr(indices), _ptr(offsets), N,
+                              _ptr(per_sample_weights), _ptr(workspace), workspace.numel(),
+                              _ptr(outputs.grad_rows), cap, _ptr(outputs.grad_idx), _ptr(outputs.seg_offsets),
+                              _ptr(outputs.grad_row_offsets), _ptr(outputs.num_unique_dev), _ptr(status),
+                              _stream(dev))
+    _check(rc, "tbe_backward")
+    return outputs

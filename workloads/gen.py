@@ -325,7 +325,8 @@ def _indices_at(spec: Spec, t: int, j: torch.Tensor) -> torch.Tensor:
         return (_bits(h, 32, 32) * R) >> 32
     alpha = float(spec.index_dist[1])
     cum = _zipf_prefix(alpha, R)
-    cum_t = _on(cum, j.device, ("zipf", alpha))
+    full = _ZIPF_CACHE[alpha]
+    cum_t = _on(full, j.device, ("zipf", alpha))[:R]
     target = _u53(h) * float(cum[R - 1])
     rank0 = torch.searchsorted(cum_t, target, right=True).clamp_(max=R - 1)
     a, c = _affine_perm(spec, t)
@@ -337,6 +338,8 @@ def gen_indices(spec: Spec, offsets: torch.Tensor) -> torch.Tensor:
     N = int(offsets[-1])
     dev = offsets.device
     out = torch.empty(N, dtype=torch.int64, device=dev)
+    if spec.B == 0 or N == 0:
+        return out
     bounds = offsets[:: spec.B].cpu().tolist()  # start of each table's lookups, plus N
     for t in range(spec.T):
         s, e = int(bounds[t]), int(bounds[t + 1])
