@@ -57,6 +57,13 @@ def forward_bytes(spec, offsets_host: np.ndarray) -> int:
     return rows + idx + bags
 
 
+def backward_bytes(spec, N: int, U: int, grad_floats: int) -> int:
+    """Compulsory bytes of one backward: int64 indices and offsets read, the
+    fp32 output gradient read once, int64 row ids, segment offsets and row
+    offsets written, and the fp32 gradient rows written."""
+    return 8 * N + 8 * (spec.T * spec.B + 1) + 4 * spec.B * spec.total_dim + 3 * 8 * (U + 1) + 4 * grad_floats
+
+
 def cpu_baseline(spec, d, target_s: float):
     """The CPU oracle on a bounded sample: the first b_s bags of every table,
     their rows copied into compact host tables; b_s is sized so the oracle
@@ -108,7 +115,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -130,6 +137,18 @@ def main():
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     out = torch.empty((spec.B, plan.total_dim), dtype=torch.float32, device=dev)
     training = spec.grad
+    grads = None
+    if training:
+        N = d["N"]
+        bounds = d["offsets"][:: spec.B].cpu().numpy()
+        cap = int((np.diff(bounds) * spec.dims.astype(np.int64)).sum())
+        grads = tbe.SparseGrad(torch.empty(cap, dtype=torch.float32, device=dev),
+                               torch.empty(N, dtype=torch.int64, device=dev),
+                               torch.empty(N + 1, dtype=torch.int64, device=dev),
+                               torch.empty(N + 1, dtype=torch.int64, device=dev),
+                               torch.zeros(1, dtype=torch.int64, device=dev))
+        workspace = torch.empty(tbe.backward_workspace_bytes(plan, N), dtype=torch.uint8, device=dev)
+        log(f"[bench] backward workspace {workspace.numel() / 1e9:.2f} GB, grad_rows capacity {cap / 2.5e8:.2f} GB")
 
     def step(ev=None):
         if ev is not None:
@@ -137,6 +156,11 @@ def main():
         tbe.forward(plan, d["tables"], d["indices"], d["offsets"], d["weights"], out=out, status=status)
         if ev is not None:
             ev[1].record()
+        if training:
+            tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], d["weights"], workspace=workspace,
+                         status=status, outputs=grads)
+            if ev is not None:
+                ev[2].record()
 
     for _ in range(args.warmup):
         step()
@@ -144,15 +168,16 @@ def main():
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())}")
 
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    fwd_ms = [a.elapsed_time(b) for a, b in evs]
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
     fwd_avg = float(np.mean(fwd_ms))
+    bwd_ms = [e[1].elapsed_time(e[2]) for e in evs] if training else None
     ms_per_step = wall * 1e3 / args.steps
     N = d["N"]
     off_host = d["offsets"].cpu().numpy()
@@ -182,6 +207,18 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "forward_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
     }
+    if training:
+        bwd_avg = float(np.mean(bwd_ms))
+        U = grads.num_unique()
+        gro_total = int(grads.grad_row_offsets[U].item())
+        bbytes = backward_bytes(spec, N, U, gro_total)
+        res["backward"] = {"ms": bwd_avg, "ms_p10": float(np.percentile(bwd_ms, 10)),
+                           "ms_p90": float(np.percentile(bwd_ms, 90)), "lookups_per_s": N / (bwd_avg * 1e-3),
+                           "unique_rows": U, "compulsory_bytes": bbytes,
+                           "effective_GBps": bbytes / (bwd_avg * 1e-3) / 1e9,
+                           "frac_of_hbm_peak": bbytes / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    if int(status.item()) != 0:
+        raise RuntimeError(f"device status {int(status.item())}")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
         res["cpu_baseline"] = cpu_baseline(spec, d, args.cpu_seconds)

@@ -1,15 +1,930 @@
-// Sparse-gradient backward (sort + segmented reduce).  Placeholder until the
-// kernels land: reports that the operation is not available.
+// Sparse (row-wise) gradient of the pooled embedding-bag lookup for gfx950.
+//
+// For every distinct row g = row_base[t] + idx that was looked up, in
+// ascending order, the gradient row is the sum, over the lookups j of g in
+// lookup order, of w_j * grad_out[b(j), dim_off[t] : dim_off[t] + D_t].
+//
+// Pipeline (all on the caller's stream, no host synchronisation):
+//   setup     per-table lookup ranges [offsets[tB], offsets[(t+1)B]) and the
+//             tiling of each range into tiles of kTile positions.
+//   keys      one wave per bag writes key_j = idx_j (32-bit, local to the
+//             table) and val_j = b(j) (plus the weight when weighted).  A
+//             table's lookups already occupy exactly the positions its rows
+//             take in the global order, so sorting every table's range by
+//             its local key yields the global stable sort.
+//   radix     stable LSD radix sort of each range, 8-bit digits, over the
+//             bits of the largest table: per pass a tile histogram, one
+//             device-wide exclusive scan (table-major, digit-major, tile-
+//             minor, so scanned counts are final positions), and a stable
+//             scatter that ranks keys with wave ballots and stages the tile
+//             in LDS so global writes run in digit order.
+//   segments  per tile: segment starts (key change) and kept lookups; one
+//             scan over tiles; then grad_idx / seg_offsets /
+//             grad_row_offsets are written for every segment start.
+//   reduce    sorted positions are cut into fixed blocks of kBlk; a lane
+//             group walks one block in order, accumulating fp32 rows of
+//             grad_out; a segment that lies inside the block is written
+//             straight to its gradient row (its only writer); a segment
+//             cut by a block edge leaves a head / tail piece.
+//   combine   each segment that crosses block edges is summed from its
+//             pieces in a fixed pairwise order and written once.
+// Every output has one writer and a fixed summation order, so the result is
+// bitwise reproducible.  Lookups whose index fails the bounds check are
+// keyed past every valid key of their table and dropped.
+
 #include "tbe_internal.h"
 
 namespace tbe {
+namespace {
 
-size_t backward_workspace_bytes(const Plan &, int64_t) { return 0; }
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kItems = 16;
+constexpr int kTile = kThreads * kItems;      // positions per tile
+constexpr int kBlk = 128;                     // positions per reduce block
+constexpr int kBlksPerTile = kTile / kBlk;    // 32
+constexpr int kRadixBits = 8;
+constexpr int kBuckets = 1 << kRadixBits;
+constexpr uint32_t kSentinel = 0xffffffffu;
+constexpr int kPairLevels = 12;               // pairwise-sum depth in combine
 
-hipError_t launch_backward(const Plan &, const float *, const int64_t *, const int64_t *, int64_t,
-                           const float *, void *, size_t, float *, int64_t, int64_t *, int64_t *,
-                           int64_t *, int64_t *, int32_t *, hipStream_t) {
-    return hipErrorNotSupported;
+// Device control block at the start of the workspace.
+struct Ctl {
+    int32_t abort;       // malformed offsets seen (bounds check on): stop
+    int32_t skip_rows;   // grad_rows too small: write no gradient row
+    int64_t total_tiles;
+    int64_t pad[6];
+};
+
+// Per-table lookup range in the sorted order and its first tile.
+struct Range {
+    int64_t start, end, tile_base, pad;
+};
+
+struct TileSeg {
+    uint64_t starts, kept, dimsum, pad;
+};
+
+// ------------------------------------------------------------------ utils
+
+__device__ inline uint64_t lanemask_lt() {
+    const int lane = threadIdx.x & 63;
+    return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+__device__ inline uint32_t wave_incl_scan(uint32_t v) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t o = __shfl_up(v, d);
+        if (lane >= d) v += o;
+    }
+    return v;
+}
+
+__device__ inline uint64_t wave_incl_scan64(uint64_t v) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint64_t o = __shfl_up(v, d);
+        if (lane >= d) v += o;
+    }
+    return v;
+}
+
+// Exclusive scan of one value per thread over the block; returns the block
+// total through *total.  `lds` holds kWaves entries.
+template <typename T>
+__device__ inline T block_excl_scan(T v, T *lds, T *total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    T inc;
+    if constexpr (sizeof(T) == 8) inc = wave_incl_scan64(v); else inc = wave_incl_scan(v);
+    if (lane == 63) lds[wave] = inc;
+    __syncthreads();
+    T before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const T s = lds[w];
+        if (w < wave) before += s;
+        all += s;
+    }
+    __syncthreads();
+    *total = all;
+    return before + inc - v;
+}
+
+// Table owning tile `tile`: the t with ranges[t].tile_base <= tile < ranges[t+1].tile_base.
+__device__ inline int find_table(const Range *__restrict__ r, int T, int64_t tile) {
+    int lo = 0, hi = T;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (r[mid].tile_base <= tile) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+struct TileInfo {
+    int t;
+    int64_t local, ntiles, p_lo, p_hi, start, end;
+};
+
+__device__ inline bool tile_info(const Range *__restrict__ ranges, int T, int64_t tile, TileInfo &ti) {
+    ti.t = find_table(ranges, T, tile);
+    const Range r = ranges[ti.t];
+    ti.start = r.start;
+    ti.end = r.end;
+    ti.local = tile - r.tile_base;
+    ti.ntiles = ranges[ti.t + 1].tile_base - r.tile_base;
+    ti.p_lo = r.start + ti.local * kTile;
+    ti.p_hi = ti.p_lo + kTile < r.end ? ti.p_lo + kTile : r.end;
+    return ti.p_lo < ti.p_hi;
+}
+
+__device__ inline uint32_t digit_of(uint32_t key, int shift, uint32_t mask) { return (key >> shift) & mask; }
+
+// Lanes of the wave (among `valid`) holding the same digit as this lane.
+__device__ inline uint64_t match_digit(uint32_t d, bool valid, int nbits) {
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t m = __ballot(valid && bit);
+        peers &= bit ? m : ~m;
+    }
+    return valid ? peers : 0ull;
+}
+
+// ------------------------------------------------------------------ setup
+
+__global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restrict__ offsets, int T, int64_t B,
+                                                         int64_t N, int check, Ctl *ctl, Range *ranges,
+                                                         int32_t *status, int64_t *num_unique,
+                                                         int64_t *seg_offsets, int64_t *grad_row_offsets) {
+    __shared__ int64_t lds[kWaves];
+    const int tid = threadIdx.x;
+    __shared__ int bad;
+    if (tid == 0) {
+        bad = 0;
+        if (check && (offsets[0] != 0 || offsets[static_cast<int64_t>(T) * B] != N)) bad = 1;
+        *num_unique = 0;
+        seg_offsets[0] = 0;
+        grad_row_offsets[0] = 0;
+    }
+    __syncthreads();
+    int64_t carry = 0;
+    for (int base = 0; base < T; base += kThreads) {
+        const int t = base + tid;
+        int64_t s = 0, e = 0, nt = 0;
+        if (t < T) {
+            s = offsets[static_cast<int64_t>(t) * B];
+            e = offsets[static_cast<int64_t>(t + 1) * B];
+            if (check && (s < 0 || e < s || e > N)) {
+                bad = 1;
+                s = e = 0;
+            }
+            nt = (e - s + kTile - 1) / kTile;
+        }
+        int64_t tot;
+        const int64_t ex = block_excl_scan<int64_t>(nt, lds, &tot);
+        if (t < T) ranges[t] = Range{s, e, carry + ex, 0};
+        carry += tot;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        ranges[T] = Range{N, N, carry, 0};
+        ctl->abort = bad;
+        ctl->skip_rows = 0;
+        ctl->total_tiles = bad ? 0 : carry;
+        if (bad) atomicOr(status, TBE_STATUS_OFFSETS);
+    }
+}
+
+// ------------------------------------------------------------------- keys
+
+template <typename V>
+__global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restrict__ meta,
+                                                        const int64_t *__restrict__ indices,
+                                                        const int64_t *__restrict__ offsets,
+                                                        const float *__restrict__ weights,
+                                                        const Range *__restrict__ ranges, int64_t B,
+                                                        int64_t nbags, int check, Ctl *ctl,
+                                                        uint32_t *__restrict__ keys, V *__restrict__ vals,
+                                                        int32_t *status) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t k = (static_cast<int64_t>(blockIdx.x) * kWaves) + wave;
+    if (k >= nbags || ctl->abort) return;
+    const int64_t t = k / B, b = k - t * B;
+    const int64_t R = meta[t].rows;
+    int64_t s = offsets[k], e = offsets[k + 1];
+    if (check) {
+        const Range r = ranges[t];
+        if (s < r.start || e < s || e > r.end) {
+            if (lane == 0) {
+                atomicOr(status, TBE_STATUS_OFFSETS);
+                atomicOr(&ctl->abort, 1);
+            }
+            return;
+        }
+    }
+    for (int64_t j = s + lane; j < e; j += 64) {
+        const int64_t idx = __builtin_nontemporal_load(indices + j);
+        uint32_t key = static_cast<uint32_t>(idx);
+        if (check && (idx < 0 || idx >= R)) {
+            key = kSentinel;
+            atomicOr(status, TBE_STATUS_INDEX_OOB);
+        }
+        keys[j] = key;
+        if constexpr (sizeof(V) == 8) {
+            const float w = weights[j];
+            vals[j] = static_cast<uint64_t>(b) | (static_cast<uint64_t>(__float_as_uint(w)) << 32);
+        } else {
+            vals[j] = static_cast<uint32_t>(b);
+        }
+    }
+}
+
+// ------------------------------------------------------------ radix sort
+
+__global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__restrict__ keys,
+                                                              const Range *__restrict__ ranges, int T,
+                                                              const Ctl *__restrict__ ctl, int shift, int nbits,
+                                                              uint32_t *__restrict__ hist) {
+    __shared__ uint32_t cnt[kBuckets];
+    const int64_t tile = blockIdx.x;
+    if (tile >= ctl->total_tiles || ctl->abort) return;
+    TileInfo ti;
+    if (!tile_info(ranges, T, tile, ti)) return;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    cnt[tid] = 0;
+    __syncthreads();
+    const uint32_t mask = (1u << nbits) - 1u;
+    const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
+#pragma unroll 4
+    for (int r = 0; r < kItems; ++r) {
+        const int64_t pos = wbase + r * 64 + lane;
+        const bool valid = pos < ti.p_hi;
+        const uint32_t d = valid ? digit_of(keys[pos], shift, mask) : 0u;
+        const uint64_t peers = match_digit(d, valid, nbits);
+        if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&cnt[d], static_cast<uint32_t>(__popcll(peers)));
+    }
+    __syncthreads();
+    // layout: table-major, digit-major, tile-minor
+    const int64_t base = ranges[ti.t].tile_base * kBuckets;
+    hist[base + static_cast<int64_t>(tid) * ti.ntiles + ti.local] = cnt[tid];
+}
+
+// Exclusive scan over `count` u32 values in place: chunk sums, a one-block
+// scan of the sums, then each chunk rescanned with its offset.
+constexpr int kScanChunk = kThreads * kItems;
+
+__device__ inline int64_t hist_count(const Ctl *ctl) { return ctl->total_tiles * kBuckets; }
+
+__global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const uint32_t *__restrict__ data,
+                                                               uint32_t *__restrict__ sums,
+                                                               const Ctl *__restrict__ ctl) {
+    __shared__ uint32_t lds[kWaves];
+    const int64_t count = hist_count(ctl);
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanChunk;
+    if (base >= count) return;
+    uint32_t s = 0;
+    for (int i = threadIdx.x; i < kScanChunk; i += kThreads)
+        if (base + i < count) s += data[base + i];
+    uint32_t tot;
+    block_excl_scan<uint32_t>(s, lds, &tot);
+    if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(kThreads) void scan_top_kernel(uint32_t *__restrict__ sums,
+                                                            const Ctl *__restrict__ ctl) {
+    __shared__ uint32_t lds[kWaves];
+    const int64_t n = (hist_count(ctl) + kScanChunk - 1) / kScanChunk;
+    uint32_t carry = 0;
+    for (int64_t base = 0; base < n; base += kThreads) {
+        const int64_t i = base + threadIdx.x;
+        const uint32_t v = i < n ? sums[i] : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_excl_scan<uint32_t>(v, lds, &tot);
+        if (i < n) sums[i] = carry + ex;
+        carry += tot;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void scan_down_kernel(uint32_t *__restrict__ data,
+                                                             const uint32_t *__restrict__ sums,
+                                                             const Ctl *__restrict__ ctl) {
+    __shared__ uint32_t lds[kWaves];
+    const int64_t count = hist_count(ctl);
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanChunk;
+    if (base >= count) return;
+    // blocked: thread i owns items [i*kItems, (i+1)*kItems) of the chunk
+    uint32_t v[kItems];
+    uint32_t s = 0;
+    const int64_t my = base + static_cast<int64_t>(threadIdx.x) * kItems;
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) {
+        v[q] = my + q < count ? data[my + q] : 0u;
+        s += v[q];
+    }
+    uint32_t tot;
+    uint32_t run = sums[blockIdx.x] + block_excl_scan<uint32_t>(s, lds, &tot);
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) {
+        if (my + q < count) data[my + q] = run;
+        run += v[q];
+    }
+}
+
+template <typename V>
+__global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
+    const uint32_t *__restrict__ keys_in, const V *__restrict__ vals_in, uint32_t *__restrict__ keys_out,
+    V *__restrict__ vals_out, const uint32_t *__restrict__ scanned, const Range *__restrict__ ranges, int T,
+    const Ctl *__restrict__ ctl, int shift, int nbits) {
+    __shared__ uint32_t cnt[kWaves][kBuckets];  // per-wave digit counts, then wave offsets
+    __shared__ uint32_t tstart[kBuckets];       // first tile-local slot of each digit
+    __shared__ uint32_t goff[kBuckets];         // first global slot of each digit for this tile
+    __shared__ uint32_t sk[kTile];
+    __shared__ V sv[kTile];
+    __shared__ uint32_t lds[kWaves];
+
+    const int64_t tile = blockIdx.x;
+    if (tile >= ctl->total_tiles || ctl->abort) return;
+    TileInfo ti;
+    if (!tile_info(ranges, T, tile, ti)) return;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t mask = (1u << nbits) - 1u;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) cnt[w][tid] = 0;
+    __syncthreads();
+
+    // Wave w ranks positions [p_lo + w*1024, +1024) in order, 64 per round.
+    const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
+    uint32_t key[kItems], rank[kItems];
+    V val[kItems];
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+        const int64_t pos = wbase + r * 64 + lane;
+        const bool valid = pos < ti.p_hi;
+        key[r] = valid ? keys_in[pos] : 0u;
+        val[r] = valid ? vals_in[pos] : V(0);
+    }
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+        const int64_t pos = wbase + r * 64 + lane;
+        const bool valid = pos < ti.p_hi;
+        const uint32_t d = digit_of(key[r], shift, mask);
+        const uint64_t peers = match_digit(d, valid, nbits);
+        const uint32_t before = static_cast<uint32_t>(__popcll(peers & lanemask_lt()));
+        uint32_t base = 0;
+        if (valid) base = cnt[wave][d];
+        rank[r] = base + before;
+        if (valid && before == 0) cnt[wave][d] = base + static_cast<uint32_t>(__popcll(peers));
+    }
+    __syncthreads();
+    {
+        const int d = tid;
+        uint32_t run = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const uint32_t c = cnt[w][d];
+            cnt[w][d] = run;
+            run += c;
+        }
+        uint32_t tot;
+        tstart[d] = block_excl_scan<uint32_t>(run, lds, &tot);
+        goff[d] = scanned[ranges[ti.t].tile_base * kBuckets + static_cast<int64_t>(d) * ti.ntiles + ti.local];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+        const int64_t pos = wbase + r * 64 + lane;
+        if (pos < ti.p_hi) {
+            const uint32_t d = digit_of(key[r], shift, mask);
+            const uint32_t slot = tstart[d] + cnt[wave][d] + rank[r];
+            sk[slot] = key[r];
+            sv[slot] = val[r];
+        }
+    }
+    __syncthreads();
+    const int n = static_cast<int>(ti.p_hi - ti.p_lo);
+    for (int i = tid; i < n; i += kThreads) {
+        const uint32_t k = sk[i];
+        const uint32_t d = digit_of(k, shift, mask);
+        const int64_t dst = static_cast<int64_t>(goff[d]) + (i - static_cast<int64_t>(tstart[d]));
+        keys_out[dst] = k;
+        vals_out[dst] = sv[i];
+    }
+}
+
+// --------------------------------------------------------------- segments
+
+// Flags of sorted position pos (inside table range [start, end)).
+__device__ inline void seg_flags(const uint32_t *__restrict__ keys, int64_t pos, int64_t start, uint32_t key,
+                                 bool &kept, bool &is_start) {
+    kept = key != kSentinel;
+    is_start = kept && (pos == start || keys[pos - 1] != key);
+}
+
+__global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t *__restrict__ keys,
+                                                             const TableMeta *__restrict__ meta,
+                                                             const Range *__restrict__ ranges, int T,
+                                                             const Ctl *__restrict__ ctl,
+                                                             TileSeg *__restrict__ tseg) {
+    __shared__ uint32_t lds[kWaves];
+    const int64_t tile = blockIdx.x;
+    if (tile >= ctl->total_tiles || ctl->abort) return;
+    TileInfo ti;
+    if (!tile_info(ranges, T, tile, ti)) return;
+    uint32_t ns = 0, nk = 0;
+    for (int64_t pos = ti.p_lo + threadIdx.x; pos < ti.p_hi; pos += kThreads) {
+        bool kept, st;
+        seg_flags(keys, pos, ti.start, keys[pos], kept, st);
+        ns += st;
+        nk += kept;
+    }
+    uint32_t ts, tk;
+    block_excl_scan<uint32_t>(ns, lds, &ts);
+    block_excl_scan<uint32_t>(nk, lds, &tk);
+    if (threadIdx.x == 0)
+        tseg[tile] = TileSeg{ts, tk, static_cast<uint64_t>(ts) * static_cast<uint64_t>(meta[ti.t].dim), 0};
+}
+
+__global__ __launch_bounds__(kThreads) void seg_scan_kernel(TileSeg *__restrict__ tseg, Ctl *ctl,
+                                                            int64_t *__restrict__ num_unique,
+                                                            int64_t *__restrict__ seg_offsets,
+                                                            int64_t *__restrict__ grad_row_offsets,
+                                                            int64_t capacity, int32_t *status) {
+    __shared__ uint64_t lds[kWaves];
+    if (ctl->abort) return;
+    const int64_t n = ctl->total_tiles;
+    uint64_t cs = 0, ck = 0, cd = 0;
+    for (int64_t base = 0; base < n; base += kThreads) {
+        const int64_t i = base + threadIdx.x;
+        TileSeg v{0, 0, 0, 0};
+        if (i < n) v = tseg[i];
+        uint64_t ts, tk, td;
+        const uint64_t es = block_excl_scan<uint64_t>(v.starts, lds, &ts);
+        const uint64_t ek = block_excl_scan<uint64_t>(v.kept, lds, &tk);
+        const uint64_t ed = block_excl_scan<uint64_t>(v.dimsum, lds, &td);
+        if (i < n) tseg[i] = TileSeg{cs + es, ck + ek, cd + ed, 0};
+        cs += ts;
+        ck += tk;
+        cd += td;
+    }
+    if (threadIdx.x == 0) {
+        *num_unique = static_cast<int64_t>(cs);
+        seg_offsets[cs] = static_cast<int64_t>(ck);
+        grad_row_offsets[cs] = static_cast<int64_t>(cd);
+        if (static_cast<int64_t>(cd) > capacity) {
+            ctl->skip_rows = 1;
+            atomicOr(status, TBE_STATUS_CAPACITY);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void seg_write_kernel(const uint32_t *__restrict__ keys,
+                                                             const TableMeta *__restrict__ meta,
+                                                             const Range *__restrict__ ranges, int T,
+                                                             const Ctl *__restrict__ ctl,
+                                                             const TileSeg *__restrict__ tseg,
+                                                             int64_t *__restrict__ grad_idx,
+                                                             int64_t *__restrict__ seg_offsets,
+                                                             int64_t *__restrict__ grad_row_offsets) {
+    __shared__ uint32_t lds[kWaves];
+    const int64_t tile = blockIdx.x;
+    if (tile >= ctl->total_tiles || ctl->abort) return;
+    TileInfo ti;
+    if (!tile_info(ranges, T, tile, ti)) return;
+    const TileSeg pre = tseg[tile];
+    const TableMeta m = meta[ti.t];
+    // blocked: thread i owns positions p_lo + i*kItems .. +kItems
+    const int64_t my = ti.p_lo + static_cast<int64_t>(threadIdx.x) * kItems;
+    uint32_t k[kItems];
+    uint32_t ns = 0, nk = 0;
+    uint32_t fl = 0;  // bit 2q: kept, bit 2q+1: start
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) {
+        const int64_t pos = my + q;
+        bool kept = false, st = false;
+        if (pos < ti.p_hi) {
+            k[q] = keys[pos];
+            seg_flags(keys, pos, ti.start, k[q], kept, st);
+        }
+        fl |= (kept ? 1u : 0u) << (2 * q);
+        fl |= (st ? 1u : 0u) << (2 * q + 1);
+        ns += st;
+        nk += kept;
+    }
+    uint32_t ts, tk;
+    uint32_t rs = block_excl_scan<uint32_t>(ns, lds, &ts);
+    uint32_t rk = block_excl_scan<uint32_t>(nk, lds, &tk);
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) {
+        if ((fl >> (2 * q + 1)) & 1u) {
+            const int64_t u = static_cast<int64_t>(pre.starts) + rs;
+            grad_idx[u] = m.row_base + static_cast<int64_t>(k[q]);
+            seg_offsets[u] = static_cast<int64_t>(pre.kept) + rk;
+            grad_row_offsets[u] = static_cast<int64_t>(pre.dimsum) + static_cast<int64_t>(rs) * m.dim;
+            ++rs;
+        }
+        rk += (fl >> (2 * q)) & 1u;
+    }
+}
+
+// ----------------------------------------------------------------- reduce
+//
+// Sorted positions are cut into blocks of kBlk.  A segment of at most kBlk
+// lookups ("short") is summed whole, in order, by the lane group of the block
+// holding its first lookup, and written once to its gradient row.  A longer
+// segment is summed piecewise: each block it touches sums its share (a head
+// piece when the segment began earlier, a tail piece in the block where it
+// begins) and the combine kernel adds the pieces.  Short and long are told
+// apart by the segment's length, the same test wherever it is made.
+
+template <typename V>
+__device__ inline void val_split(V v, uint32_t &b, float &w) {
+    if constexpr (sizeof(V) == 8) {
+        b = static_cast<uint32_t>(v);
+        w = __uint_as_float(static_cast<uint32_t>(v >> 32));
+    } else {
+        b = v;
+        w = 1.0f;
+    }
+}
+
+__device__ inline void store4(float *p, const float4 &a) { *reinterpret_cast<float4 *>(p) = a; }
+
+constexpr uint32_t kTopBit = 0x80000000u;
+
+template <typename V, int LPR>
+__device__ inline void reduce_tile(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
+                                   const float *__restrict__ grad_out, const int64_t *__restrict__ seg_offsets,
+                                   const TableMeta &m, const TileInfo &ti, const TileSeg &pre,
+                                   const uint32_t *blk_starts, int64_t total_dim, float *__restrict__ grad_rows,
+                                   float *__restrict__ partials, int max_dim, int32_t *__restrict__ head_seg,
+                                   int32_t *__restrict__ tail_seg, int64_t tile) {
+    constexpr int G = 64 / LPR;
+    constexpr int U = LPR < 8 ? LPR : 8;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane / LPR, v = lane % LPR;
+    const int nsub = kWaves * G;
+    const int sub = wave * G + g;
+    const int nvec = m.dim / 4;  // 16-byte fp32 vectors per gradient row
+    const uint64_t gmask = (LPR == 64 ? ~0ull : ((1ull << LPR) - 1)) << (g * LPR);
+    const uint64_t le_mask = lanemask_lt() | (1ull << lane);
+
+    for (int q = sub; q < kBlksPerTile; q += nsub) {
+        const int64_t p0 = ti.p_lo + static_cast<int64_t>(q) * kBlk;
+        const int64_t gq = tile * kBlksPerTile + q;
+        int32_t hs = -1, tsg = -1;
+        if (p0 < ti.p_hi) {
+            const int64_t p1 = p0 + kBlk < ti.p_hi ? p0 + kBlk : ti.p_hi;
+            const uint32_t u_before = static_cast<uint32_t>(pre.starts) + blk_starts[q];
+            const uint32_t nsb = blk_starts[q + 1] - blk_starts[q];
+            // long = more than kBlk lookups; the head segment (begun before p0)
+            // and the last segment begun in this block are the only candidates
+            bool head_long = false, cross_long = false;
+            const uint32_t cross_u = u_before + nsb - 1;
+            if (u_before > 0) {
+                const int64_t a = seg_offsets[u_before - 1], b = seg_offsets[u_before];
+                head_long = b - a > kBlk;
+            }
+            if (nsb > 0) {
+                const int64_t a = seg_offsets[cross_u], b = seg_offsets[cross_u + 1];
+                cross_long = b - a > kBlk;
+            }
+            const int64_t lim = p1 + kBlk < ti.end ? p1 + kBlk : ti.end;
+            for (int c0 = 0; c0 < nvec; c0 += LPR) {  // column chunks of 64 vectors (one for D <= 256)
+                const bool vact = c0 + v < nvec;
+                const float *gcol = grad_out + m.dim_off + static_cast<int64_t>(c0 + v) * 4;
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                uint32_t run = u_before;  // segment starts before the current chunk
+                for (int64_t c = p0; c < lim; c += LPR) {
+                    // lane v of the group describes position c + v
+                    const int64_t pos = c + v;
+                    uint32_t key = kSentinel, bb = 0;
+                    float ww = 0.f;
+                    bool st = false, last = false;
+                    if (pos < lim) {
+                        key = keys[pos];
+                        if (key != kSentinel) {
+                            st = pos == ti.start || keys[pos - 1] != key;
+                            last = pos + 1 >= ti.end || keys[pos + 1] != key;
+                        }
+                        val_split<V>(vals[pos], bb, ww);
+                    }
+                    const uint64_t smask = __ballot(st) & gmask;
+                    const uint32_t useg = run + static_cast<uint32_t>(__popcll(smask & le_mask)) - 1u;
+                    run += static_cast<uint32_t>(__popcll(smask));
+                    bool proc = false;
+                    if (key != kSentinel && pos < lim) {
+                        if (useg < u_before) proc = pos < p1 && head_long;
+                        else if (useg < u_before + nsb) proc = pos < p1 || !(useg == cross_u && cross_long);
+                    }
+                    bool flush = false;
+                    if (proc) flush = last || (pos == p1 - 1 && (useg < u_before || (useg == cross_u && cross_long)));
+                    const uint32_t pb = bb | (proc ? kTopBit : 0u);
+                    const uint32_t pu = useg | (flush ? kTopBit : 0u);
+                    // does a short segment run on past this chunk?
+                    const bool cont = __shfl(proc && !last ? 1 : 0, g * LPR + LPR - 1) != 0;
+#pragma unroll
+                    for (int s0 = 0; s0 < LPR; s0 += U) {
+                        float4 row[U];
+                        uint32_t fb[U], fu[U];
+                        float wv[U];
+#pragma unroll
+                        for (int uu = 0; uu < U; ++uu) {
+                            const int src = g * LPR + s0 + uu;
+                            fb[uu] = __shfl(pb, src);
+                            fu[uu] = __shfl(pu, src);
+                            wv[uu] = sizeof(V) == 8 ? __shfl(ww, src) : 1.0f;
+                            row[uu] = make_float4(0.f, 0.f, 0.f, 0.f);
+                            if ((fb[uu] & kTopBit) && vact)
+                                row[uu] = *reinterpret_cast<const float4 *>(
+                                    gcol + static_cast<int64_t>(fb[uu] & ~kTopBit) * total_dim);
+                        }
+#pragma unroll
+                        for (int uu = 0; uu < U; ++uu) {
+                            if (!(fb[uu] & kTopBit)) continue;
+                            acc.x = __builtin_fmaf(wv[uu], row[uu].x, acc.x);
+                            acc.y = __builtin_fmaf(wv[uu], row[uu].y, acc.y);
+                            acc.z = __builtin_fmaf(wv[uu], row[uu].z, acc.z);
+                            acc.w = __builtin_fmaf(wv[uu], row[uu].w, acc.w);
+                            if (fu[uu] & kTopBit) {
+                                const uint32_t u = fu[uu] & ~kTopBit;
+                                float *dst;
+                                if (u < u_before) {
+                                    dst = partials + (2 * gq) * max_dim;
+                                    hs = static_cast<int32_t>(u);
+                                } else if (u == cross_u && cross_long) {
+                                    dst = partials + (2 * gq + 1) * max_dim;
+                                    tsg = static_cast<int32_t>(u);
+                                } else {
+                                    dst = grad_rows + static_cast<int64_t>(pre.dimsum) +
+                                          static_cast<int64_t>(u - static_cast<uint32_t>(pre.starts)) * m.dim;
+                                }
+                                if (vact) store4(dst + static_cast<int64_t>(c0 + v) * 4, acc);
+                                acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                            }
+                        }
+                    }
+                    if (c + LPR >= p1 && !cont) break;
+                }
+            }
+        }
+        if (v == 0) {
+            head_seg[gq] = hs;
+            tail_seg[gq] = tsg;
+        }
+    }
+}
+
+template <typename V>
+__global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__restrict__ keys,
+                                                          const V *__restrict__ vals,
+                                                          const float *__restrict__ grad_out,
+                                                          const int64_t *__restrict__ seg_offsets,
+                                                          const TableMeta *__restrict__ meta,
+                                                          const Range *__restrict__ ranges, int T,
+                                                          const Ctl *__restrict__ ctl,
+                                                          const TileSeg *__restrict__ tseg, int64_t total_dim,
+                                                          float *__restrict__ grad_rows,
+                                                          float *__restrict__ partials, int max_dim,
+                                                          int32_t *__restrict__ head_seg,
+                                                          int32_t *__restrict__ tail_seg) {
+    __shared__ uint32_t blk_cnt[kBlksPerTile];
+    __shared__ uint32_t blk_starts[kBlksPerTile + 1];
+    // consecutive tiles (one table's gradient slice) stay on one XCD's L2
+    const int64_t tile = xcd_remap(blockIdx.x, gridDim.x, kNumXcd);
+    if (tile >= ctl->total_tiles || ctl->skip_rows || ctl->abort) return;
+    TileInfo ti;
+    if (!tile_info(ranges, T, tile, ti)) return;
+    const TableMeta m = meta[ti.t];
+    const TileSeg pre = tseg[tile];
+    const int tid = threadIdx.x;
+    // segment starts per block of kBlk positions (8 threads x 16 positions)
+    if (tid < kBlksPerTile) blk_cnt[tid] = 0;
+    __syncthreads();
+    {
+        const int64_t my = ti.p_lo + static_cast<int64_t>(tid) * kItems;
+        uint32_t ns = 0;
+#pragma unroll
+        for (int q = 0; q < kItems; ++q) {
+            const int64_t pos = my + q;
+            if (pos < ti.p_hi) {
+                bool kept, st;
+                seg_flags(keys, pos, ti.start, keys[pos], kept, st);
+                ns += st;
+            }
+        }
+        if (ns) atomicAdd(&blk_cnt[tid / (kBlk / kItems)], ns);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t run = 0;
+        for (int q = 0; q < kBlksPerTile; ++q) {
+            blk_starts[q] = run;
+            run += blk_cnt[q];
+        }
+        blk_starts[kBlksPerTile] = run;
+    }
+    __syncthreads();
+    switch (m.glpr_log2) {
+#define TBE_REDUCE_CASE(L, LPR)                                                                            \
+    case L:                                                                                                \
+        reduce_tile<V, LPR>(keys, vals, grad_out, seg_offsets, m, ti, pre, blk_starts, total_dim, grad_rows, \
+                            partials, max_dim, head_seg, tail_seg, tile);                                  \
+        break;
+        TBE_REDUCE_CASE(0, 1)
+        TBE_REDUCE_CASE(1, 2)
+        TBE_REDUCE_CASE(2, 4)
+        TBE_REDUCE_CASE(3, 8)
+        TBE_REDUCE_CASE(4, 16)
+        TBE_REDUCE_CASE(5, 32)
+        default:
+        TBE_REDUCE_CASE(6, 64)
+#undef TBE_REDUCE_CASE
+    }
+}
+
+// Sums the pieces of every segment that crosses a block edge, in a fixed
+// pairwise order (binary-counter summation over the pieces), and writes its
+// gradient row once.
+__global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restrict__ ranges, int T,
+                                                           const TableMeta *__restrict__ meta,
+                                                           const Ctl *__restrict__ ctl,
+                                                           const int32_t *__restrict__ head_seg,
+                                                           const int32_t *__restrict__ tail_seg,
+                                                           const float *__restrict__ partials, int max_dim,
+                                                           const int64_t *__restrict__ grad_row_offsets,
+                                                           float *__restrict__ grad_rows) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+    if (ctl->skip_rows || ctl->abort) return;
+    const int64_t nblk = ctl->total_tiles * kBlksPerTile;
+    if (q >= nblk) return;
+    const int32_t u = tail_seg[q];
+    if (u < 0) return;
+    const int t = find_table(ranges, T, q / kBlksPerTile);
+    const int nvec = meta[t].dim / 4;
+    float *out = grad_rows + grad_row_offsets[u];
+    for (int c0 = 0; c0 < nvec; c0 += 64) {
+        const int cv = c0 + lane;
+        const bool act = cv < nvec;
+        float4 st[kPairLevels];
+        float4 top = make_float4(0.f, 0.f, 0.f, 0.f);
+        bool top_used = false;
+        uint32_t n = 0;
+        int64_t qq = q;
+        int64_t slot = 2 * q + 1;
+        while (true) {
+            float4 x = act ? *reinterpret_cast<const float4 *>(partials + slot * max_dim + cv * 4)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+            bool done = false;
+#pragma unroll
+            for (int l = 0; l < kPairLevels; ++l) {
+                if (!done) {
+                    if ((n >> l) & 1u) {
+                        x = make_float4(st[l].x + x.x, st[l].y + x.y, st[l].z + x.z, st[l].w + x.w);
+                    } else {
+                        st[l] = x;
+                        done = true;
+                    }
+                }
+            }
+            if (!done) {
+                top = top_used ? make_float4(top.x + x.x, top.y + x.y, top.z + x.z, top.w + x.w) : x;
+                top_used = true;
+            }
+            ++n;
+            ++qq;
+            if (qq >= nblk || head_seg[qq] != u) break;
+            slot = 2 * qq;
+        }
+        float4 sum = top;
+        bool have = top_used;
+#pragma unroll
+        for (int l = kPairLevels - 1; l >= 0; --l) {
+            if ((n >> l) & 1u) {
+                sum = have ? make_float4(sum.x + st[l].x, sum.y + st[l].y, sum.z + st[l].z, sum.w + st[l].w)
+                           : st[l];
+                have = true;
+            }
+        }
+        if (act) store4(out + cv * 4, sum);
+    }
+}
+
+// ------------------------------------------------------------- workspace
+
+struct Layout {
+    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, head, tail, partials, total;
+    int64_t max_tiles, max_blocks, hist_chunks;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+Layout layout(const Plan &p, int64_t N) {
+    Layout L{};
+    const size_t vb = 8;  // room for weighted values; unweighted calls use half
+    L.max_tiles = (N + kTile - 1) / kTile + p.T;
+    L.max_blocks = L.max_tiles * kBlksPerTile;
+    L.hist_chunks = (L.max_tiles * kBuckets + kScanChunk - 1) / kScanChunk;
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o = align256(o + bytes);
+        return at;
+    };
+    L.ctl = take(sizeof(Ctl));
+    L.ranges = take(sizeof(Range) * (p.T + 1));
+    L.keys0 = take(sizeof(uint32_t) * N);
+    L.keys1 = take(sizeof(uint32_t) * N);
+    L.vals0 = take(vb * N);
+    L.vals1 = take(vb * N);
+    L.hist = take(sizeof(uint32_t) * L.max_tiles * kBuckets);
+    L.sums = take(sizeof(uint32_t) * (L.hist_chunks + 1));
+    L.tseg = take(sizeof(TileSeg) * L.max_tiles);
+    L.head = take(sizeof(int32_t) * L.max_blocks);
+    L.tail = take(sizeof(int32_t) * L.max_blocks);
+    L.partials = take(sizeof(float) * 2 * L.max_blocks * static_cast<size_t>(p.max_dim));
+    L.total = o;
+    return L;
+}
+
+template <typename V>
+hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, const int64_t *offsets,
+               int64_t N, const float *weights, char *ws, const Layout &L, float *grad_rows, int64_t capacity,
+               int64_t *grad_idx, int64_t *seg_offsets, int64_t *grad_row_offsets, int64_t *num_unique,
+               int32_t *status, hipStream_t stream) {
+    Ctl *ctl = reinterpret_cast<Ctl *>(ws + L.ctl);
+    Range *ranges = reinterpret_cast<Range *>(ws + L.ranges);
+    uint32_t *keys[2] = {reinterpret_cast<uint32_t *>(ws + L.keys0), reinterpret_cast<uint32_t *>(ws + L.keys1)};
+    V *vals[2] = {reinterpret_cast<V *>(ws + L.vals0), reinterpret_cast<V *>(ws + L.vals1)};
+    uint32_t *hist = reinterpret_cast<uint32_t *>(ws + L.hist);
+    uint32_t *sums = reinterpret_cast<uint32_t *>(ws + L.sums);
+    TileSeg *tseg = reinterpret_cast<TileSeg *>(ws + L.tseg);
+    int32_t *head = reinterpret_cast<int32_t *>(ws + L.head);
+    int32_t *tail = reinterpret_cast<int32_t *>(ws + L.tail);
+    float *partials = reinterpret_cast<float *>(ws + L.partials);
+    const int check = p.bounds_check;
+    const int T = p.T;
+    const int64_t nbags = static_cast<int64_t>(T) * p.B;
+
+    hipLaunchKernelGGL(setup_kernel, dim3(1), dim3(kThreads), 0, stream, offsets, T, p.B, N, check, ctl, ranges,
+                       status, num_unique, seg_offsets, grad_row_offsets);
+    if (N == 0 || nbags == 0) return hipGetLastError();
+    hipLaunchKernelGGL(keys_kernel<V>, dim3(static_cast<unsigned>((nbags + kWaves - 1) / kWaves)), dim3(kThreads),
+                       0, stream, p.meta_dev, indices, offsets, weights, ranges, p.B, nbags, check, ctl, keys[0],
+                       vals[0], status);
+    // bits: every valid local key, and the drop key's low bits above them
+    int64_t max_rows = 1;
+    for (int t = 0; t < T; ++t) max_rows = p.meta_host[t].rows > max_rows ? p.meta_host[t].rows : max_rows;
+    int bits = 1;
+    while (bits < 32 && (int64_t(1) << bits) <= max_rows) ++bits;
+    const dim3 tiles(static_cast<unsigned>(L.max_tiles)), blk(kThreads);
+    int cur = 0;
+    for (int shift = 0; shift < bits; shift += kRadixBits) {
+        const int nb = bits - shift < kRadixBits ? bits - shift : kRadixBits;
+        hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, keys[cur], ranges, T, ctl, shift, nb, hist);
+        hipLaunchKernelGGL(scan_reduce_kernel, dim3(static_cast<unsigned>(L.hist_chunks)), blk, 0, stream, hist,
+                           sums, ctl);
+        hipLaunchKernelGGL(scan_top_kernel, dim3(1), blk, 0, stream, sums, ctl);
+        hipLaunchKernelGGL(scan_down_kernel, dim3(static_cast<unsigned>(L.hist_chunks)), blk, 0, stream, hist,
+                           sums, ctl);
+        hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, blk, 0, stream, keys[cur], vals[cur], keys[cur ^ 1],
+                           vals[cur ^ 1], hist, ranges, T, ctl, shift, nb);
+        cur ^= 1;
+    }
+    hipLaunchKernelGGL(seg_count_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg);
+    hipLaunchKernelGGL(seg_scan_kernel, dim3(1), blk, 0, stream, tseg, ctl, num_unique, seg_offsets,
+                       grad_row_offsets, capacity, status);
+    hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
+                       grad_idx, seg_offsets, grad_row_offsets);
+    hipLaunchKernelGGL(reduce_kernel<V>, tiles, blk, 0, stream, keys[cur], vals[cur], grad_out, seg_offsets,
+                       p.meta_dev, ranges, T, ctl, tseg, p.total_dim, grad_rows, partials, p.max_dim, head, tail);
+    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((L.max_blocks + kWaves - 1) / kWaves)), blk, 0,
+                       stream, ranges, T, p.meta_dev, ctl, head, tail, partials, p.max_dim, grad_row_offsets,
+                       grad_rows);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t backward_workspace_bytes(const Plan &p, int64_t num_indices) { return layout(p, num_indices).total; }
+
+hipError_t launch_backward(const Plan &p, const float *grad_out, const int64_t *indices, const int64_t *offsets,
+                           int64_t num_indices, const float *weights, void *workspace, size_t workspace_bytes,
+                           float *grad_rows, int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
+                           int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, hipStream_t stream) {
+    (void)workspace_bytes;
+    const Layout L = layout(p, num_indices);
+    char *ws = static_cast<char *>(workspace);
+    if (weights)
+        return run<uint64_t>(p, grad_out, indices, offsets, num_indices, weights, ws, L, grad_rows,
+                             grad_rows_capacity, grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream);
+    return run<uint32_t>(p, grad_out, indices, offsets, num_indices, nullptr, ws, L, grad_rows, grad_rows_capacity,
+                         grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream);
 }
 
 }  // namespace tbe

@@ -97,7 +97,10 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
         int l = 0;
         while ((1 << l) < m.nvec && l < 6) ++l;
         m.lpr_log2 = l;
-        m.pad[0] = m.pad[1] = 0;
+        l = 0;
+        while ((1 << l) < D / 4 && l < 6) ++l;
+        m.glpr_log2 = l;
+        m.pad = 0;
         packed += R * D;
         dim_off += D;
         row_base += R;
@@ -164,7 +167,7 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *ind
 int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, size_t *bytes) {
     const tbe::Plan *p = plan_of(plan);
     if (!p || !bytes) return TBE_ERR_NULL;
-    if (num_indices < 0 || num_indices >= (int64_t(1) << 32)) return TBE_ERR_SHAPE;
+    if (num_indices < 0 || num_indices >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
     *bytes = tbe::backward_workspace_bytes(*p, num_indices);
     return TBE_OK;
 }
@@ -176,8 +179,11 @@ int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t 
                      int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream) {
     const tbe::Plan *p = plan_of(plan);
     if (!p) return TBE_ERR_NULL;
-    // lookup positions are carried as 32-bit values through the sort
-    if (num_indices < 0 || num_indices >= (int64_t(1) << 32)) return TBE_ERR_SHAPE;
+    // sorted positions and segment ids are carried in 32 bits on the device
+    if (num_indices < 0 || num_indices >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
+    // local row ids are 32-bit sort keys, with one key value kept for dropped lookups
+    for (int32_t t = 0; t < p->T; ++t)
+        if (p->meta_host[t].rows >= (int64_t(1) << 32) - 1) return TBE_ERR_SHAPE;
     if (grad_rows_capacity < 0) return TBE_ERR_SHAPE;
     const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
     if ((!offsets && nbags > 0) || !seg_offsets || !grad_row_offsets || !num_unique) return TBE_ERR_NULL;

@@ -18,7 +18,8 @@ struct TableMeta {
     int32_t dim_off;      // first output column: sum of D_t' for t' < t
     int32_t nvec;         // 16-byte vectors per table row: D_t * elem_size / 16
     int32_t lpr_log2;     // log2 of lanes per row: smallest power of two >= min(nvec, 64)
-    int32_t pad[2];
+    int32_t glpr_log2;    // the same for an fp32 row of D_t (gradient rows): min(D_t / 4, 64)
+    int32_t pad;
 };
 static_assert(sizeof(TableMeta) == 48, "TableMeta layout");
 

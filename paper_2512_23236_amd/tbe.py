@@ -218,7 +218,10 @@ def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets:
     dev = plan.device
     if outputs is None:
         if grad_rows_capacity is None:
-            grad_rows_capacity = N * int(plan.dims.max()) if N else 0
+            # bound: every lookup its own row; needs the per-table lookup counts
+            # (one small device-to-host copy of T+1 offsets)
+            bounds = offsets[:: plan.B].cpu().numpy() if plan.B else np.zeros(plan.T + 1, np.int64)
+            grad_rows_capacity = int((np.diff(bounds) * plan.dims.astype(np.int64)).sum()) if N else 0
         outputs = SparseGrad(
             torch.empty(max(grad_rows_capacity, 1), dtype=torch.float32, device=dev),
             torch.empty(max(N, 1), dtype=torch.int64, device=dev),

@@ -1,0 +1,195 @@
+"""Backward (sparse gradient) parity of the HIP path against the CPU oracle:
+row ids, segment boundaries and row offsets bit-exact; gradient rows within
+the fp32 summation tolerance."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from paper_2512_23236_amd import tbe
+from tests.gpu_util import device, note, plan_for
+
+pytestmark = pytest.mark.gpu
+
+GRAD_RTOL = 1e-5   # the gradient touches only fp32 data
+
+
+def run_backward(spec, d, bounds_check=True, capacity=None):
+    plan = plan_for(spec, bounds_check)
+    status = torch.zeros(1, dtype=torch.int32, device=device())
+    g = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], d.get("weights"),
+                     grad_rows_capacity=capacity, status=status)
+    torch.cuda.synchronize()
+    return g, int(status.item())
+
+
+def oracle_backward(spec, d):
+    idx = d["indices"].cpu().numpy()
+    off = d["offsets"].cpu().numpy()
+    seg = oracle.backward_segments(spec.rows, spec.dims, idx, off, spec.B)
+    w = None if d.get("weights") is None else d["weights"].cpu().numpy()
+    rows, ab, _ = oracle.backward_rows(spec.rows, spec.dims, off, spec.B, d["grad_out"].cpu().numpy(), seg, weights=w)
+    return seg, rows, ab
+
+
+def check(spec, d=None, weighted=None):
+    note(f"[bwd] {spec.name} T={spec.T} B={spec.B} dims={list(spec.dims)[:6]} weighted={spec.weighted}")
+    if d is None:
+        d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    g, st = run_backward(spec, d)
+    assert st == 0, f"status {st}"
+    gidx, segs, gro, rows = g.trimmed()
+    seg, ref, ab = oracle_backward(spec, d)
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(segs.numpy(), seg["seg_offsets"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    err = float(oracle.summation_error(rows.numpy(), ref, ab).max()) if ref.size else 0.0
+    note(f"[bwd] {spec.name}: U={seg['U']} N={d['N']} max summation error {err:.3g}")
+    assert err <= GRAD_RTOL
+    return g, d
+
+
+@pytest.mark.parametrize("k", [5, 4])
+@pytest.mark.parametrize("seed", [1, 2])
+def test_small_configs(k, seed):
+    # B large enough that each table's range spans several 4096-position tiles
+    check(workloads.small_config(k, seed=seed, T=4, B=300))
+
+
+@pytest.mark.parametrize("weighted", [False, True])
+def test_dims(weighted):
+    dims = [4, 8, 24, 64, 128, 256, 512, 1536]
+    base = workloads.small_config(5, seed=4, T=len(dims), B=90)
+    spec = dataclasses.replace(base, dtype="f32", dims=np.array(dims, np.int32), weighted=weighted,
+                               name=f"bwd-dims-{'w' if weighted else 'u'}")
+    check(spec)
+
+
+def test_hot_rows_and_block_edges():
+    """One table hit only at row 3 (a single segment thousands long, cut by
+    many block edges), and a table whose segments have lengths around the
+    128-position block size."""
+    spec = workloads.small_config(5, seed=6, T=3, B=400)
+    d = workloads.gen_all(spec, device())
+    off = d["offsets"].cpu()
+    s0, e0 = int(off[0]), int(off[spec.B])
+    d["indices"][s0:e0] = 3
+    s1, e1 = int(off[spec.B]), int(off[2 * spec.B])
+    n1 = e1 - s1
+    pattern = np.repeat(np.arange(n1), np.resize([127, 128, 129, 1, 256, 300, 5], n1))[:n1]
+    pattern = pattern % int(spec.rows[1])
+    d["indices"][s1:e1] = torch.as_tensor(pattern, device=device())
+    g, _ = check(spec, d)
+
+
+def test_all_tables_one_row():
+    spec = dataclasses.replace(workloads.small_config(5, seed=7, T=2, B=200), rows=np.array([1, 1], np.int64))
+    check(spec)
+
+
+def test_deterministic_repeat():
+    spec = workloads.small_config(4, seed=8, T=3, B=400)
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    a, _ = run_backward(spec, d)
+    b, _ = run_backward(spec, d)
+    for x, y in zip(a.trimmed(), b.trimmed()):
+        assert torch.equal(x, y)
+
+
+def test_bounds_check_drops_bad_lookups():
+    spec = workloads.small_config(5, seed=9, T=3, B=60)
+    d = workloads.gen_all(spec, device())
+    N = d["N"]
+    bad = torch.tensor([1, N // 2, N - 1], device=device())
+    good = d["indices"].clone()
+    d["indices"][bad] = torch.tensor([-1, 10 ** 9, int(spec.rows.max()) + 1], device=device())
+    g, st = run_backward(spec, d)
+    assert st & tbe.STATUS_INDEX_OOB
+    # expected: the oracle on the same lookups with the bad ones removed
+    keep = torch.ones(N, dtype=torch.bool)
+    keep[bad.cpu()] = False
+    off = d["offsets"].cpu()
+    bag = torch.repeat_interleave(torch.arange(off.numel() - 1), torch.diff(off))
+    lens = torch.bincount(bag[keep], minlength=off.numel() - 1)
+    off2 = torch.zeros_like(off)
+    torch.cumsum(lens, 0, out=off2[1:])
+    d2 = dict(d, indices=good[keep.to(device())], offsets=off2.to(device()))
+    seg, ref, ab = oracle_backward(spec, d2)
+    gidx, segs, gro, rows = g.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(segs.numpy(), seg["seg_offsets"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    assert float(oracle.summation_error(rows.numpy(), ref, ab).max()) <= GRAD_RTOL
+
+
+def test_bad_offsets_flagged():
+    spec = workloads.small_config(5, seed=10, T=2, B=30)
+    d = workloads.gen_all(spec, device())
+    off = d["offsets"].clone()
+    off[3], off[4] = off[4].item(), off[3].item()
+    g, st = run_backward(spec, dict(d, offsets=off))
+    assert st & tbe.STATUS_OFFSETS
+    assert g.num_unique() == 0
+
+
+def test_capacity_too_small():
+    spec = workloads.small_config(5, seed=11, T=2, B=50)
+    d = workloads.gen_all(spec, device())
+    g, st = run_backward(spec, d, capacity=16)
+    assert st & tbe.STATUS_CAPACITY
+    seg, _, _ = oracle_backward(spec, d)
+    gidx, segs, gro, _ = g.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+
+
+def test_no_lookups():
+    spec = dataclasses.replace(workloads.small_config(5, seed=12, T=2, B=8), empty_p=1.0)
+    d = workloads.gen_all(spec, device())
+    assert d["N"] == 0
+    g, st = run_backward(spec, d)
+    assert st == 0 and g.num_unique() == 0
+    assert int(g.seg_offsets[0]) == 0 and int(g.grad_row_offsets[0]) == 0
+
+
+def test_workspace_too_small_rejected():
+    spec = workloads.small_config(5, seed=13, T=2, B=8)
+    d = workloads.gen_all(spec, device())
+    plan = plan_for(spec)
+    ws = torch.empty(16, dtype=torch.uint8, device=device())
+    with pytest.raises(tbe.TBEError):
+        tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], workspace=ws)
+
+
+@pytest.mark.slow
+def test_full_size_cfg5():
+    """Configuration 5 at full size in the benchmark's launch configuration:
+    every integer output bit-exact against the oracle, gradient rows checked
+    on a sample that includes the longest segments."""
+    spec = workloads.make_config(5)
+    note(f"[bwd-full] cfg5: generating inputs ({spec.table_bytes / 1e9:.1f} GB tables)")
+    offsets = workloads.gen_offsets(spec, device())
+    d = {"offsets": offsets, "indices": workloads.gen_indices(spec, offsets), "N": int(offsets[-1]),
+         "grad_out": workloads.gen_grad_out(spec, device())}
+    g, st = run_backward(spec, d)
+    assert st == 0
+    note("[bwd-full] GPU done; oracle integer part")
+    idx = d["indices"].cpu().numpy()
+    off = d["offsets"].cpu().numpy()
+    seg = oracle.backward_segments(spec.rows, spec.dims, idx, off, spec.B)
+    gidx, segs, gro, rows = g.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(segs.numpy(), seg["seg_offsets"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    lens = np.diff(seg["seg_offsets"])
+    rng = np.random.default_rng(5)
+    sel = np.unique(np.concatenate([np.argsort(lens)[-20:], rng.choice(seg["U"], 2000, replace=False)]))
+    note(f"[bwd-full] U={seg['U']}, oracle rows for {sel.size} segments (longest {lens.max()})")
+    ref, ab, ro = oracle.backward_rows(spec.rows, spec.dims, off, spec.B, d["grad_out"].cpu().numpy(), seg, sel=sel)
+    got = np.concatenate([rows[int(gro[u]):int(gro[u + 1])].numpy() for u in sel])
+    err = float(oracle.summation_error(got, ref, ab).max())
+    note(f"[bwd-full] max summation error {err:.3g}")
+    assert err <= GRAD_RTOL
