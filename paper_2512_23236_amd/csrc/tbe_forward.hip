@@ -1,19 +1,20 @@
 // Forward pooled embedding-bag lookup for gfx950 (CDNA4, wave64).
 //
-// One wavefront pools one (bag, table).  A table row of D_t elements is
-// nvec = D_t * elem_size / 16 sixteen-byte vectors; LPR lanes (the smallest
-// power of two >= nvec, at most 64) read one row with 16-byte loads, so one
-// wave instruction gathers G = 64 / LPR rows.  The bag's indices are read 64
-// at a time, one per lane, turned into row byte offsets, and handed to the
-// sub-groups with cross-lane permutes; each sub-group issues U row loads
-// before it consumes any, keeping several kilobytes in flight per wave.  Each
-// lane accumulates its columns in fp32 (fp16 / bf16 widened exactly), in
-// lookup order within its sub-group; the G partial rows are then combined by
-// a fixed xor-butterfly, so every output element has one writer and a fixed
-// summation order.
+// A table row of D_t elements is nvec = D_t * elem_size / 16 sixteen-byte
+// vectors, read by a lane group of LPR lanes (the smallest power of two >=
+// nvec, at most 64) with one 16-byte load per lane; a wave holds G = 64 / LPR
+// lane groups.  Each lane group owns kBagsPerGroup consecutive bags of one
+// table and streams through their lookups in order, keeping a ring of U row
+// loads in flight: the row U lookups ahead is requested as soon as a row is
+// consumed, so loads stay outstanding across bag boundaries and the wave
+// never waits on a bag's index list before its rows.  Each lane accumulates
+// its columns in fp32 (fp16 / bf16 widened exactly) in lookup order and
+// writes the bag's pooled row when the bag's last lookup is consumed: every
+// output element has one writer and a fixed summation order.
 //
-// The work is bound by HBM (or cache) bandwidth: about one fma per element
-// read, far below the fp32 vector ridge point.
+// The work is bound by memory latency and bandwidth (HBM and the L2 /
+// Infinity Cache that serve hot rows): about one fma per element read, far
+// below the fp32 vector ridge point.
 
 #include "tbe_internal.h"
 
@@ -22,6 +23,7 @@ namespace {
 
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = 64 * kWavesPerBlock;
+typedef float f4 __attribute__((ext_vector_type(4)));
 
 // Adds w * (one 16-byte vector of table elements) to acc.
 template <int DT>
@@ -72,112 +74,217 @@ struct Elem<TBE_BF16> {
     }
 };
 
-__device__ inline int64_t shfl64(int64_t v, int src) {
-    const int lo = __shfl(static_cast<int>(v & 0xffffffff), src);
-    const int hi = __shfl(static_cast<int>(v >> 32), src);
-    return (static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo);
-}
 
-// Pools bag [s, e) of table m into out_row (B-row slice at dim_off).
-template <int DT, int LPR>
-__device__ inline void pool_bag(const TableMeta &m, const char *__restrict__ table,
-                                const int64_t *__restrict__ indices,
-                                const float *__restrict__ weights, int64_t s, int64_t e,
-                                float *__restrict__ out_row, int lane, bool check,
-                                int32_t *status) {
+// Streams kBagsPerGroup bags per lane group: bags k0 + g*kBagsPerGroup + i of
+// one table (the unit holds nbags_unit bags, k0 first).  Inside the stream
+// loop every row load is issued unconditionally (lanes with nothing to read
+// load zeros from the zero page) and finished bags are parked in LDS, so the
+// loop holds no conditional vector-memory instruction and the ring's loads
+// are waited for one at a time, oldest first.
+template <int DT, int LPR, bool WEIGHTED>
+__device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ table,
+                                 const int64_t *__restrict__ indices, const float *__restrict__ weights,
+                                 const int64_t *__restrict__ offsets, int64_t k0, int nbags_unit,
+                                 float *__restrict__ out, int64_t B, int64_t N, int64_t total_dim, bool check,
+                                 int32_t *status, int lane, const char *__restrict__ zero_page,
+                                 float *__restrict__ stage) {
     using E = Elem<DT>;
-    constexpr int G = 64 / LPR;                 // rows per wave instruction
-    constexpr int U0 = 32 / G;
-    constexpr int U = U0 < 1 ? 1 : (U0 > 8 ? 8 : U0);  // row loads in flight per lane
+    constexpr int U = LPR < 8 ? LPR : 8;  // row loads in flight per lane group
+    constexpr int NB = kBagsPerGroup;
+    constexpr uint32_t kSkip = 0xffffffffu;
     const int g = lane / LPR, v = lane % LPR;
-    const int64_t row_bytes = static_cast<int64_t>(m.nvec) * 16;
+    const int nbs = nbags_unit - g * NB < 0 ? 0 : (nbags_unit - g * NB > NB ? NB : nbags_unit - g * NB);
+    const int64_t kg = k0 + static_cast<int64_t>(g) * NB < k0 + nbags_unit ? k0 + static_cast<int64_t>(g) * NB
+                                                                            : k0 + nbags_unit;
+    // bag boundaries of this group, clamped monotone into [0, N] when checking
+    int64_t bnd64[NB + 1];
+#pragma unroll
+    for (int i = 0; i <= NB; ++i) bnd64[i] = offsets[kg + (i < nbs ? i : nbs)];
+    if (check) {
+        int64_t lo = 0;
+        bool bad = false;
+#pragma unroll
+        for (int i = 0; i <= NB; ++i) {
+            const int64_t c = bnd64[i] < lo ? lo : (bnd64[i] > N ? N : bnd64[i]);
+            bad |= c != bnd64[i];
+            bnd64[i] = c;
+            lo = c;
+        }
+        if (bad) atomicOr(status, TBE_STATUS_OFFSETS);
+    }
+    const int64_t P = bnd64[0];
+    int32_t bnd[NB + 1];  // relative to P
+#pragma unroll
+    for (int i = 0; i <= NB; ++i) bnd[i] = static_cast<int32_t>(bnd64[i] - P);
+    const int32_t Q = bnd[NB];
+    const uint32_t b0 = static_cast<uint32_t>(kg % B);
+    float *out0 = out + static_cast<int64_t>(b0) * total_dim + m.dim_off;
+    const uint32_t row_bytes = static_cast<uint32_t>(m.nvec) * 16u;
+
+    // the wave walks the longest group's span
+    int32_t span = Q;
+#pragma unroll
+    for (int mask = LPR; mask < 64; mask <<= 1) {
+        const int32_t o = __shfl_xor(span, mask);
+        span = o > span ? o : span;
+    }
+    float *my_stage = stage + (static_cast<int>(g) * NB * LPR + v) * E::kPerVec;  // + bag * LPR * kPerVec
 
     for (int c0 = 0; c0 < m.nvec; c0 += LPR) {  // one pass unless rows exceed 1 KiB
         const bool vact = c0 + v < m.nvec;
-        const int64_t col_bytes = static_cast<int64_t>(c0 + v) * 16;
+        const char *colp = table + static_cast<int64_t>(c0 + v) * 16;
+        const char *zerop = zero_page + v * 16;
+        // lane v of the group holds lookup rel + v (cur) and rel + LPR + v (nxt)
+        // Index chunks of LPR lookups, lane v holding lookup rel + v: `cur`
+        // and `nxt` are checked row ids (kSkip = nothing to read); `far` is
+        // the raw chunk after them, still in flight, so an index load always
+        // has a chunk's worth of row loads behind it before it is read.
+        // Index loads are unconditional too: past the stream end they read
+        // the zero page.
+        bool oob = false;
+        auto load_chunk = [&](int32_t rel, int64_t &idx, float &w) {
+            const int32_t rp = rel + v;
+            const bool in = rp < Q;
+            idx = __builtin_nontemporal_load(in ? indices + P + rp : reinterpret_cast<const int64_t *>(zero_page));
+            w = 1.0f;
+            if constexpr (WEIGHTED)
+                w = __builtin_nontemporal_load(in ? weights + P + rp : reinterpret_cast<const float *>(zero_page));
+        };
+        auto check_chunk = [&](int32_t rel, int64_t idx) {
+            const bool in = rel + v < Q;
+            const bool ok = in && (!check || (idx >= 0 && idx < m.rows));
+            oob |= in && !ok;
+            return ok ? static_cast<uint32_t>(idx) : kSkip;
+        };
+        int64_t far_idx;
+        float cur_w, nxt_w, far_w;
+        load_chunk(0, far_idx, cur_w);
+        uint32_t cur_r = check_chunk(0, far_idx);
+        load_chunk(LPR, far_idx, nxt_w);
+        uint32_t nxt_r = check_chunk(LPR, far_idx);
+        load_chunk(2 * LPR, far_idx, far_w);
+
+        uint4 ring[U];
+        float ring_w[WEIGHTED ? U : 1];
+        auto issue = [&](int src_lane, bool from_next, uint4 &dst, float &dw) {
+            const int src = g * LPR + src_lane;
+            const uint32_t r = from_next ? __shfl(nxt_r, src) : __shfl(cur_r, src);
+            const bool ok = r != kSkip && vact;
+            const char *addr = ok ? colp + static_cast<uint64_t>(r) * row_bytes : zerop;
+            dst = *reinterpret_cast<const uint4 *>(addr);
+            if constexpr (WEIGHTED) {
+                const float w = from_next ? __shfl(nxt_w, src) : __shfl(cur_w, src);
+                dw = ok ? w : 0.f;
+            }
+        };
+#pragma unroll
+        for (int sl = 0; sl < U; ++sl) issue(sl, false, ring[sl], ring_w[WEIGHTED ? sl : 0]);
+
         float acc[E::kPerVec];
 #pragma unroll
         for (int i = 0; i < E::kPerVec; ++i) acc[i] = 0.0f;
+        int bag = 0;
+        auto end_of = [&](int i) {
+            return i == 0 ? bnd[1] : i == 1 ? bnd[2] : i == 2 ? bnd[3] : bnd[4];
+        };
+        int32_t bag_end = bnd[1];
+        while (bag + 1 < nbs && bag_end == 0) bag_end = end_of(++bag);
 
-        for (int64_t base = s; base < e; base += 64) {
-            const int n = static_cast<int>(e - base < 64 ? e - base : 64);
-            int64_t my_off = -1;  // byte offset of this lane's row; -1 = skip
-            float my_w = 1.0f;
-            if (lane < n) {
-                const int64_t idx = __builtin_nontemporal_load(indices + base + lane);
-                if (weights) my_w = __builtin_nontemporal_load(weights + base + lane);
-                if (!check || (idx >= 0 && idx < m.rows)) {
-                    my_off = idx * row_bytes;
-                } else {
-                    atomicOr(status, TBE_STATUS_INDEX_OOB);
+        for (int32_t base = 0; base < span; base += LPR) {
+#pragma unroll 1
+            for (int s0 = 0; s0 < LPR; s0 += U) {
+#pragma unroll
+                for (int sl = 0; sl < U; ++sl) {
+                    const int32_t rp = base + s0 + sl;
+                    E::fma(acc, ring[sl], WEIGHTED ? ring_w[WEIGHTED ? sl : 0] : 1.0f);
+                    if (rp < Q && rp + 1 == bag_end) {
+                        float *st = my_stage + bag * LPR * E::kPerVec;
+#pragma unroll
+                        for (int i = 0; i < E::kPerVec; ++i) {
+                            st[i] = acc[i];
+                            acc[i] = 0.0f;
+                        }
+                        while (bag + 1 < nbs && bag_end == rp + 1) bag_end = end_of(++bag);
+                    }
+                    const int ahead = s0 + sl + U;
+                    issue(ahead & (LPR - 1), ahead >= LPR, ring[sl], ring_w[WEIGHTED ? sl : 0]);
                 }
             }
-            for (int i = 0; i < n; i += G * U) {
-                uint4 val[U];
-                float wr[U];
+            cur_r = nxt_r;
+            cur_w = nxt_w;
+            nxt_r = check_chunk(base + 2 * LPR, far_idx);
+            nxt_w = far_w;
+            load_chunk(base + 3 * LPR, far_idx, far_w);
+        }
+        if (oob) atomicOr(status, TBE_STATUS_INDEX_OOB);
+        // parked bags to memory; empty bags as +0.0
+        if (vact) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int r = i + u * G + g;
-                    const int64_t off = shfl64(my_off, r & 63);
-                    wr[u] = __shfl(my_w, r & 63);
-                    val[u] = make_uint4(0, 0, 0, 0);
-                    if (r < n && off >= 0 && vact) {
-                        val[u] = *reinterpret_cast<const uint4 *>(table + off + col_bytes);
-                    } else {
-                        wr[u] = 0.0f;
+            for (int i = 0; i < NB; ++i) {
+                if (i < nbs) {
+                    const bool empty = bnd[i] == bnd[i + 1];
+                    const float *st = my_stage + i * LPR * E::kPerVec;
+                    f4 *o = reinterpret_cast<f4 *>(out0 + static_cast<int64_t>(i) * total_dim + (c0 + v) * E::kPerVec);
+#pragma unroll
+                    for (int q = 0; q < E::kPerVec / 4; ++q) {
+                        const f4 val = empty ? f4{0.f, 0.f, 0.f, 0.f}
+                                             : f4{st[4 * q], st[4 * q + 1], st[4 * q + 2], st[4 * q + 3]};
+                        __builtin_nontemporal_store(val, o + q);
                     }
                 }
-#pragma unroll
-                for (int u = 0; u < U; ++u) E::fma(acc, val[u], wr[u]);
             }
-        }
-        // Fixed-order butterfly over the G sub-groups.
-#pragma unroll
-        for (int mask = LPR; mask < 64; mask <<= 1) {
-#pragma unroll
-            for (int i = 0; i < E::kPerVec; ++i) acc[i] += __shfl_xor(acc[i], mask);
-        }
-        if (g == 0 && vact) {
-            float4 *o = reinterpret_cast<float4 *>(out_row + (c0 + v) * E::kPerVec);
-#pragma unroll
-            for (int q = 0; q < E::kPerVec / 4; ++q)
-                o[q] = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
         }
     }
 }
 
-template <int DT>
+// Work unit -> table: the t with meta[t].unit_base <= unit < meta[t+1].unit_base.
+__device__ inline int table_of_unit(const TableMeta *__restrict__ meta, int T, int64_t unit) {
+    int lo = 0, hi = T;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (meta[mid].unit_base <= unit) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+template <int DT, bool WEIGHTED>
 __global__ __launch_bounds__(kBlock) void forward_kernel(
-    const TableMeta *__restrict__ meta, const char *__restrict__ tables,
+    const TableMeta *__restrict__ meta, int T, const char *__restrict__ tables,
     const int64_t *__restrict__ indices, const int64_t *__restrict__ offsets,
     const float *__restrict__ weights, float *__restrict__ out, int32_t *status, int64_t B,
-    int64_t nbags, int64_t N, int64_t total_dim, int check) {
+    int64_t nbags, int64_t N, int64_t total_dim, int64_t units, int check, const char *__restrict__ zero_page) {
+    // finished bags of each lane group, parked until the stream ends
+    __shared__ float stage_all[kWavesPerBlock][64 * kBagsPerGroup * 8];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t wg = xcd_remap(blockIdx.x, gridDim.x, kNumXcd);
-    const int64_t k = wg * kWavesPerBlock + wave;  // bag id, table-major
-    if (k >= nbags) return;
-    if (check && k == 0 && lane == 0) {
+    const int64_t unit = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave;
+    if (check && unit == 0 && lane == 0) {
         if (offsets[0] != 0 || offsets[nbags] != N) atomicOr(status, TBE_STATUS_OFFSETS);
     }
-    const int64_t t = k / B, b = k - t * B;
+    if (unit >= units) return;
+    const int t = table_of_unit(meta, T, unit);
     const TableMeta m = meta[t];
-    int64_t s = offsets[k], e = offsets[k + 1];
-    if (check && (s < 0 || e < s || e > N)) {
-        if (lane == 0) atomicOr(status, TBE_STATUS_OFFSETS);
-        s = e = 0;  // malformed bag: pooled as empty, nothing read
-    }
+    const int64_t first = (unit - m.unit_base) * m.unit_bags;       // bag within the table
+    const int nb = static_cast<int>(B - first < m.unit_bags ? B - first : m.unit_bags);
+    const int64_t k0 = static_cast<int64_t>(t) * B + first;
     constexpr int ES = DT == TBE_F32 ? 4 : 2;
     const char *table = tables + m.elem_offset * ES;
-    float *out_row = out + b * total_dim + m.dim_off;
+    float *stage = stage_all[wave];
     switch (m.lpr_log2) {
-        case 0: pool_bag<DT, 1>(m, table, indices, weights, s, e, out_row, lane, check, status); break;
-        case 1: pool_bag<DT, 2>(m, table, indices, weights, s, e, out_row, lane, check, status); break;
-        case 2: pool_bag<DT, 4>(m, table, indices, weights, s, e, out_row, lane, check, status); break;
-        case 3: pool_bag<DT, 8>(m, table, indices, weights, s, e, out_row, lane, check, status); break;
-        case 4: pool_bag<DT, 16>(m, table, indices, weights, s, e, out_row, lane, check, status); break;
-        case 5: pool_bag<DT, 32>(m, table, indices, weights, s, e, out_row, lane, check, status); break;
-        default: pool_bag<DT, 64>(m, table, indices, weights, s, e, out_row, lane, check, status); break;
+#define TBE_POOL_CASE(L, LPR)                                                                                   \
+    case L:                                                                                                     \
+        pool_unit<DT, LPR, WEIGHTED>(m, table, indices, weights, offsets, k0, nb, out, B, N, total_dim, check, \
+                                     status, lane, zero_page, stage);                                           \
+        break;
+        TBE_POOL_CASE(0, 1)
+        TBE_POOL_CASE(1, 2)
+        TBE_POOL_CASE(2, 4)
+        TBE_POOL_CASE(3, 8)
+        TBE_POOL_CASE(4, 16)
+        TBE_POOL_CASE(5, 32)
+        default:
+        TBE_POOL_CASE(6, 64)
+#undef TBE_POOL_CASE
     }
 }
 
@@ -188,26 +295,20 @@ hipError_t launch_forward(const Plan &p, const void *tables, const int64_t *indi
                           float *out, int32_t *status, hipStream_t stream) {
     const int64_t nbags = static_cast<int64_t>(p.T) * p.B;
     if (nbags == 0) return hipSuccess;
-    const int64_t nwg = (nbags + kWavesPerBlock - 1) / kWavesPerBlock;
-    const dim3 grid(static_cast<unsigned>(nwg)), block(kBlock);
+    const dim3 grid(static_cast<unsigned>((p.fwd_units + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
     const char *tb = static_cast<const char *>(tables);
+    const char *zp = static_cast<const char *>(p.zero_page);
+#define TBE_LAUNCH(DT, W)                                                                                    \
+    hipLaunchKernelGGL((forward_kernel<DT, W>), grid, block, 0, stream, p.meta_dev, p.T, tb, indices, offsets, \
+                       weights, out, status, p.B, nbags, num_indices, p.total_dim, p.fwd_units, p.bounds_check, \
+                       zp)
+    const bool w = weights != nullptr;
     switch (p.dtype) {
-        case TBE_F32:
-            hipLaunchKernelGGL(forward_kernel<TBE_F32>, grid, block, 0, stream, p.meta_dev, tb, indices,
-                               offsets, weights, out, status, p.B, nbags, num_indices, p.total_dim,
-                               p.bounds_check);
-            break;
-        case TBE_F16:
-            hipLaunchKernelGGL(forward_kernel<TBE_F16>, grid, block, 0, stream, p.meta_dev, tb, indices,
-                               offsets, weights, out, status, p.B, nbags, num_indices, p.total_dim,
-                               p.bounds_check);
-            break;
-        default:
-            hipLaunchKernelGGL(forward_kernel<TBE_BF16>, grid, block, 0, stream, p.meta_dev, tb, indices,
-                               offsets, weights, out, status, p.B, nbags, num_indices, p.total_dim,
-                               p.bounds_check);
-            break;
+        case TBE_F32: if (w) TBE_LAUNCH(TBE_F32, true); else TBE_LAUNCH(TBE_F32, false); break;
+        case TBE_F16: if (w) TBE_LAUNCH(TBE_F16, true); else TBE_LAUNCH(TBE_F16, false); break;
+        default: if (w) TBE_LAUNCH(TBE_BF16, true); else TBE_LAUNCH(TBE_BF16, false); break;
     }
+#undef TBE_LAUNCH
     return hipGetLastError();
 }
 

@@ -100,6 +100,9 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
         l = 0;
         while ((1 << l) < D / 4 && l < 6) ++l;
         m.glpr_log2 = l;
+        m.unit_bags = tbe::kBagsPerGroup * (64 >> m.lpr_log2);
+        m.unit_base = p.fwd_units;
+        p.fwd_units += (p.B + m.unit_bags - 1) / m.unit_bags;
         m.pad = 0;
         packed += R * D;
         dim_off += D;
@@ -112,15 +115,17 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
     while (bits < 63 && (int64_t(1) << bits) < p.total_rows) ++bits;
     p.key_bits = bits;
 
+    const size_t meta_bytes = sizeof(tbe::TableMeta) * p.T;
     if (hipGetDevice(&p.device) != hipSuccess ||
-        hipMalloc(reinterpret_cast<void **>(&p.meta_dev), sizeof(tbe::TableMeta) * p.T) != hipSuccess ||
-        hipMemcpy(p.meta_dev, p.meta_host, sizeof(tbe::TableMeta) * p.T, hipMemcpyHostToDevice) !=
-            hipSuccess) {
+        hipMalloc(reinterpret_cast<void **>(&p.meta_dev), meta_bytes + tbe::kZeroPageBytes) != hipSuccess ||
+        hipMemcpy(p.meta_dev, p.meta_host, meta_bytes, hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemset(reinterpret_cast<char *>(p.meta_dev) + meta_bytes, 0, tbe::kZeroPageBytes) != hipSuccess) {
         if (p.meta_dev) (void)hipFree(p.meta_dev);
         delete[] p.meta_host;
         delete h;
         return TBE_ERR_HIP;
     }
+    p.zero_page = reinterpret_cast<const char *>(p.meta_dev) + meta_bytes;
     *plan = h;
     return TBE_OK;
 }

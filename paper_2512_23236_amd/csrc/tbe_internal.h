@@ -8,7 +8,7 @@
 
 namespace tbe {
 
-// Per-table facts the kernels need, one 48-byte record per table, uploaded
+// Per-table facts the kernels need, one 64-byte record per table, uploaded
 // once per plan.  Read wave-uniformly, so they live in scalar registers.
 struct TableMeta {
     int64_t elem_offset;  // first element of the table in the flat buffer
@@ -19,9 +19,11 @@ struct TableMeta {
     int32_t nvec;         // 16-byte vectors per table row: D_t * elem_size / 16
     int32_t lpr_log2;     // log2 of lanes per row: smallest power of two >= min(nvec, 64)
     int32_t glpr_log2;    // the same for an fp32 row of D_t (gradient rows): min(D_t / 4, 64)
-    int32_t pad;
+    int32_t unit_bags;    // forward: bags per wave work unit (bags per lane group x groups per wave)
+    int64_t unit_base;    // forward: work units of all tables before t
+    int64_t pad;
 };
-static_assert(sizeof(TableMeta) == 48, "TableMeta layout");
+static_assert(sizeof(TableMeta) == 64, "TableMeta layout");
 
 inline int elem_size(int dtype) { return dtype == TBE_F32 ? 4 : 2; }
 
@@ -35,8 +37,10 @@ struct Plan {
     int64_t total_rows = 0;
     int64_t table_elems = 0;
     int32_t max_dim = 0;
+    int64_t fwd_units = 0;     // forward work units over all tables
     int device = 0;
-    TableMeta *meta_dev = nullptr;
+    TableMeta *meta_dev = nullptr;   // device: T records, then kZeroPageBytes of zeros
+    const void *zero_page = nullptr; // inside the same allocation as meta_dev
     TableMeta *meta_host = nullptr;
 };
 
@@ -65,5 +69,13 @@ __device__ inline int64_t xcd_remap(int64_t w, int64_t nwg, int num_xcd) {
 }
 
 constexpr int kNumXcd = 8;
+
+// Forward work decomposition: each lane group of a wave streams through
+// kBagsPerGroup consecutive bags of one table.
+constexpr int kBagsPerGroup = 4;
+
+// Zeros that a lane with no row to read loads instead (one wave's 16 bytes per
+// lane), so every row load in the forward stream is issued unconditionally.
+constexpr int kZeroPageBytes = 1024;
 
 }  // namespace tbe
