@@ -377,7 +377,11 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
         uint32_t base = 0;
         if (valid) base = cnt[wave][d];
         rank[r] = base + before;
+        // every lane of the wave reads its digit's count before the digit's
+        // first lane writes the updated count
+        __builtin_amdgcn_wave_barrier();
         if (valid && before == 0) cnt[wave][d] = base + static_cast<uint32_t>(__popcll(peers));
+        __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
     {
@@ -555,15 +559,23 @@ __device__ inline void store4(float *p, const float4 &a) { *reinterpret_cast<flo
 
 constexpr uint32_t kTopBit = 0x80000000u;
 
+// One lane group walks one block at a time: the positions of the segments it
+// owns, in order, as a stream with a ring of U gradient-row loads in flight.
+// Position metadata (key change flags, segment id, batch row, weight) is
+// prepared one chunk of LPR positions ahead from loads issued two chunks
+// ahead; row loads are unconditional (positions the group does not own read
+// the zero page with weight 0), so the loop's waits are for the oldest ring
+// slot only.
 template <typename V, int LPR>
 __device__ inline void reduce_tile(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
                                    const float *__restrict__ grad_out, const int64_t *__restrict__ seg_offsets,
                                    const TableMeta &m, const TileInfo &ti, const TileSeg &pre,
                                    const uint32_t *blk_starts, int64_t total_dim, float *__restrict__ grad_rows,
                                    float *__restrict__ partials, int max_dim, int32_t *__restrict__ head_seg,
-                                   int32_t *__restrict__ tail_seg, int64_t tile) {
+                                   int32_t *__restrict__ tail_seg, int64_t tile, const float *__restrict__ zero_page) {
     constexpr int G = 64 / LPR;
     constexpr int U = LPR < 8 ? LPR : 8;
+    constexpr bool kWeighted = sizeof(V) == 8;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane / LPR, v = lane % LPR;
     const int nsub = kWaves * G;
@@ -571,107 +583,148 @@ __device__ inline void reduce_tile(const uint32_t *__restrict__ keys, const V *_
     const int nvec = m.dim / 4;  // 16-byte fp32 vectors per gradient row
     const uint64_t gmask = (LPR == 64 ? ~0ull : ((1ull << LPR) - 1)) << (g * LPR);
     const uint64_t le_mask = lanemask_lt() | (1ull << lane);
+    const int nblk_rounds = (kBlksPerTile + nsub - 1) / nsub;
 
-    for (int q = sub; q < kBlksPerTile; q += nsub) {
+    for (int round = 0; round < nblk_rounds; ++round) {
+        const int q = sub + round * nsub;
+        const bool qv = q < kBlksPerTile;
         const int64_t p0 = ti.p_lo + static_cast<int64_t>(q) * kBlk;
         const int64_t gq = tile * kBlksPerTile + q;
+        const bool active = qv && p0 < ti.p_hi;
+        int64_t p1 = p0, lim = p0;
+        uint32_t u_before = 0, nsb = 0, cross_u = 0;
+        bool head_long = false, cross_long = false;
+        if (active) {
+            p1 = p0 + kBlk < ti.p_hi ? p0 + kBlk : ti.p_hi;
+            lim = p1 + kBlk < ti.end ? p1 + kBlk : ti.end;
+            u_before = static_cast<uint32_t>(pre.starts) + blk_starts[q];
+            nsb = blk_starts[q + 1] - blk_starts[q];
+            cross_u = u_before + nsb - 1;
+            // long = more than kBlk lookups; only the segment begun before p0
+            // and the last one begun in this block can cross a block edge
+            if (u_before > 0) head_long = seg_offsets[u_before] - seg_offsets[u_before - 1] > kBlk;
+            if (nsb > 0) cross_long = seg_offsets[cross_u + 1] - seg_offsets[cross_u] > kBlk;
+        }
         int32_t hs = -1, tsg = -1;
-        if (p0 < ti.p_hi) {
-            const int64_t p1 = p0 + kBlk < ti.p_hi ? p0 + kBlk : ti.p_hi;
-            const uint32_t u_before = static_cast<uint32_t>(pre.starts) + blk_starts[q];
-            const uint32_t nsb = blk_starts[q + 1] - blk_starts[q];
-            // long = more than kBlk lookups; the head segment (begun before p0)
-            // and the last segment begun in this block are the only candidates
-            bool head_long = false, cross_long = false;
-            const uint32_t cross_u = u_before + nsb - 1;
-            if (u_before > 0) {
-                const int64_t a = seg_offsets[u_before - 1], b = seg_offsets[u_before];
-                head_long = b - a > kBlk;
-            }
-            if (nsb > 0) {
-                const int64_t a = seg_offsets[cross_u], b = seg_offsets[cross_u + 1];
-                cross_long = b - a > kBlk;
-            }
-            const int64_t lim = p1 + kBlk < ti.end ? p1 + kBlk : ti.end;
-            for (int c0 = 0; c0 < nvec; c0 += LPR) {  // column chunks of 64 vectors (one for D <= 256)
-                const bool vact = c0 + v < nvec;
-                const float *gcol = grad_out + m.dim_off + static_cast<int64_t>(c0 + v) * 4;
-                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-                uint32_t run = u_before;  // segment starts before the current chunk
-                for (int64_t c = p0; c < lim; c += LPR) {
-                    // lane v of the group describes position c + v
-                    const int64_t pos = c + v;
-                    uint32_t key = kSentinel, bb = 0;
-                    float ww = 0.f;
-                    bool st = false, last = false;
-                    if (pos < lim) {
-                        key = keys[pos];
-                        if (key != kSentinel) {
-                            st = pos == ti.start || keys[pos - 1] != key;
-                            last = pos + 1 >= ti.end || keys[pos + 1] != key;
-                        }
-                        val_split<V>(vals[pos], bb, ww);
-                    }
-                    const uint64_t smask = __ballot(st) & gmask;
-                    const uint32_t useg = run + static_cast<uint32_t>(__popcll(smask & le_mask)) - 1u;
-                    run += static_cast<uint32_t>(__popcll(smask));
-                    bool proc = false;
-                    if (key != kSentinel && pos < lim) {
-                        if (useg < u_before) proc = pos < p1 && head_long;
-                        else if (useg < u_before + nsb) proc = pos < p1 || !(useg == cross_u && cross_long);
-                    }
-                    bool flush = false;
-                    if (proc) flush = last || (pos == p1 - 1 && (useg < u_before || (useg == cross_u && cross_long)));
-                    const uint32_t pb = bb | (proc ? kTopBit : 0u);
-                    const uint32_t pu = useg | (flush ? kTopBit : 0u);
-                    // does a short segment run on past this chunk?
-                    const bool cont = __shfl(proc && !last ? 1 : 0, g * LPR + LPR - 1) != 0;
-#pragma unroll
-                    for (int s0 = 0; s0 < LPR; s0 += U) {
-                        float4 row[U];
-                        uint32_t fb[U], fu[U];
-                        float wv[U];
-#pragma unroll
-                        for (int uu = 0; uu < U; ++uu) {
-                            const int src = g * LPR + s0 + uu;
-                            fb[uu] = __shfl(pb, src);
-                            fu[uu] = __shfl(pu, src);
-                            wv[uu] = sizeof(V) == 8 ? __shfl(ww, src) : 1.0f;
-                            row[uu] = make_float4(0.f, 0.f, 0.f, 0.f);
-                            if ((fb[uu] & kTopBit) && vact)
-                                row[uu] = *reinterpret_cast<const float4 *>(
-                                    gcol + static_cast<int64_t>(fb[uu] & ~kTopBit) * total_dim);
-                        }
-#pragma unroll
-                        for (int uu = 0; uu < U; ++uu) {
-                            if (!(fb[uu] & kTopBit)) continue;
-                            acc.x = __builtin_fmaf(wv[uu], row[uu].x, acc.x);
-                            acc.y = __builtin_fmaf(wv[uu], row[uu].y, acc.y);
-                            acc.z = __builtin_fmaf(wv[uu], row[uu].z, acc.z);
-                            acc.w = __builtin_fmaf(wv[uu], row[uu].w, acc.w);
-                            if (fu[uu] & kTopBit) {
-                                const uint32_t u = fu[uu] & ~kTopBit;
-                                float *dst;
-                                if (u < u_before) {
-                                    dst = partials + (2 * gq) * max_dim;
-                                    hs = static_cast<int32_t>(u);
-                                } else if (u == cross_u && cross_long) {
-                                    dst = partials + (2 * gq + 1) * max_dim;
-                                    tsg = static_cast<int32_t>(u);
-                                } else {
-                                    dst = grad_rows + static_cast<int64_t>(pre.dimsum) +
-                                          static_cast<int64_t>(u - static_cast<uint32_t>(pre.starts)) * m.dim;
-                                }
-                                if (vact) store4(dst + static_cast<int64_t>(c0 + v) * 4, acc);
-                                acc = make_float4(0.f, 0.f, 0.f, 0.f);
-                            }
-                        }
-                    }
-                    if (c + LPR >= p1 && !cont) break;
+        for (int c0 = 0; c0 < nvec; c0 += LPR) {  // column chunks of 64 vectors (one for D <= 256)
+            const bool vact = c0 + v < nvec;
+            const float *gcol = grad_out + m.dim_off + static_cast<int64_t>(c0 + v) * 4;
+            const float *zcol = zero_page + v * 4;
+            // raw metadata of position c + v: keys at pos-1, pos, pos+1 and its value
+            struct Raw {
+                uint32_t kp, k, kn;
+                V val;
+            };
+            auto load_raw = [&](int64_t c, Raw &r) {
+                const int64_t pos = c + v;
+                // always a readable position of this table: the clamp keeps the
+                // loads unconditional
+                const int64_t pc = active ? (pos < lim ? pos : lim - 1) : ti.start;
+                r.k = keys[pc];
+                r.kp = keys[pc > ti.start ? pc - 1 : pc];
+                r.kn = keys[pc + 1 < ti.end ? pc + 1 : pc];
+                r.val = vals[pc];
+            };
+            uint32_t run = u_before;  // segment starts before the chunk being prepared
+            // prepared metadata: pb = batch row | own bit, pu = segment id | flush bit
+            auto cook = [&](int64_t c, const Raw &r, uint32_t &pb, uint32_t &pu, float &w) {
+                const int64_t pos = c + v;
+                const bool in = active && pos < lim;
+                const bool kept = in && r.k != kSentinel;
+                const bool st = kept && (pos == ti.start || r.kp != r.k);
+                const bool last = kept && (pos + 1 >= ti.end || r.kn != r.k);
+                const uint64_t smask = __ballot(st) & gmask;
+                const uint32_t useg = run + static_cast<uint32_t>(__popcll(smask & le_mask)) - 1u;
+                run += static_cast<uint32_t>(__popcll(smask));
+                bool proc = false;
+                if (kept) {
+                    if (useg < u_before) proc = pos < p1 && head_long;
+                    else if (useg < u_before + nsb) proc = pos < p1 || !(useg == cross_u && cross_long);
                 }
+                const bool flush =
+                    proc && (last || (pos == p1 - 1 && (useg < u_before || (useg == cross_u && cross_long))));
+                uint32_t b;
+                float wl;
+                val_split<V>(r.val, b, wl);
+                // the top bit is the flag, so the id is carried only with it: a
+                // position before the group's first segment start has
+                // useg = 0xffffffff, which must not read as a flush
+                pb = proc ? (b | kTopBit) : 0u;
+                pu = flush ? (useg | kTopBit) : 0u;
+                w = proc ? wl : 0.f;
+            };
+            Raw far;
+            uint32_t cur_b, cur_u, nxt_b, nxt_u;
+            float cur_w, nxt_w;
+            load_raw(p0, far);
+            cook(p0, far, cur_b, cur_u, cur_w);
+            load_raw(p0 + LPR, far);
+            cook(p0 + LPR, far, nxt_b, nxt_u, nxt_w);
+            load_raw(p0 + 2 * LPR, far);
+
+            float4 ring[U];
+            float ring_w[kWeighted ? U : 1];
+            auto issue = [&](int src_lane, bool from_next, float4 &dst, float &dw) {
+                const int src = g * LPR + src_lane;
+                const uint32_t pb = from_next ? __shfl(nxt_b, src) : __shfl(cur_b, src);
+                const bool own = (pb & kTopBit) && vact;
+                const float *addr = own ? gcol + static_cast<int64_t>(pb & ~kTopBit) * total_dim : zcol;
+                dst = *reinterpret_cast<const float4 *>(addr);
+                if constexpr (kWeighted) {
+                    const float w = from_next ? __shfl(nxt_w, src) : __shfl(cur_w, src);
+                    dw = w;
+                }
+            };
+#pragma unroll
+            for (int sl = 0; sl < U; ++sl) issue(sl, false, ring[sl], ring_w[kWeighted ? sl : 0]);
+
+            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int64_t c = p0;; c += LPR) {
+#pragma unroll 1
+                for (int s0 = 0; s0 < LPR; s0 += U) {
+#pragma unroll
+                    for (int sl = 0; sl < U; ++sl) {
+                        const int src = g * LPR + s0 + sl;
+                        const float wv = kWeighted ? ring_w[kWeighted ? sl : 0] : 1.0f;
+                        acc.x = __builtin_fmaf(wv, ring[sl].x, acc.x);
+                        acc.y = __builtin_fmaf(wv, ring[sl].y, acc.y);
+                        acc.z = __builtin_fmaf(wv, ring[sl].z, acc.z);
+                        acc.w = __builtin_fmaf(wv, ring[sl].w, acc.w);
+                        const uint32_t pu = __shfl(cur_u, src);
+                        if (pu & kTopBit) {
+                            const uint32_t u = pu & ~kTopBit;
+                            float *dst;
+                            if (u < u_before) {
+                                dst = partials + (2 * gq) * max_dim;
+                                hs = static_cast<int32_t>(u);
+                            } else if (u == cross_u && cross_long) {
+                                dst = partials + (2 * gq + 1) * max_dim;
+                                tsg = static_cast<int32_t>(u);
+                            } else {
+                                dst = grad_rows + static_cast<int64_t>(pre.dimsum) +
+                                      static_cast<int64_t>(u - static_cast<uint32_t>(pre.starts)) * m.dim;
+                            }
+                            if (vact) store4(dst + static_cast<int64_t>(c0 + v) * 4, acc);
+                            acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                        }
+                        const int ahead = s0 + sl + U;
+                        issue(ahead & (LPR - 1), ahead >= LPR, ring[sl], ring_w[kWeighted ? sl : 0]);
+                    }
+                }
+                // does this group still own positions after this chunk?
+                const int64_t cn = c + LPR;
+                const bool own_last = (__shfl(cur_b, g * LPR + LPR - 1) & kTopBit) != 0;
+                const bool last_flush = (__shfl(cur_u, g * LPR + LPR - 1) & kTopBit) != 0;
+                const bool more = active && cn < lim && (cn < p1 || (own_last && !last_flush));
+                if (__ballot(more) == 0) break;
+                cur_b = nxt_b;
+                cur_u = nxt_u;
+                cur_w = nxt_w;
+                cook(cn + LPR, far, nxt_b, nxt_u, nxt_w);
+                load_raw(cn + 2 * LPR, far);
             }
         }
-        if (v == 0) {
+        if (qv && v == 0) {
             head_seg[gq] = hs;
             tail_seg[gq] = tsg;
         }
@@ -690,7 +743,8 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
                                                           float *__restrict__ grad_rows,
                                                           float *__restrict__ partials, int max_dim,
                                                           int32_t *__restrict__ head_seg,
-                                                          int32_t *__restrict__ tail_seg) {
+                                                          int32_t *__restrict__ tail_seg,
+                                                          const float *__restrict__ zero_page) {
     __shared__ uint32_t blk_cnt[kBlksPerTile];
     __shared__ uint32_t blk_starts[kBlksPerTile + 1];
     // consecutive tiles (one table's gradient slice) stay on one XCD's L2
@@ -705,16 +759,21 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
     if (tid < kBlksPerTile) blk_cnt[tid] = 0;
     __syncthreads();
     {
+        // all 17 keys go out before any is used (clamped, unconditional loads)
         const int64_t my = ti.p_lo + static_cast<int64_t>(tid) * kItems;
+        uint32_t k[kItems + 1];
+#pragma unroll
+        for (int q = 0; q <= kItems; ++q) {
+            int64_t pos = my + q - 1;
+            pos = pos < ti.start ? ti.start : (pos >= ti.p_hi ? ti.p_hi - 1 : pos);
+            k[q] = keys[pos];
+        }
         uint32_t ns = 0;
 #pragma unroll
         for (int q = 0; q < kItems; ++q) {
             const int64_t pos = my + q;
-            if (pos < ti.p_hi) {
-                bool kept, st;
-                seg_flags(keys, pos, ti.start, keys[pos], kept, st);
-                ns += st;
-            }
+            const bool st = pos < ti.p_hi && k[q + 1] != kSentinel && (pos == ti.start || k[q] != k[q + 1]);
+            ns += st;
         }
         if (ns) atomicAdd(&blk_cnt[tid / (kBlk / kItems)], ns);
     }
@@ -732,7 +791,7 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
 #define TBE_REDUCE_CASE(L, LPR)                                                                            \
     case L:                                                                                                \
         reduce_tile<V, LPR>(keys, vals, grad_out, seg_offsets, m, ti, pre, blk_starts, total_dim, grad_rows, \
-                            partials, max_dim, head_seg, tail_seg, tile);                                  \
+                            partials, max_dim, head_seg, tail_seg, tile, zero_page);                       \
         break;
         TBE_REDUCE_CASE(0, 1)
         TBE_REDUCE_CASE(1, 2)
@@ -902,7 +961,8 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
     hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
                        grad_idx, seg_offsets, grad_row_offsets);
     hipLaunchKernelGGL(reduce_kernel<V>, tiles, blk, 0, stream, keys[cur], vals[cur], grad_out, seg_offsets,
-                       p.meta_dev, ranges, T, ctl, tseg, p.total_dim, grad_rows, partials, p.max_dim, head, tail);
+                       p.meta_dev, ranges, T, ctl, tseg, p.total_dim, grad_rows, partials, p.max_dim, head, tail,
+                       static_cast<const float *>(p.zero_page));
     hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((L.max_blocks + kWaves - 1) / kWaves)), blk, 0,
                        stream, ranges, T, p.meta_dev, ctl, head, tail, partials, p.max_dim, grad_row_offsets,
                        grad_rows);
