@@ -21,8 +21,8 @@
 //   segments  per tile: segment starts (key change) and kept lookups; one
 //             scan over tiles; then grad_idx / seg_offsets /
 //             grad_row_offsets are written for every segment start.
-//   reduce    sorted positions are cut into fixed blocks of kBlk; a lane
-//             group walks one block in order, accumulating fp32 rows of
+//   reduce    sorted positions are cut into fixed blocks of kBlk; a wave
+//             walks one block in order, accumulating fp32 rows of
 //             grad_out; a segment that lies inside the block is written
 //             straight to its gradient row (its only writer); a segment
 //             cut by a block edge leaves a head / tail piece.
@@ -43,6 +43,9 @@ constexpr int kItems = 16;
 constexpr int kTile = kThreads * kItems;      // positions per tile
 constexpr int kBlk = 128;                     // positions per reduce block
 constexpr int kBlksPerTile = kTile / kBlk;    // 32
+constexpr int kBlksPerWave = kBlksPerTile / kWaves;  // one wave's contiguous range in the reduce
+constexpr int kSliceCols = 64;                // gradient columns per reduce work item (one per lane)
+static_assert(kBlk == 128 && kBlksPerTile <= 62, "reduce block indexing");
 constexpr int kRadixBits = 8;
 constexpr int kBuckets = 1 << kRadixBits;
 constexpr uint32_t kSentinel = 0xffffffffu;
@@ -53,12 +56,14 @@ struct Ctl {
     int32_t abort;       // malformed offsets seen (bounds check on): stop
     int32_t skip_rows;   // grad_rows too small: write no gradient row
     int64_t total_tiles;
-    int64_t pad[6];
+    int64_t total_works;  // reduce work items: (table, column slice, tile)
+    int64_t pad[5];
 };
 
-// Per-table lookup range in the sorted order and its first tile.
+// Per-table lookup range in the sorted order, its first tile and its first
+// reduce work item.
 struct Range {
-    int64_t start, end, tile_base, pad;
+    int64_t start, end, tile_base, work_base;
 };
 
 struct TileSeg {
@@ -155,7 +160,8 @@ __device__ inline uint64_t match_digit(uint32_t d, bool valid, int nbits) {
 
 // ------------------------------------------------------------------ setup
 
-__global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restrict__ offsets, int T, int64_t B,
+__global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restrict__ offsets,
+                                                         const TableMeta *__restrict__ meta, int T, int64_t B,
                                                          int64_t N, int check, Ctl *ctl, Range *ranges,
                                                          int32_t *status, int64_t *num_unique,
                                                          int64_t *seg_offsets, int64_t *grad_row_offsets) {
@@ -170,10 +176,10 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restri
         grad_row_offsets[0] = 0;
     }
     __syncthreads();
-    int64_t carry = 0;
+    int64_t carry = 0, wcarry = 0;
     for (int base = 0; base < T; base += kThreads) {
         const int t = base + tid;
-        int64_t s = 0, e = 0, nt = 0;
+        int64_t s = 0, e = 0, nt = 0, nw = 0;
         if (t < T) {
             s = offsets[static_cast<int64_t>(t) * B];
             e = offsets[static_cast<int64_t>(t + 1) * B];
@@ -182,18 +188,22 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restri
                 s = e = 0;
             }
             nt = (e - s + kTile - 1) / kTile;
+            nw = nt * ((meta[t].dim + kSliceCols - 1) / kSliceCols);
         }
-        int64_t tot;
+        int64_t tot, wtot;
         const int64_t ex = block_excl_scan<int64_t>(nt, lds, &tot);
-        if (t < T) ranges[t] = Range{s, e, carry + ex, 0};
+        const int64_t wex = block_excl_scan<int64_t>(nw, lds, &wtot);
+        if (t < T) ranges[t] = Range{s, e, carry + ex, wcarry + wex};
         carry += tot;
+        wcarry += wtot;
     }
     __syncthreads();
     if (tid == 0) {
-        ranges[T] = Range{N, N, carry, 0};
+        ranges[T] = Range{N, N, carry, wcarry};
         ctl->abort = bad;
         ctl->skip_rows = 0;
         ctl->total_tiles = bad ? 0 : carry;
+        ctl->total_works = bad ? 0 : wcarry;
         if (bad) atomicOr(status, TBE_STATUS_OFFSETS);
     }
 }
@@ -537,12 +547,12 @@ __global__ __launch_bounds__(kThreads) void seg_write_kernel(const uint32_t *__r
 // ----------------------------------------------------------------- reduce
 //
 // Sorted positions are cut into blocks of kBlk.  A segment of at most kBlk
-// lookups ("short") is summed whole, in order, by the lane group of the block
-// holding its first lookup, and written once to its gradient row.  A longer
-// segment is summed piecewise: each block it touches sums its share (a head
-// piece when the segment began earlier, a tail piece in the block where it
-// begins) and the combine kernel adds the pieces.  Short and long are told
-// apart by the segment's length, the same test wherever it is made.
+// lookups ("short") is summed whole, in order, by the wave whose range holds
+// its first lookup, and written once to its gradient row.  A longer segment
+// is summed piecewise: each block it touches sums its share (a head piece
+// when the segment began in an earlier block, a tail piece in the block where
+// it begins) and the combine kernel adds the pieces.  Short and long are told
+// apart by the segment's length, read once per block edge the segment crosses.
 
 template <typename V>
 __device__ inline void val_split(V v, uint32_t &b, float &w) {
@@ -557,202 +567,229 @@ __device__ inline void val_split(V v, uint32_t &b, float &w) {
 
 __device__ inline void store4(float *p, const float4 &a) { *reinterpret_cast<float4 *>(p) = a; }
 
-constexpr uint32_t kTopBit = 0x80000000u;
+// Global-memory (address space 1) views, so accesses through addresses
+// rebuilt from scalar registers stay global rather than flat.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+template <typename T>
+using gptr = const T __attribute__((address_space(1))) *;
+template <typename T>
+using gmut = T __attribute__((address_space(1))) *;
 
-// One lane group walks one block at a time: the positions of the segments it
-// owns, in order, as a stream with a ring of U gradient-row loads in flight.
-// Position metadata (key change flags, segment id, batch row, weight) is
-// prepared one chunk of LPR positions ahead from loads issued two chunks
-// ahead; row loads are unconditional (positions the group does not own read
-// the zero page with weight 0), so the loop's waits are for the oldest ring
-// slot only.
-template <typename V, int LPR>
-__device__ inline void reduce_tile(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
-                                   const float *__restrict__ grad_out, const int64_t *__restrict__ seg_offsets,
-                                   const TableMeta &m, const TileInfo &ti, const TileSeg &pre,
-                                   const uint32_t *blk_starts, int64_t total_dim, float *__restrict__ grad_rows,
-                                   float *__restrict__ partials, int max_dim, int32_t *__restrict__ head_seg,
-                                   int32_t *__restrict__ tail_seg, int64_t tile, const float *__restrict__ zero_page) {
-    constexpr int G = 64 / LPR;
-    constexpr int U = LPR < 8 ? LPR : 8;
-    constexpr bool kWeighted = sizeof(V) == 8;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int g = lane / LPR, v = lane % LPR;
-    const int nsub = kWaves * G;
-    const int sub = wave * G + g;
-    const int nvec = m.dim / 4;  // 16-byte fp32 vectors per gradient row
-    const uint64_t gmask = (LPR == 64 ? ~0ull : ((1ull << LPR) - 1)) << (g * LPR);
-    const uint64_t le_mask = lanemask_lt() | (1ull << lane);
-    const int nblk_rounds = (kBlksPerTile + nsub - 1) / nsub;
-
-    for (int round = 0; round < nblk_rounds; ++round) {
-        const int q = sub + round * nsub;
-        const bool qv = q < kBlksPerTile;
-        const int64_t p0 = ti.p_lo + static_cast<int64_t>(q) * kBlk;
-        const int64_t gq = tile * kBlksPerTile + q;
-        const bool active = qv && p0 < ti.p_hi;
-        int64_t p1 = p0, lim = p0;
-        uint32_t u_before = 0, nsb = 0, cross_u = 0;
-        bool head_long = false, cross_long = false;
-        if (active) {
-            p1 = p0 + kBlk < ti.p_hi ? p0 + kBlk : ti.p_hi;
-            lim = p1 + kBlk < ti.end ? p1 + kBlk : ti.end;
-            u_before = static_cast<uint32_t>(pre.starts) + blk_starts[q];
-            nsb = blk_starts[q + 1] - blk_starts[q];
-            cross_u = u_before + nsb - 1;
-            // long = more than kBlk lookups; only the segment begun before p0
-            // and the last one begun in this block can cross a block edge
-            if (u_before > 0) head_long = seg_offsets[u_before] - seg_offsets[u_before - 1] > kBlk;
-            if (nsb > 0) cross_long = seg_offsets[cross_u + 1] - seg_offsets[cross_u] > kBlk;
-        }
-        int32_t hs = -1, tsg = -1;
-        for (int c0 = 0; c0 < nvec; c0 += LPR) {  // column chunks of 64 vectors (one for D <= 256)
-            const bool vact = c0 + v < nvec;
-            const float *gcol = grad_out + m.dim_off + static_cast<int64_t>(c0 + v) * 4;
-            const float *zcol = zero_page + v * 4;
-            // raw metadata of position c + v: keys at pos-1, pos, pos+1 and its value
-            struct Raw {
-                uint32_t kp, k, kn;
-                V val;
-            };
-            auto load_raw = [&](int64_t c, Raw &r) {
-                const int64_t pos = c + v;
-                // always a readable position of this table: the clamp keeps the
-                // loads unconditional
-                const int64_t pc = active ? (pos < lim ? pos : lim - 1) : ti.start;
-                r.k = keys[pc];
-                r.kp = keys[pc > ti.start ? pc - 1 : pc];
-                r.kn = keys[pc + 1 < ti.end ? pc + 1 : pc];
-                r.val = vals[pc];
-            };
-            uint32_t run = u_before;  // segment starts before the chunk being prepared
-            // prepared metadata: pb = batch row | own bit, pu = segment id | flush bit
-            auto cook = [&](int64_t c, const Raw &r, uint32_t &pb, uint32_t &pu, float &w) {
-                const int64_t pos = c + v;
-                const bool in = active && pos < lim;
-                const bool kept = in && r.k != kSentinel;
-                const bool st = kept && (pos == ti.start || r.kp != r.k);
-                const bool last = kept && (pos + 1 >= ti.end || r.kn != r.k);
-                const uint64_t smask = __ballot(st) & gmask;
-                const uint32_t useg = run + static_cast<uint32_t>(__popcll(smask & le_mask)) - 1u;
-                run += static_cast<uint32_t>(__popcll(smask));
-                bool proc = false;
-                if (kept) {
-                    if (useg < u_before) proc = pos < p1 && head_long;
-                    else if (useg < u_before + nsb) proc = pos < p1 || !(useg == cross_u && cross_long);
-                }
-                const bool flush =
-                    proc && (last || (pos == p1 - 1 && (useg < u_before || (useg == cross_u && cross_long))));
-                uint32_t b;
-                float wl;
-                val_split<V>(r.val, b, wl);
-                // the top bit is the flag, so the id is carried only with it: a
-                // position before the group's first segment start has
-                // useg = 0xffffffff, which must not read as a flush
-                pb = proc ? (b | kTopBit) : 0u;
-                pu = flush ? (useg | kTopBit) : 0u;
-                w = proc ? wl : 0.f;
-            };
-            Raw far;
-            uint32_t cur_b, cur_u, nxt_b, nxt_u;
-            float cur_w, nxt_w;
-            load_raw(p0, far);
-            cook(p0, far, cur_b, cur_u, cur_w);
-            load_raw(p0 + LPR, far);
-            cook(p0 + LPR, far, nxt_b, nxt_u, nxt_w);
-            load_raw(p0 + 2 * LPR, far);
-
-            float4 ring[U];
-            float ring_w[kWeighted ? U : 1];
-            auto issue = [&](int src_lane, bool from_next, float4 &dst, float &dw) {
-                const int src = g * LPR + src_lane;
-                const uint32_t pb = from_next ? __shfl(nxt_b, src) : __shfl(cur_b, src);
-                const bool own = (pb & kTopBit) && vact;
-                const float *addr = own ? gcol + static_cast<int64_t>(pb & ~kTopBit) * total_dim : zcol;
-                dst = *reinterpret_cast<const float4 *>(addr);
-                if constexpr (kWeighted) {
-                    const float w = from_next ? __shfl(nxt_w, src) : __shfl(cur_w, src);
-                    dw = w;
-                }
-            };
-#pragma unroll
-            for (int sl = 0; sl < U; ++sl) issue(sl, false, ring[sl], ring_w[kWeighted ? sl : 0]);
-
-            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-            for (int64_t c = p0;; c += LPR) {
-#pragma unroll 1
-                for (int s0 = 0; s0 < LPR; s0 += U) {
-#pragma unroll
-                    for (int sl = 0; sl < U; ++sl) {
-                        const int src = g * LPR + s0 + sl;
-                        const float wv = kWeighted ? ring_w[kWeighted ? sl : 0] : 1.0f;
-                        acc.x = __builtin_fmaf(wv, ring[sl].x, acc.x);
-                        acc.y = __builtin_fmaf(wv, ring[sl].y, acc.y);
-                        acc.z = __builtin_fmaf(wv, ring[sl].z, acc.z);
-                        acc.w = __builtin_fmaf(wv, ring[sl].w, acc.w);
-                        const uint32_t pu = __shfl(cur_u, src);
-                        if (pu & kTopBit) {
-                            const uint32_t u = pu & ~kTopBit;
-                            float *dst;
-                            if (u < u_before) {
-                                dst = partials + (2 * gq) * max_dim;
-                                hs = static_cast<int32_t>(u);
-                            } else if (u == cross_u && cross_long) {
-                                dst = partials + (2 * gq + 1) * max_dim;
-                                tsg = static_cast<int32_t>(u);
-                            } else {
-                                dst = grad_rows + static_cast<int64_t>(pre.dimsum) +
-                                      static_cast<int64_t>(u - static_cast<uint32_t>(pre.starts)) * m.dim;
-                            }
-                            if (vact) store4(dst + static_cast<int64_t>(c0 + v) * 4, acc);
-                            acc = make_float4(0.f, 0.f, 0.f, 0.f);
-                        }
-                        const int ahead = s0 + sl + U;
-                        issue(ahead & (LPR - 1), ahead >= LPR, ring[sl], ring_w[kWeighted ? sl : 0]);
-                    }
-                }
-                // does this group still own positions after this chunk?
-                const int64_t cn = c + LPR;
-                const bool own_last = (__shfl(cur_b, g * LPR + LPR - 1) & kTopBit) != 0;
-                const bool last_flush = (__shfl(cur_u, g * LPR + LPR - 1) & kTopBit) != 0;
-                const bool more = active && cn < lim && (cn < p1 || (own_last && !last_flush));
-                if (__ballot(more) == 0) break;
-                cur_b = nxt_b;
-                cur_u = nxt_u;
-                cur_w = nxt_w;
-                cook(cn + LPR, far, nxt_b, nxt_u, nxt_w);
-                load_raw(cn + 2 * LPR, far);
-            }
-        }
-        if (qv && v == 0) {
-            head_seg[gq] = hs;
-            tail_seg[gq] = tsg;
-        }
+// Loads NV consecutive floats (16, 8 or 4 bytes) at byte offset off from a
+// wave-uniform base into d.
+template <int NV>
+__device__ inline void load_cols(uint64_t base, uint32_t off, float (&d)[NV]) {
+    // a fresh 32-bit offset per access keeps the scalar-base + vector-offset
+    // addressing form (a loop-invariant offset would be widened and hoisted)
+    asm volatile("" : "+v"(off));
+    const gptr<char> p = reinterpret_cast<gptr<char>>(base) + off;
+    if constexpr (NV == 4) {
+        const f32x4 x = *reinterpret_cast<gptr<f32x4>>(p);
+        d[0] = x.x; d[1] = x.y; d[2] = x.z; d[3] = x.w;
+    } else if constexpr (NV == 2) {
+        const f32x2 x = *reinterpret_cast<gptr<f32x2>>(p);
+        d[0] = x.x; d[1] = x.y;
+    } else {
+        d[0] = *reinterpret_cast<gptr<float>>(p);
     }
 }
 
+// Streaming store of NV floats: gradient rows are written once and never
+// read here, so they should not displace grad_out lines from the caches.
+template <int NV>
+__device__ inline void store_cols(uint64_t base, uint32_t off, const float (&s)[NV]) {
+    asm volatile("" : "+v"(off));
+    const gmut<char> p = reinterpret_cast<gmut<char>>(base) + off;
+    if constexpr (NV == 4) {
+        f32x4 x = {s[0], s[1], s[2], s[3]};
+        __builtin_nontemporal_store(x, reinterpret_cast<gmut<f32x4>>(p));
+    } else if constexpr (NV == 2) {
+        f32x2 x = {s[0], s[1]};
+        __builtin_nontemporal_store(x, reinterpret_cast<gmut<f32x2>>(p));
+    } else {
+        __builtin_nontemporal_store(s[0], reinterpret_cast<gmut<float>>(p));
+    }
+}
+
+__device__ inline uint32_t rl(uint32_t x, int l) {
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x), l));
+}
+
+__device__ inline uint64_t rl64(uint64_t a, int l) {
+    const uint64_t lo = rl(static_cast<uint32_t>(a), l), hi = rl(static_cast<uint32_t>(a >> 32), l);
+    return (hi << 32) | lo;
+}
+
+__device__ inline uint32_t uni(uint32_t x) {
+    return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(x)));
+}
+
+// Index of the highest set bit of a nonzero mask.
+__device__ inline int top_bit(uint64_t m) { return 63 - __clzll(static_cast<long long>(m)); }
+
+// Per-tile facts the reduce waves share.
+struct TileEdges {
+    uint64_t long_mask;                 // bit e: block edge e lies inside a long segment
+    uint32_t starts[kBlksPerTile + 1];  // segment starts in the tile before block e
+    uint32_t pad[5];
+};
+static_assert(sizeof(TileEdges) % 16 == 0, "TileEdges layout");
+
+constexpr int kRing = 32;  // row loads in flight per reduce wave
+
+// One wave walks one contiguous range of positions (kBlksPerWave blocks) in
+// order for one slice of kSliceCols gradient columns, one position per step
+// with the whole wave on that position's slice (one column per lane).
+// Per-position metadata (row address, destination address, weight, flush
+// flag) is prepared by one lane per position, 64 positions at a time, one
+// chunk ahead, from key / value loads issued two chunks ahead; every step then
+// moves its position's values into scalar registers, so addressing and the
+// flush test are uniform.  A ring of kRing row loads stays in flight;
+// positions the wave does not own read the zero page with weight 0.
 template <typename V>
-__global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__restrict__ keys,
-                                                          const V *__restrict__ vals,
-                                                          const float *__restrict__ grad_out,
-                                                          const int64_t *__restrict__ seg_offsets,
-                                                          const TableMeta *__restrict__ meta,
-                                                          const Range *__restrict__ ranges, int T,
-                                                          const Ctl *__restrict__ ctl,
-                                                          const TileSeg *__restrict__ tseg, int64_t total_dim,
-                                                          float *__restrict__ grad_rows,
-                                                          float *__restrict__ partials, int max_dim,
-                                                          int32_t *__restrict__ head_seg,
-                                                          int32_t *__restrict__ tail_seg,
-                                                          const float *__restrict__ zero_page) {
+__device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
+                                   const float *__restrict__ grad_out, const TableMeta &m, const TileInfo &ti,
+                                   const TileSeg &pre, const TileEdges &te, int64_t total_dim,
+                                   float *__restrict__ grad_rows, float *__restrict__ partials, int max_dim,
+                                   int64_t tile, int c0, const float *__restrict__ zero_page) {
+    constexpr int U = kRing;
+    constexpr bool kWeighted = sizeof(V) == 8;
+    const int lane = threadIdx.x & 63;
+    const int wave = static_cast<int>(uni(threadIdx.x >> 6));
+    const uint64_t le_mask = lanemask_lt() | (1ull << lane);
+
+    const int q0 = wave * kBlksPerWave;  // first block of the range
+    const int64_t r0 = ti.p_lo + static_cast<int64_t>(q0) * kBlk;
+    if (r0 >= ti.p_hi) return;
+    const int64_t r1 = r0 + kBlksPerWave * kBlk < ti.p_hi ? r0 + kBlksPerWave * kBlk : ti.p_hi;
+    // a short segment begun in the range is finished past its end
+    const int64_t lim = r1 + kBlk < ti.end ? r1 + kBlk : ti.end;
+    const uint64_t long_mask = te.long_mask;
+    const bool long_r0 = (long_mask >> q0) & 1ull;
+    const int q1 = static_cast<int>((r1 - ti.p_lo + kBlk - 1) / kBlk);
+    const bool long_r1 = r1 < ti.end && ((long_mask >> q1) & 1ull);
+    const uint32_t u_r0 = static_cast<uint32_t>(pre.starts) + te.starts[q0];
+    const int64_t part0 = 2 * (tile * kBlksPerTile) * max_dim;
+
+    const int col = c0 + lane;
+    const bool vact = col < m.dim;
+    const uint32_t voff = vact ? static_cast<uint32_t>(lane * 4) : 0u;  // bytes
+    const float *const gbase = grad_out + m.dim_off + c0;
+    float *const row_base = grad_rows + static_cast<int64_t>(pre.dimsum) + c0;
+    float *const part_base = partials + part0 + c0;
+    struct Raw {
+        uint32_t kp, k, kn;
+        V val;
+    };
+    // keys at pos-1, pos, pos+1 and the value of position c + lane, clamped
+    // to a readable position of this table
+    auto load_raw = [&](int64_t c, Raw &r) {
+        const int64_t pos = c + lane;
+        const int64_t pc = pos < lim ? pos : lim - 1;
+        r.k = keys[pc];
+        r.kp = keys[pc > ti.start ? pc - 1 : pc];
+        r.kn = keys[pc + 1 < ti.end ? pc + 1 : pc];
+        r.val = vals[pc];
+    };
+    uint32_t run = u_r0;          // segments begun before the chunk being prepared
+    int64_t run_start = r0 - 1;   // start of the segment open at that chunk (before r0: unknown)
+    struct Cooked {
+        uint64_t addr;   // gradient row slice to add, or the zero page
+        uint64_t dst;    // where the running sum goes when this step flushes
+        float w;         // weight (0 where not owned)
+        uint64_t fmask;  // steps that end a piece or a segment
+        uint64_t pmask;  // positions the wave owns
+    };
+    auto cook = [&](int64_t c, const Raw &r, Cooked &o) {
+        const int64_t pos = c + lane;
+        const bool kept = pos < lim && r.k != kSentinel;
+        const bool st = kept && (pos == ti.start || r.kp != r.k);
+        const bool last = kept && (pos + 1 >= ti.end || r.kn != r.k);
+        const uint64_t smask = __ballot(st);
+        const uint64_t lm = smask & le_mask;
+        const uint32_t useg = run + static_cast<uint32_t>(__popcll(lm)) - 1u;
+        const int64_t seg_start = lm ? c + top_bit(lm) : run_start;
+        run += static_cast<uint32_t>(__popcll(smask));
+        if (smask) run_start = c + top_bit(smask);
+        const int q = static_cast<int>((pos - ti.p_lo) >> 7);  // block of pos (kBlk == 128)
+        const bool before_blk = seg_start < ti.p_lo + static_cast<int64_t>(q) * kBlk;
+        const bool in_range = seg_start >= r0;
+        const bool own = kept && (pos < r1 ? (in_range || long_r0) : (in_range && !long_r1));
+        const bool long_q = (long_mask >> q) & 1ull;
+        const bool long_q1 = (long_mask >> (q + 1)) & 1ull;
+        const bool blk_end = pos < r1 && ((pos - ti.p_lo) & (kBlk - 1)) == kBlk - 1;
+        const bool flush = own && (last || (blk_end && long_q1));
+        float *const head = part_base + (2 * q) * max_dim;
+        float *dst;
+        if (last) dst = (before_blk && long_q) ? head : row_base + static_cast<int64_t>(useg - static_cast<uint32_t>(pre.starts)) * m.dim;
+        else dst = before_blk ? head : head + max_dim;
+        uint32_t b;
+        float wl;
+        val_split<V>(r.val, b, wl);
+        const float *row = gbase + static_cast<int64_t>(b) * total_dim;
+        o.addr = reinterpret_cast<uint64_t>(own ? row : zero_page);
+        o.dst = reinterpret_cast<uint64_t>(dst);
+        o.w = own ? wl : 0.f;
+        o.fmask = __ballot(flush);
+        o.pmask = __ballot(own);
+    };
+    Raw far;
+    Cooked cur, nxt;
+    load_raw(r0, far);
+    cook(r0, far, cur);
+    load_raw(r0 + 64, far);
+    cook(r0 + 64, far, nxt);
+    load_raw(r0 + 128, far);
+
+    float ring[U][1];
+#pragma unroll
+    for (int s = 0; s < U; ++s) load_cols<1>(rl64(cur.addr, s), voff, ring[s]);
+
+    float acc[1] = {0.f};
+    for (int64_t c = r0;; c += 64) {
+#pragma unroll
+        for (int j = 0; j < 64; ++j) {
+            const int s = j % U;
+            const float w = kWeighted ? __int_as_float(static_cast<int>(rl(__float_as_uint(cur.w), j))) : 1.0f;
+            acc[0] = __builtin_fmaf(w, ring[s][0], acc[0]);
+            if ((cur.fmask >> j) & 1ull) {
+                const uint64_t dst = rl64(cur.dst, j);
+                if (vact) store_cols<1>(dst, voff, acc);
+                acc[0] = 0.f;
+            }
+            const int a = j + U;
+            if (a < 64) load_cols<1>(rl64(cur.addr, a), voff, ring[s]);
+            else load_cols<1>(rl64(nxt.addr, a - 64), voff, ring[s]);
+        }
+        // does the wave still own positions after this chunk?
+        const int64_t cn = c + 64;
+        const bool own_last = (cur.pmask >> 63) & 1ull;
+        const bool last_flush = (cur.fmask >> 63) & 1ull;
+        if (!(cn < lim && (cn < r1 || (own_last && !last_flush)))) break;
+        cur = nxt;
+        cook(cn + 64, far, nxt);
+        load_raw(cn + 128, far);
+    }
+}
+
+// Per-tile facts of the reduce, computed once for all column slices: segment
+// starts per block, which block edges lie inside a long segment (one with
+// more than kBlk lookups), and the head / tail pieces of every block (read by
+// the combine kernel).
+__global__ __launch_bounds__(kThreads) void edges_kernel(const uint32_t *__restrict__ keys,
+                                                         const int64_t *__restrict__ seg_offsets,
+                                                         const Range *__restrict__ ranges, int T,
+                                                         const Ctl *__restrict__ ctl,
+                                                         const TileSeg *__restrict__ tseg,
+                                                         TileEdges *__restrict__ edges,
+                                                         int32_t *__restrict__ head_seg,
+                                                         int32_t *__restrict__ tail_seg) {
     __shared__ uint32_t blk_cnt[kBlksPerTile];
-    __shared__ uint32_t blk_starts[kBlksPerTile + 1];
-    // consecutive tiles (one table's gradient slice) stay on one XCD's L2
-    const int64_t tile = xcd_remap(blockIdx.x, gridDim.x, kNumXcd);
+    const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->skip_rows || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
-    const TableMeta m = meta[ti.t];
     const TileSeg pre = tseg[tile];
     const int tid = threadIdx.x;
     // segment starts per block of kBlk positions (8 threads x 16 positions)
@@ -778,31 +815,80 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
         if (ns) atomicAdd(&blk_cnt[tid / (kBlk / kItems)], ns);
     }
     __syncthreads();
-    if (tid == 0) {
-        uint32_t run = 0;
-        for (int q = 0; q < kBlksPerTile; ++q) {
-            blk_starts[q] = run;
-            run += blk_cnt[q];
+    if (tid < 64) {
+        // lane e: block edge e at position p_lo + e * kBlk (e = kBlksPerTile is
+        // the tile's end).  The edge lies inside a segment when the keys on
+        // both sides match; that segment is long when it has more than kBlk
+        // lookups.
+        const int e = tid;
+        const uint32_t cnt = e < kBlksPerTile ? blk_cnt[e] : 0u;
+        const uint32_t incl = wave_incl_scan(cnt);
+        const uint32_t before = incl - cnt;  // starts in blocks < e
+        const int64_t pos = ti.p_lo + static_cast<int64_t>(e) * kBlk;
+        const bool edge = e <= kBlksPerTile;
+        const int64_t pc = pos < ti.end ? pos : ti.end - 1;
+        const uint32_t kk = keys[pc], kb = keys[pc > ti.start ? pc - 1 : pc];
+        const bool open = edge && pos > ti.start && pos < ti.end && kk != kSentinel && kk == kb;
+        const uint32_t u = static_cast<uint32_t>(pre.starts) + before - 1u;  // segment open at the edge
+        bool lng = false;
+        if (open) lng = seg_offsets[u + 1] - seg_offsets[u] > kBlk;
+        const uint64_t lmask = __ballot(lng);
+        if (edge) edges[tile].starts[e] = before;
+        if (e == 0) edges[tile].long_mask = lmask;
+        const uint32_t u_next = __shfl(u, (e + 1) & 63);
+        if (e < kBlksPerTile) {
+            const bool valid = pos < ti.p_hi;
+            const bool head = valid && lng;
+            const bool tail = valid && ((lmask >> (e + 1)) & 1ull) && cnt > 0;
+            const int64_t gq = tile * kBlksPerTile + e;
+            head_seg[gq] = head ? static_cast<int32_t>(u) : -1;
+            tail_seg[gq] = tail ? static_cast<int32_t>(u_next) : -1;
         }
-        blk_starts[kBlksPerTile] = run;
     }
-    __syncthreads();
-    switch (m.glpr_log2) {
-#define TBE_REDUCE_CASE(L, LPR)                                                                            \
-    case L:                                                                                                \
-        reduce_tile<V, LPR>(keys, vals, grad_out, seg_offsets, m, ti, pre, blk_starts, total_dim, grad_rows, \
-                            partials, max_dim, head_seg, tail_seg, tile, zero_page);                       \
-        break;
-        TBE_REDUCE_CASE(0, 1)
-        TBE_REDUCE_CASE(1, 2)
-        TBE_REDUCE_CASE(2, 4)
-        TBE_REDUCE_CASE(3, 8)
-        TBE_REDUCE_CASE(4, 16)
-        TBE_REDUCE_CASE(5, 32)
-        default:
-        TBE_REDUCE_CASE(6, 64)
-#undef TBE_REDUCE_CASE
+}
+
+// Table owning reduce work item w: the t with ranges[t].work_base <= w < ranges[t+1].work_base.
+__device__ inline int find_work_table(const Range *__restrict__ r, int T, int64_t w) {
+    int lo = 0, hi = T;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (r[mid].work_base <= w) lo = mid; else hi = mid;
     }
+    return lo;
+}
+
+// One workgroup per work item (table, column slice, tile), slice-major within
+// a table, numbered so that each XCD takes a contiguous run of work items:
+// the waves of one XCD then share one table slice of grad_out in their L2.
+template <typename V>
+__global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__restrict__ keys,
+                                                          const V *__restrict__ vals,
+                                                          const float *__restrict__ grad_out,
+                                                          const TableMeta *__restrict__ meta,
+                                                          const Range *__restrict__ ranges, int T,
+                                                          const Ctl *__restrict__ ctl,
+                                                          const TileSeg *__restrict__ tseg,
+                                                          const TileEdges *__restrict__ edges, int64_t total_dim,
+                                                          float *__restrict__ grad_rows,
+                                                          float *__restrict__ partials, int max_dim,
+                                                          const float *__restrict__ zero_page) {
+    if (ctl->skip_rows || ctl->abort) return;
+    const int64_t works = ctl->total_works;
+    if (static_cast<int64_t>(blockIdx.x) >= works) return;
+    const int64_t w = xcd_remap(blockIdx.x, works, kNumXcd);
+    const int t = find_work_table(ranges, T, w);
+    const Range r = ranges[t];
+    const int64_t ntiles = ranges[t + 1].tile_base - r.tile_base;
+    const int64_t local = w - r.work_base;
+    const int slice = static_cast<int>(local / ntiles);
+    const int64_t tile = r.tile_base + local % ntiles;
+    TileInfo ti;
+    if (!tile_info(ranges, T, tile, ti)) return;
+    const TableMeta m = meta[t];
+    const TileSeg pre = tseg[tile];
+    const TileEdges te = edges[tile];
+    reduce_wave<V>(keys, vals, grad_out, m, ti, pre, te, total_dim, grad_rows, partials, max_dim, tile,
+                   slice * kSliceCols, zero_page);
 }
 
 // Sums the pieces of every segment that crosses a block edge, in a fixed
@@ -877,8 +963,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
 // ------------------------------------------------------------- workspace
 
 struct Layout {
-    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, head, tail, partials, total;
-    int64_t max_tiles, max_blocks, hist_chunks;
+    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, edges, head, tail, partials, total;
+    int64_t max_tiles, max_blocks, max_works, hist_chunks;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -888,6 +974,7 @@ Layout layout(const Plan &p, int64_t N) {
     const size_t vb = 8;  // room for weighted values; unweighted calls use half
     L.max_tiles = (N + kTile - 1) / kTile + p.T;
     L.max_blocks = L.max_tiles * kBlksPerTile;
+    L.max_works = L.max_tiles * ((p.max_dim + kSliceCols - 1) / kSliceCols);
     L.hist_chunks = (L.max_tiles * kBuckets + kScanChunk - 1) / kScanChunk;
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -904,6 +991,7 @@ Layout layout(const Plan &p, int64_t N) {
     L.hist = take(sizeof(uint32_t) * L.max_tiles * kBuckets);
     L.sums = take(sizeof(uint32_t) * (L.hist_chunks + 1));
     L.tseg = take(sizeof(TileSeg) * L.max_tiles);
+    L.edges = take(sizeof(TileEdges) * L.max_tiles);
     L.head = take(sizeof(int32_t) * L.max_blocks);
     L.tail = take(sizeof(int32_t) * L.max_blocks);
     L.partials = take(sizeof(float) * 2 * L.max_blocks * static_cast<size_t>(p.max_dim));
@@ -923,6 +1011,7 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
     uint32_t *hist = reinterpret_cast<uint32_t *>(ws + L.hist);
     uint32_t *sums = reinterpret_cast<uint32_t *>(ws + L.sums);
     TileSeg *tseg = reinterpret_cast<TileSeg *>(ws + L.tseg);
+    TileEdges *edges = reinterpret_cast<TileEdges *>(ws + L.edges);
     int32_t *head = reinterpret_cast<int32_t *>(ws + L.head);
     int32_t *tail = reinterpret_cast<int32_t *>(ws + L.tail);
     float *partials = reinterpret_cast<float *>(ws + L.partials);
@@ -930,7 +1019,8 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
     const int T = p.T;
     const int64_t nbags = static_cast<int64_t>(T) * p.B;
 
-    hipLaunchKernelGGL(setup_kernel, dim3(1), dim3(kThreads), 0, stream, offsets, T, p.B, N, check, ctl, ranges,
+    hipLaunchKernelGGL(setup_kernel, dim3(1), dim3(kThreads), 0, stream, offsets, p.meta_dev, T, p.B, N, check, ctl,
+                       ranges,
                        status, num_unique, seg_offsets, grad_row_offsets);
     if (N == 0 || nbags == 0) return hipGetLastError();
     hipLaunchKernelGGL(keys_kernel<V>, dim3(static_cast<unsigned>((nbags + kWaves - 1) / kWaves)), dim3(kThreads),
@@ -960,9 +1050,11 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
                        grad_row_offsets, capacity, status);
     hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
                        grad_idx, seg_offsets, grad_row_offsets);
-    hipLaunchKernelGGL(reduce_kernel<V>, tiles, blk, 0, stream, keys[cur], vals[cur], grad_out, seg_offsets,
-                       p.meta_dev, ranges, T, ctl, tseg, p.total_dim, grad_rows, partials, p.max_dim, head, tail,
-                       static_cast<const float *>(p.zero_page));
+    hipLaunchKernelGGL(edges_kernel, tiles, blk, 0, stream, keys[cur], seg_offsets, ranges, T, ctl, tseg, edges, head,
+                       tail);
+    hipLaunchKernelGGL(reduce_kernel<V>, dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream, keys[cur],
+                       vals[cur], grad_out, p.meta_dev, ranges, T, ctl, tseg, edges, p.total_dim, grad_rows, partials,
+                       p.max_dim, static_cast<const float *>(p.zero_page));
     hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((L.max_blocks + kWaves - 1) / kWaves)), blk, 0,
                        stream, ranges, T, p.meta_dev, ctl, head, tail, partials, p.max_dim, grad_row_offsets,
                        grad_rows);

@@ -85,6 +85,38 @@ def test_hot_rows_and_block_edges():
     g, _ = check(spec, d)
 
 
+@pytest.mark.parametrize("fill", [0x00, 0x5A, 0xFF])
+def test_workspace_contents_ignored(fill):
+    """The workspace may hold anything on entry (here: a byte pattern, then
+    what a different call left there); outputs are bitwise the same.  The
+    first table's one long segment leaves a tile with blocks past its end."""
+    spec = workloads.small_config(5, seed=14, T=3, B=300)
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    off = d["offsets"].cpu()
+    d["indices"][int(off[0]):int(off[spec.B])] = 1
+    other = workloads.small_config(5, seed=15, T=3, B=300)
+    od = workloads.gen_all(dataclasses.replace(other, grad=True), device())
+    plan, oplan = plan_for(spec), plan_for(other)
+    need = max(tbe.backward_workspace_bytes(plan, d["N"]), tbe.backward_workspace_bytes(oplan, od["N"]))
+    ws = torch.full((need,), fill, dtype=torch.uint8, device=device())
+    status = torch.zeros(1, dtype=torch.int32, device=device())
+    first = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], workspace=ws, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    # another workload through the same workspace, then the first again
+    tbe.backward(oplan, od["grad_out"], od["indices"], od["offsets"], workspace=ws, status=status)
+    again = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], workspace=ws, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for x, y in zip(first.trimmed(), again.trimmed()):
+        assert torch.equal(x, y)
+    seg, ref, ab = oracle_backward(spec, d)
+    gidx, segs, gro, rows = first.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    assert float(oracle.summation_error(rows.numpy(), ref, ab).max()) <= GRAD_RTOL
+
+
 def test_all_tables_one_row():
     spec = dataclasses.replace(workloads.small_config(5, seed=7, T=2, B=200), rows=np.array([1, 1], np.int64))
     check(spec)
