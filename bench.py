@@ -4,8 +4,9 @@ One step = one pass of the whole path over one batch: the forward pooled
 lookup over every (bag, table) and, for the training configuration, the
 sparse backward (key build, radix sort, segments, segmented reduce).  Inputs
 are seeded synthetic draws resident in HBM before timing starts.  Prints one
-JSON line: whole-step lookups/s, the forward kernel's roofline against HBM,
-and the CPU oracle timed on a bounded sample of the same workload.
+JSON line: whole-step lookups/s, the roofline of the step's dominant kernel
+(and of the forward kernel) against HBM, per-phase backward times, and the
+CPU oracle timed on a bounded sample of the same workload.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 5]
 """
@@ -62,6 +63,50 @@ def backward_bytes(spec, N: int, U: int, grad_floats: int) -> int:
     fp32 output gradient read once, int64 row ids, segment offsets and row
     offsets written, and the fp32 gradient rows written."""
     return 8 * N + 8 * (spec.T * spec.B + 1) + 4 * spec.B * spec.total_dim + 3 * 8 * (U + 1) + 4 * grad_floats
+
+
+def reduce_bytes(spec, N: int, grad_floats: int) -> int:
+    """Algorithmic bytes of one segmented-reduce launch: each sorted lookup's
+    key and batch row (4 + 4 bytes, + 4 for its weight), the fp32 output
+    gradient read once, and the fp32 gradient rows written."""
+    return (8 + (4 if spec.weighted else 0)) * N + 4 * spec.B * spec.total_dim + 4 * grad_floats
+
+
+# Counter-derived HBM traffic per launch, with the hash of the kernel source it
+# was measured on; a figure whose source has changed since is not reported.
+KERNEL_SOURCES = {
+    "forward_kernel": ["paper_2512_23236_amd/csrc/tbe_forward.hip", "paper_2512_23236_amd/csrc/tbe_internal.h"],
+    "reduce_kernel": ["paper_2512_23236_amd/csrc/tbe_backward.hip", "paper_2512_23236_amd/csrc/tbe_internal.h"],
+}
+
+
+def source_hash(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from profiles/<kernel>_<workload>_traffic.md
+    (FETCH_SIZE and WRITE_SIZE, scaled by the copy-kernel calibration), if
+    that file was written for the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("source_sha256") != source_hash(kernel):
+        return None
+    try:
+        return int(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(spec, d, target_s: float):
@@ -168,10 +213,9 @@ def main():
         if ev is not None:
             ev[1].record()
         if training:
+            # ev[1:] also bracket the backward's phases (ev[1] opens the first)
             tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], d["weights"], workspace=workspace,
-                         status=status, outputs=grads)
-            if ev is not None:
-                ev[2].record()
+                         status=status, outputs=grads, phase_events=None if ev is None else ev[1:])
 
     for _ in range(args.warmup):
         step()
@@ -179,7 +223,8 @@ def main():
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())}")
 
-    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
+    nev = 2 + (tbe.NUM_PHASES if training else 0)
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(nev)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -188,7 +233,9 @@ def main():
     wall = time.perf_counter() - t0
     fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
     fwd_avg = float(np.mean(fwd_ms))
-    bwd_ms = [e[1].elapsed_time(e[2]) for e in evs] if training else None
+    bwd_ms = [e[1].elapsed_time(e[-1]) for e in evs] if training else None
+    phase_ms = ([[e[1 + i].elapsed_time(e[2 + i]) for e in evs] for i in range(tbe.NUM_PHASES)]
+                if training else None)
     ms_per_step = wall * 1e3 / args.steps
     N = d["N"]
     off_host = d["offsets"].cpu().numpy()
@@ -215,9 +262,11 @@ def main():
                     "ms_p90": float(np.percentile(fwd_ms, 90)), "lookups_per_s": N / (fwd_avg * 1e-3),
                     "algorithmic_bytes": fbytes, "effective_GBps": achieved,
                     "frac_of_hbm_peak": achieved / HBM_PEAK_GBS},
-        "roofline": {"bound": "hbm", "kernel": "forward_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
     }
+    workload = f"cfg{args.config}"
+    roof = {"forward_kernel": {"bound": "hbm", "kernel": "forward_kernel", "ms": fwd_avg, "achieved": achieved,
+                               "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                               "traffic": measured_traffic("forward_kernel", workload), "algorithmic_bytes": fbytes}}
     if training:
         bwd_avg = float(np.mean(bwd_ms))
         U = grads.num_unique()
@@ -227,7 +276,19 @@ def main():
                            "ms_p90": float(np.percentile(bwd_ms, 90)), "lookups_per_s": N / (bwd_avg * 1e-3),
                            "unique_rows": U, "compulsory_bytes": bbytes,
                            "effective_GBps": bbytes / (bwd_avg * 1e-3) / 1e9,
-                           "frac_of_hbm_peak": bbytes / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS}
+                           "frac_of_hbm_peak": bbytes / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                           "phases_ms": {name: float(np.mean(t)) for name, t in zip(tbe.PHASES, phase_ms)}}
+        red_ms = float(np.mean(phase_ms[tbe.PHASES.index("reduce")]))
+        rbytes = reduce_bytes(spec, N, gro_total)
+        red_gbs = rbytes / (red_ms * 1e-3) / 1e9
+        roof["reduce_kernel"] = {"bound": "hbm", "kernel": "reduce_kernel", "ms": red_ms, "achieved": red_gbs,
+                                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": red_gbs / HBM_PEAK_GBS,
+                                 "traffic": measured_traffic("reduce_kernel", workload),
+                                 "algorithmic_bytes": rbytes}
+    # the roofline of the step's dominant kernel (the longest average launch)
+    dominant = max(roof.values(), key=lambda r: r["ms"])
+    res["roofline"] = dominant
+    res["roofline_forward"] = roof["forward_kernel"]
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())}")
     if not args.no_cpu_baseline:

@@ -166,6 +166,33 @@ int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t 
                      int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                      int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream);
 
+/* Parts of tbe_backward, in launch order, for tbe_backward_timed. */
+enum tbe_backward_phase {
+    TBE_PHASE_KEYS = 0,     /* validate offsets, build sort keys and values      */
+    TBE_PHASE_SORT = 1,     /* per-table radix sort                              */
+    TBE_PHASE_SEGMENTS = 2, /* segment starts, grad_idx / offsets, block edges   */
+    TBE_PHASE_REDUCE = 3,   /* the segmented-reduce kernel alone                 */
+    TBE_PHASE_COMBINE = 4,  /* sum of the pieces of long segments                */
+    TBE_NUM_PHASES = 5
+};
+
+/*
+ * tbe_backward that also records caller-created HIP events (hipEvent_t) on
+ * the stream: phase_events[i] where phase i begins and
+ * phase_events[TBE_NUM_PHASES] after the last one, so the elapsed time between
+ * phase_events[i] and phase_events[i+1] is phase i.  Every event is recorded
+ * (phases with nothing to do take no time), and only recorded: creating,
+ * waiting on and destroying them is the caller's.  phase_events == NULL makes
+ * this tbe_backward.  A failed record returns TBE_ERR_HIP.
+ * For callers that time the parts of the backward (profilers, benchmarks).
+ */
+int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const int64_t *indices,
+                           const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+                           void *workspace, size_t workspace_bytes, float *grad_rows,
+                           int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
+                           int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream,
+                           void *const *phase_events);
+
 #ifdef __cplusplus
 }
 #endif

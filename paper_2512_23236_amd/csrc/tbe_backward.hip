@@ -50,6 +50,9 @@ constexpr int kRadixBits = 8;
 constexpr int kBuckets = 1 << kRadixBits;
 constexpr uint32_t kSentinel = 0xffffffffu;
 constexpr int kPairLevels = 12;               // pairwise-sum depth in combine
+constexpr int kCombineGroups = 2048;          // combine grid (waves loop over the tail list)
+constexpr int kKeyBags = 256;                 // bags per keys workgroup
+constexpr int kCombineBatch = 8;              // piece rows loaded at once in combine
 
 // Device control block at the start of the workspace.
 struct Ctl {
@@ -57,7 +60,8 @@ struct Ctl {
     int32_t skip_rows;   // grad_rows too small: write no gradient row
     int64_t total_tiles;
     int64_t total_works;  // reduce work items: (table, column slice, tile)
-    int64_t pad[5];
+    uint64_t n_tails;     // blocks holding the first piece of a long segment
+    int64_t pad[4];
 };
 
 // Per-table lookup range in the sorted order, its first tile and its first
@@ -204,12 +208,17 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restri
         ctl->skip_rows = 0;
         ctl->total_tiles = bad ? 0 : carry;
         ctl->total_works = bad ? 0 : wcarry;
+        ctl->n_tails = 0;
         if (bad) atomicOr(status, TBE_STATUS_OFFSETS);
     }
 }
 
 // ------------------------------------------------------------------- keys
 
+// One workgroup per run of kKeyBags consecutive bags (table-major order).  The
+// run's offsets are staged in LDS; the threads then walk the run's lookups in
+// order, 256 at a time (coalesced loads and stores), and find each lookup's
+// bag by binary search over the staged offsets.
 template <typename V>
 __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restrict__ meta,
                                                         const int64_t *__restrict__ indices,
@@ -219,27 +228,44 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
                                                         int64_t nbags, int check, Ctl *ctl,
                                                         uint32_t *__restrict__ keys, V *__restrict__ vals,
                                                         int32_t *status) {
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t k = (static_cast<int64_t>(blockIdx.x) * kWaves) + wave;
-    if (k >= nbags || ctl->abort) return;
-    const int64_t t = k / B, b = k - t * B;
-    const int64_t R = meta[t].rows;
-    int64_t s = offsets[k], e = offsets[k + 1];
+    __shared__ int64_t off[kKeyBags + 1];
+    __shared__ int bad;
+    const int tid = threadIdx.x;
+    const int64_t k0 = static_cast<int64_t>(blockIdx.x) * kKeyBags;
+    if (k0 >= nbags || ctl->abort) return;
+    const int nk = nbags - k0 < kKeyBags ? static_cast<int>(nbags - k0) : kKeyBags;
+    if (tid == 0) bad = 0;
+    for (int i = tid; i <= nk; i += kThreads) off[i] = offsets[k0 + i];
+    __syncthreads();
     if (check) {
-        const Range r = ranges[t];
-        if (s < r.start || e < s || e > r.end) {
-            if (lane == 0) {
+        // each bag lies inside its table's range, in order
+        for (int i = tid; i < nk; i += kThreads) {
+            const int64_t t = (k0 + i) / B;
+            const Range r = ranges[t];
+            const int64_t s = off[i], e = off[i + 1];
+            if (s < r.start || e < s || e > r.end) bad = 1;
+        }
+        __syncthreads();
+        if (bad) {
+            if (tid == 0) {
                 atomicOr(status, TBE_STATUS_OFFSETS);
                 atomicOr(&ctl->abort, 1);
             }
             return;
         }
     }
-    for (int64_t j = s + lane; j < e; j += 64) {
+    const int64_t first = off[0], last = off[nk];
+    for (int64_t j = first + tid; j < last; j += kThreads) {
+        int lo = 0, hi = nk;  // off[lo] <= j < off[hi]
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (off[mid] <= j) lo = mid; else hi = mid;
+        }
+        const int64_t k = k0 + lo;
+        const int64_t t = k / B, b = k - t * B;
         const int64_t idx = __builtin_nontemporal_load(indices + j);
         uint32_t key = static_cast<uint32_t>(idx);
-        if (check && (idx < 0 || idx >= R)) {
+        if (check && (idx < 0 || idx >= meta[t].rows)) {
             key = kSentinel;
             atomicOr(status, TBE_STATUS_INDEX_OOB);
         }
@@ -636,7 +662,11 @@ struct TileEdges {
 };
 static_assert(sizeof(TileEdges) % 16 == 0, "TileEdges layout");
 
-constexpr int kRing = 32;  // row loads in flight per reduce wave
+constexpr int kRing = 64;  // row loads in flight per reduce wave
+// Buffer resources: byte offsets below kBufferLimit; word 3 of an untyped
+// 32-bit-element resource.
+constexpr int64_t kBufferLimit = int64_t(1) << 31;
+constexpr int kBufferWord3 = 0x00020000;
 
 // One wave walks one contiguous range of positions (kBlksPerWave blocks) in
 // order for one slice of kSliceCols gradient columns, one position per step
@@ -647,12 +677,13 @@ constexpr int kRing = 32;  // row loads in flight per reduce wave
 // moves its position's values into scalar registers, so addressing and the
 // flush test are uniform.  A ring of kRing row loads stays in flight;
 // positions the wave does not own read the zero page with weight 0.
-template <typename V>
+template <typename V, bool kWide>
 __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
                                    const float *__restrict__ grad_out, const TableMeta &m, const TileInfo &ti,
                                    const TileSeg &pre, const TileEdges &te, int64_t total_dim,
-                                   float *__restrict__ grad_rows, float *__restrict__ partials, int max_dim,
-                                   int64_t tile, int c0, const float *__restrict__ zero_page) {
+                                   int64_t gout_elems, float *__restrict__ grad_rows,
+                                   float *__restrict__ partials, int max_dim, int64_t tile, int c0,
+                                   const float *__restrict__ zero_page) {
     constexpr int U = kRing;
     constexpr bool kWeighted = sizeof(V) == 8;
     const int lane = threadIdx.x & 63;
@@ -676,6 +707,10 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     const bool vact = col < m.dim;
     const uint32_t voff = vact ? static_cast<uint32_t>(lane * 4) : 0u;  // bytes
     const float *const gbase = grad_out + m.dim_off + c0;
+    // grad_out below 2 GiB: rows are 32-bit byte offsets from gbase into a
+    // buffer resource; a step whose position is not owned reads through a
+    // resource of length 0, which returns zeros without a memory access
+    const uint32_t gbytes = static_cast<uint32_t>((gout_elems - (m.dim_off + c0)) * 4);
     float *const row_base = grad_rows + static_cast<int64_t>(pre.dimsum) + c0;
     float *const part_base = partials + part0 + c0;
     struct Raw {
@@ -695,7 +730,7 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     uint32_t run = u_r0;          // segments begun before the chunk being prepared
     int64_t run_start = r0 - 1;   // start of the segment open at that chunk (before r0: unknown)
     struct Cooked {
-        uint64_t addr;   // gradient row slice to add, or the zero page
+        uint64_t addr;   // gradient row slice to add (zero page / byte offset, see kWide)
         uint64_t dst;    // where the running sum goes when this step flushes
         float w;         // weight (0 where not owned)
         uint64_t fmask;  // steps that end a piece or a segment
@@ -727,8 +762,12 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
         uint32_t b;
         float wl;
         val_split<V>(r.val, b, wl);
-        const float *row = gbase + static_cast<int64_t>(b) * total_dim;
-        o.addr = reinterpret_cast<uint64_t>(own ? row : zero_page);
+        if constexpr (kWide) {
+            const float *row = gbase + static_cast<int64_t>(b) * total_dim;
+            o.addr = reinterpret_cast<uint64_t>(own ? row : zero_page);
+        } else {
+            o.addr = static_cast<uint32_t>(b) * static_cast<uint32_t>(total_dim * 4);
+        }
         o.dst = reinterpret_cast<uint64_t>(dst);
         o.w = own ? wl : 0.f;
         o.fmask = __ballot(flush);
@@ -742,9 +781,23 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     cook(r0 + 64, far, nxt);
     load_raw(r0 + 128, far);
 
+    // one gradient column of the row slice of step j of a chunk
+    auto fetch = [&](const Cooked &ck, int j, float (&d)[1]) {
+        if constexpr (kWide) {
+            load_cols<1>(rl64(ck.addr, j), voff, d);
+        } else {
+            const int n = ((ck.pmask >> j) & 1ull) ? static_cast<int>(gbytes) : 0;
+            const __amdgpu_buffer_rsrc_t rs =
+                __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(gbase), 0, n, kBufferWord3);
+            // lanes past the row slice read its first column (voff), so every
+            // address stays inside grad_out
+            d[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                rs, static_cast<int>(voff), static_cast<int>(rl(static_cast<uint32_t>(ck.addr), j)), 0));
+        }
+    };
     float ring[U][1];
 #pragma unroll
-    for (int s = 0; s < U; ++s) load_cols<1>(rl64(cur.addr, s), voff, ring[s]);
+    for (int s = 0; s < U; ++s) fetch(cur, s, ring[s]);
 
     float acc[1] = {0.f};
     for (int64_t c = r0;; c += 64) {
@@ -759,8 +812,8 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
                 acc[0] = 0.f;
             }
             const int a = j + U;
-            if (a < 64) load_cols<1>(rl64(cur.addr, a), voff, ring[s]);
-            else load_cols<1>(rl64(nxt.addr, a - 64), voff, ring[s]);
+            if (a < 64) fetch(cur, a, ring[s]);
+            else fetch(nxt, a - 64, ring[s]);
         }
         // does the wave still own positions after this chunk?
         const int64_t cn = c + 64;
@@ -779,12 +832,12 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
 // the combine kernel).
 __global__ __launch_bounds__(kThreads) void edges_kernel(const uint32_t *__restrict__ keys,
                                                          const int64_t *__restrict__ seg_offsets,
-                                                         const Range *__restrict__ ranges, int T,
-                                                         const Ctl *__restrict__ ctl,
+                                                         const Range *__restrict__ ranges, int T, Ctl *ctl,
                                                          const TileSeg *__restrict__ tseg,
                                                          TileEdges *__restrict__ edges,
                                                          int32_t *__restrict__ head_seg,
-                                                         int32_t *__restrict__ tail_seg) {
+                                                         int32_t *__restrict__ tail_seg,
+                                                         int64_t *__restrict__ tail_list) {
     __shared__ uint32_t blk_cnt[kBlksPerTile];
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->skip_rows || ctl->abort) return;
@@ -836,14 +889,21 @@ __global__ __launch_bounds__(kThreads) void edges_kernel(const uint32_t *__restr
         if (edge) edges[tile].starts[e] = before;
         if (e == 0) edges[tile].long_mask = lmask;
         const uint32_t u_next = __shfl(u, (e + 1) & 63);
+        const bool valid = e < kBlksPerTile && pos < ti.p_hi;
+        const bool head = valid && lng;
+        const bool tail = valid && ((lmask >> (e + 1)) & 1ull) && cnt > 0;
+        const int64_t gq = tile * kBlksPerTile + e;
         if (e < kBlksPerTile) {
-            const bool valid = pos < ti.p_hi;
-            const bool head = valid && lng;
-            const bool tail = valid && ((lmask >> (e + 1)) & 1ull) && cnt > 0;
-            const int64_t gq = tile * kBlksPerTile + e;
             head_seg[gq] = head ? static_cast<int32_t>(u) : -1;
             tail_seg[gq] = tail ? static_cast<int32_t>(u_next) : -1;
         }
+        // append this tile's tail blocks to the combine kernel's work list
+        // (list order is free: every entry is summed and written on its own)
+        const uint64_t tmask = __ballot(tail);
+        uint64_t base = 0;
+        if (e == 0 && tmask) base = atomicAdd(&ctl->n_tails, static_cast<uint64_t>(__popcll(tmask)));
+        base = __shfl(base, 0);
+        if (tail) tail_list[base + __popcll(tmask & lanemask_lt())] = gq;
     }
 }
 
@@ -869,7 +929,7 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
                                                           const Ctl *__restrict__ ctl,
                                                           const TileSeg *__restrict__ tseg,
                                                           const TileEdges *__restrict__ edges, int64_t total_dim,
-                                                          float *__restrict__ grad_rows,
+                                                          int64_t gout_elems, float *__restrict__ grad_rows,
                                                           float *__restrict__ partials, int max_dim,
                                                           const float *__restrict__ zero_page) {
     if (ctl->skip_rows || ctl->abort) return;
@@ -887,83 +947,110 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
     const TableMeta m = meta[t];
     const TileSeg pre = tseg[tile];
     const TileEdges te = edges[tile];
-    reduce_wave<V>(keys, vals, grad_out, m, ti, pre, te, total_dim, grad_rows, partials, max_dim, tile,
-                   slice * kSliceCols, zero_page);
+    if (gout_elems * 4 < kBufferLimit)
+        reduce_wave<V, false>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
+                              max_dim, tile, slice * kSliceCols, zero_page);
+    else
+        reduce_wave<V, true>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
+                             max_dim, tile, slice * kSliceCols, zero_page);
 }
 
 // Sums the pieces of every segment that crosses a block edge, in a fixed
-// pairwise order (binary-counter summation over the pieces), and writes its
-// gradient row once.
+// pairwise order (binary-counter summation over the pieces: the tail piece of
+// the block where the segment begins, then the head pieces of the blocks that
+// follow), and writes its gradient row once.  One wave per entry of the tail
+// list, which holds the block of each such segment's tail piece.
 __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restrict__ ranges, int T,
                                                            const TableMeta *__restrict__ meta,
                                                            const Ctl *__restrict__ ctl,
                                                            const int32_t *__restrict__ head_seg,
                                                            const int32_t *__restrict__ tail_seg,
+                                                           const int64_t *__restrict__ tail_list,
                                                            const float *__restrict__ partials, int max_dim,
                                                            const int64_t *__restrict__ grad_row_offsets,
                                                            float *__restrict__ grad_rows) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t q = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
     if (ctl->skip_rows || ctl->abort) return;
     const int64_t nblk = ctl->total_tiles * kBlksPerTile;
-    if (q >= nblk) return;
-    const int32_t u = tail_seg[q];
-    if (u < 0) return;
-    const int t = find_table(ranges, T, q / kBlksPerTile);
-    const int nvec = meta[t].dim / 4;
-    float *out = grad_rows + grad_row_offsets[u];
-    for (int c0 = 0; c0 < nvec; c0 += 64) {
-        const int cv = c0 + lane;
-        const bool act = cv < nvec;
-        float4 st[kPairLevels];
-        float4 top = make_float4(0.f, 0.f, 0.f, 0.f);
-        bool top_used = false;
-        uint32_t n = 0;
-        int64_t qq = q;
-        int64_t slot = 2 * q + 1;
-        while (true) {
-            float4 x = act ? *reinterpret_cast<const float4 *>(partials + slot * max_dim + cv * 4)
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
-            bool done = false;
+    const int64_t ntail = static_cast<int64_t>(ctl->n_tails);
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kWaves + wave; i < ntail;
+         i += static_cast<int64_t>(gridDim.x) * kWaves) {
+        const int64_t q = tail_list[i];
+        const int32_t u = tail_seg[q];
+        const int t = find_table(ranges, T, q / kBlksPerTile);
+        const int nvec = meta[t].dim / 4;
+        float *out = grad_rows + grad_row_offsets[u];
+        // pieces: the tail of block q, then the heads of blocks q+1 .. q+nh
+        int64_t nh = 0;
+        for (;;) {
+            const int64_t qq = q + 1 + nh + lane;
+            const bool same = qq < nblk && head_seg[qq] == u;
+            const uint64_t run = ~__ballot(same);  // first lane that is not a head of u
+            const int c = run ? __ffsll(static_cast<long long>(run)) - 1 : 64;
+            nh += c;
+            if (c < 64) break;
+        }
+        const int64_t npieces = nh + 1;
+        for (int c0 = 0; c0 < nvec; c0 += 64) {
+            const int cv = c0 + lane;
+            const bool act = cv < nvec;
+            float4 st[kPairLevels];
+            float4 top = make_float4(0.f, 0.f, 0.f, 0.f);
+            bool top_used = false;
+            uint32_t n = 0;
+            // piece p lives in partial slot 2q+1 (p = 0) or 2(q+p) (p > 0)
+            auto slot_of = [&](int64_t pc) { return pc == 0 ? 2 * q + 1 : 2 * (q + pc); };
+            for (int64_t p0 = 0; p0 < npieces; p0 += kCombineBatch) {
+                float4 xs[kCombineBatch];
 #pragma unroll
-            for (int l = 0; l < kPairLevels; ++l) {
-                if (!done) {
-                    if ((n >> l) & 1u) {
-                        x = make_float4(st[l].x + x.x, st[l].y + x.y, st[l].z + x.z, st[l].w + x.w);
-                    } else {
-                        st[l] = x;
-                        done = true;
+                for (int r = 0; r < kCombineBatch; ++r) {
+                    const int64_t pc = p0 + r < npieces ? p0 + r : npieces - 1;  // clamped, unconditional
+                    xs[r] = act ? *reinterpret_cast<const float4 *>(partials + slot_of(pc) * max_dim + cv * 4)
+                                : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+#pragma unroll
+                for (int r = 0; r < kCombineBatch; ++r) {
+                    if (p0 + r >= npieces) break;
+                    float4 x = xs[r];
+                    bool done = false;
+#pragma unroll
+                    for (int l = 0; l < kPairLevels; ++l) {
+                        if (!done) {
+                            if ((n >> l) & 1u) {
+                                x = make_float4(st[l].x + x.x, st[l].y + x.y, st[l].z + x.z, st[l].w + x.w);
+                            } else {
+                                st[l] = x;
+                                done = true;
+                            }
+                        }
                     }
+                    if (!done) {
+                        top = top_used ? make_float4(top.x + x.x, top.y + x.y, top.z + x.z, top.w + x.w) : x;
+                        top_used = true;
+                    }
+                    ++n;
                 }
             }
-            if (!done) {
-                top = top_used ? make_float4(top.x + x.x, top.y + x.y, top.z + x.z, top.w + x.w) : x;
-                top_used = true;
-            }
-            ++n;
-            ++qq;
-            if (qq >= nblk || head_seg[qq] != u) break;
-            slot = 2 * qq;
-        }
-        float4 sum = top;
-        bool have = top_used;
+            float4 sum = top;
+            bool have = top_used;
 #pragma unroll
-        for (int l = kPairLevels - 1; l >= 0; --l) {
-            if ((n >> l) & 1u) {
-                sum = have ? make_float4(sum.x + st[l].x, sum.y + st[l].y, sum.z + st[l].z, sum.w + st[l].w)
-                           : st[l];
-                have = true;
+            for (int l = kPairLevels - 1; l >= 0; --l) {
+                if ((n >> l) & 1u) {
+                    sum = have ? make_float4(sum.x + st[l].x, sum.y + st[l].y, sum.z + st[l].z, sum.w + st[l].w)
+                               : st[l];
+                    have = true;
+                }
             }
+            if (act) store4(out + cv * 4, sum);
         }
-        if (act) store4(out + cv * 4, sum);
     }
 }
 
 // ------------------------------------------------------------- workspace
 
 struct Layout {
-    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, edges, head, tail, partials, total;
+    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, edges, head, tail, tails, partials, total;
     int64_t max_tiles, max_blocks, max_works, hist_chunks;
 };
 
@@ -994,6 +1081,7 @@ Layout layout(const Plan &p, int64_t N) {
     L.edges = take(sizeof(TileEdges) * L.max_tiles);
     L.head = take(sizeof(int32_t) * L.max_blocks);
     L.tail = take(sizeof(int32_t) * L.max_blocks);
+    L.tails = take(sizeof(int64_t) * L.max_blocks);
     L.partials = take(sizeof(float) * 2 * L.max_blocks * static_cast<size_t>(p.max_dim));
     L.total = o;
     return L;
@@ -1003,7 +1091,7 @@ template <typename V>
 hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, const int64_t *offsets,
                int64_t N, const float *weights, char *ws, const Layout &L, float *grad_rows, int64_t capacity,
                int64_t *grad_idx, int64_t *seg_offsets, int64_t *grad_row_offsets, int64_t *num_unique,
-               int32_t *status, hipStream_t stream) {
+               int32_t *status, hipStream_t stream, void *const *phase_events) {
     Ctl *ctl = reinterpret_cast<Ctl *>(ws + L.ctl);
     Range *ranges = reinterpret_cast<Range *>(ws + L.ranges);
     uint32_t *keys[2] = {reinterpret_cast<uint32_t *>(ws + L.keys0), reinterpret_cast<uint32_t *>(ws + L.keys1)};
@@ -1014,16 +1102,30 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
     TileEdges *edges = reinterpret_cast<TileEdges *>(ws + L.edges);
     int32_t *head = reinterpret_cast<int32_t *>(ws + L.head);
     int32_t *tail = reinterpret_cast<int32_t *>(ws + L.tail);
+    int64_t *tails = reinterpret_cast<int64_t *>(ws + L.tails);
     float *partials = reinterpret_cast<float *>(ws + L.partials);
     const int check = p.bounds_check;
     const int T = p.T;
     const int64_t nbags = static_cast<int64_t>(T) * p.B;
+    // phase boundary events (tbe_backward_timed); `marked` phases are recorded
+    int marked = 0;
+    auto mark = [&](int upto) -> hipError_t {
+        for (; phase_events && marked <= upto; ++marked) {
+            const hipError_t e = hipEventRecord(static_cast<hipEvent_t>(phase_events[marked]), stream);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    };
+    hipError_t me = mark(TBE_PHASE_KEYS);
+    if (me != hipSuccess) return me;
 
     hipLaunchKernelGGL(setup_kernel, dim3(1), dim3(kThreads), 0, stream, offsets, p.meta_dev, T, p.B, N, check, ctl,
-                       ranges,
-                       status, num_unique, seg_offsets, grad_row_offsets);
-    if (N == 0 || nbags == 0) return hipGetLastError();
-    hipLaunchKernelGGL(keys_kernel<V>, dim3(static_cast<unsigned>((nbags + kWaves - 1) / kWaves)), dim3(kThreads),
+                       ranges, status, num_unique, seg_offsets, grad_row_offsets);
+    if (N == 0 || nbags == 0) {
+        const hipError_t e = hipGetLastError();
+        return e != hipSuccess ? e : mark(TBE_NUM_PHASES);
+    }
+    hipLaunchKernelGGL(keys_kernel<V>, dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)), dim3(kThreads),
                        0, stream, p.meta_dev, indices, offsets, weights, ranges, p.B, nbags, check, ctl, keys[0],
                        vals[0], status);
     // bits: every valid local key, and the drop key's low bits above them
@@ -1032,6 +1134,7 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
     int bits = 1;
     while (bits < 32 && (int64_t(1) << bits) <= max_rows) ++bits;
     const dim3 tiles(static_cast<unsigned>(L.max_tiles)), blk(kThreads);
+    if ((me = mark(TBE_PHASE_SORT)) != hipSuccess) return me;
     int cur = 0;
     for (int shift = 0; shift < bits; shift += kRadixBits) {
         const int nb = bits - shift < kRadixBits ? bits - shift : kRadixBits;
@@ -1045,20 +1148,26 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
                            vals[cur ^ 1], hist, ranges, T, ctl, shift, nb);
         cur ^= 1;
     }
+    if ((me = mark(TBE_PHASE_SEGMENTS)) != hipSuccess) return me;
     hipLaunchKernelGGL(seg_count_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg);
     hipLaunchKernelGGL(seg_scan_kernel, dim3(1), blk, 0, stream, tseg, ctl, num_unique, seg_offsets,
                        grad_row_offsets, capacity, status);
     hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
                        grad_idx, seg_offsets, grad_row_offsets);
     hipLaunchKernelGGL(edges_kernel, tiles, blk, 0, stream, keys[cur], seg_offsets, ranges, T, ctl, tseg, edges, head,
-                       tail);
+                       tail, tails);
+    if ((me = mark(TBE_PHASE_REDUCE)) != hipSuccess) return me;
     hipLaunchKernelGGL(reduce_kernel<V>, dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream, keys[cur],
-                       vals[cur], grad_out, p.meta_dev, ranges, T, ctl, tseg, edges, p.total_dim, grad_rows, partials,
-                       p.max_dim, static_cast<const float *>(p.zero_page));
-    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((L.max_blocks + kWaves - 1) / kWaves)), blk, 0,
-                       stream, ranges, T, p.meta_dev, ctl, head, tail, partials, p.max_dim, grad_row_offsets,
-                       grad_rows);
-    return hipGetLastError();
+                       vals[cur], grad_out, p.meta_dev, ranges, T, ctl, tseg, edges, p.total_dim, p.B * p.total_dim,
+                       grad_rows, partials, p.max_dim, static_cast<const float *>(p.zero_page));
+    if ((me = mark(TBE_PHASE_COMBINE)) != hipSuccess) return me;
+    // the tail list is short (one entry per segment longer than a block)
+    const int64_t combine_groups = (L.max_blocks + kWaves - 1) / kWaves < kCombineGroups
+                                       ? (L.max_blocks + kWaves - 1) / kWaves : kCombineGroups;
+    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>(combine_groups)), blk, 0, stream, ranges, T,
+                       p.meta_dev, ctl, head, tail, tails, partials, p.max_dim, grad_row_offsets, grad_rows);
+    const hipError_t e = hipGetLastError();
+    return e != hipSuccess ? e : mark(TBE_NUM_PHASES);
 }
 
 }  // namespace
@@ -1068,15 +1177,17 @@ size_t backward_workspace_bytes(const Plan &p, int64_t num_indices) { return lay
 hipError_t launch_backward(const Plan &p, const float *grad_out, const int64_t *indices, const int64_t *offsets,
                            int64_t num_indices, const float *weights, void *workspace, size_t workspace_bytes,
                            float *grad_rows, int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
-                           int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, hipStream_t stream) {
+                           int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, hipStream_t stream,
+                           void *const *phase_events) {
     (void)workspace_bytes;
     const Layout L = layout(p, num_indices);
     char *ws = static_cast<char *>(workspace);
     if (weights)
         return run<uint64_t>(p, grad_out, indices, offsets, num_indices, weights, ws, L, grad_rows,
-                             grad_rows_capacity, grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream);
+                             grad_rows_capacity, grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream,
+                             phase_events);
     return run<uint32_t>(p, grad_out, indices, offsets, num_indices, nullptr, ws, L, grad_rows, grad_rows_capacity,
-                         grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream);
+                         grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream, phase_events);
 }
 
 }  // namespace tbe

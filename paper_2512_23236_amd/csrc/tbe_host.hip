@@ -182,6 +182,17 @@ int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t 
                      void *workspace, size_t workspace_bytes, float *grad_rows,
                      int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                      int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream) {
+    return tbe_backward_timed(plan, grad_out, indices, offsets, num_indices, per_sample_weights, workspace,
+                              workspace_bytes, grad_rows, grad_rows_capacity, grad_idx, seg_offsets,
+                              grad_row_offsets, num_unique, status, stream, nullptr);
+}
+
+int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const int64_t *indices,
+                           const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+                           void *workspace, size_t workspace_bytes, float *grad_rows,
+                           int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
+                           int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream,
+                           void *const *phase_events) {
     const tbe::Plan *p = plan_of(plan);
     if (!p) return TBE_ERR_NULL;
     // sorted positions and segment ids are carried in 32 bits on the device
@@ -210,7 +221,7 @@ int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t 
                                               per_sample_weights, workspace, workspace_bytes,
                                               grad_rows, grad_rows_capacity, grad_idx, seg_offsets,
                                               grad_row_offsets, num_unique, status,
-                                              static_cast<hipStream_t>(stream));
+                                              static_cast<hipStream_t>(stream), phase_events);
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
 }
 

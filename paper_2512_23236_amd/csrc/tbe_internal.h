@@ -56,7 +56,7 @@ hipError_t launch_backward(const Plan &p, const float *grad_out, const int64_t *
                            void *workspace, size_t workspace_bytes, float *grad_rows,
                            int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                            int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status,
-                           hipStream_t stream);
+                           hipStream_t stream, void *const *phase_events);
 
 // Logical workgroup id under round-robin dispatch of workgroups over the
 // XCDs: workgroup w runs on XCD w % num_xcd, and the XCDs are given

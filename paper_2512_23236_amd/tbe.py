@@ -22,6 +22,8 @@ F32, F16, BF16 = 0, 1, 2
 DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 
 STATUS_INDEX_OOB, STATUS_OFFSETS, STATUS_CAPACITY = 1, 2, 4
+PHASES = ("keys", "sort", "segments", "reduce", "combine")  # tbe_backward_phase order
+NUM_PHASES = len(PHASES)
 
 _lib = None
 
@@ -68,6 +70,8 @@ def _load():
         lib.tbe_backward_workspace_bytes.argtypes = [P, i64, P]
         lib.tbe_backward.restype = i32
         lib.tbe_backward.argtypes = [P, P, P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P, P, P]
+        lib.tbe_backward_timed.restype = i32
+        lib.tbe_backward_timed.argtypes = [P, P, P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P, P, P, P]
         if lib.tbe_abi_version() != ABI_VERSION:
             raise ImportError(f"libtbe ABI {lib.tbe_abi_version()} != {ABI_VERSION}")
         _lib = lib
@@ -203,8 +207,12 @@ class SparseGrad:
 def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets: torch.Tensor,
              per_sample_weights: Optional[torch.Tensor] = None, grad_rows_capacity: Optional[int] = None,
              workspace: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
-             outputs: Optional[SparseGrad] = None) -> SparseGrad:
-    """Sparse gradient of the tables (queued on the current stream)."""
+             outputs: Optional[SparseGrad] = None,
+             phase_events: Optional[Sequence[torch.cuda.Event]] = None) -> SparseGrad:
+    """Sparse gradient of the tables (queued on the current stream).
+
+    phase_events: NUM_PHASES + 1 events recorded at the phase boundaries of
+    the backward (tbe_backward_timed); event i .. i+1 brackets phase i."""
     N = indices.numel()
     _dev_tensor(grad_out, torch.float32, "grad_out", plan)
     _dev_tensor(indices, torch.int64, "indices", plan)
@@ -232,10 +240,19 @@ def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets:
     need = backward_workspace_bytes(plan, N)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    rc = _load().tbe_backward(plan.handle, _ptr(grad_out), _ptr(indices), _ptr(offsets), N,
-                              _ptr(per_sample_weights), _ptr(workspace), workspace.numel(),
-                              _ptr(outputs.grad_rows), cap, _ptr(outputs.grad_idx), _ptr(outputs.seg_offsets),
-                              _ptr(outputs.grad_row_offsets), _ptr(outputs.num_unique_dev), _ptr(status),
-                              _stream(dev))
-    _check(rc, "tbe_backward")
+    args = (plan.handle, _ptr(grad_out), _ptr(indices), _ptr(offsets), N, _ptr(per_sample_weights),
+            _ptr(workspace), workspace.numel(), _ptr(outputs.grad_rows), cap, _ptr(outputs.grad_idx),
+            _ptr(outputs.seg_offsets), _ptr(outputs.grad_row_offsets), _ptr(outputs.num_unique_dev), _ptr(status),
+            _stream(dev))
+    if phase_events is None:
+        _check(_load().tbe_backward(*args), "tbe_backward")
+    else:
+        if len(phase_events) != NUM_PHASES + 1:
+            raise ValueError(f"phase_events needs {NUM_PHASES + 1} events")
+        handles = (ctypes.c_void_p * len(phase_events))()
+        for i, ev in enumerate(phase_events):
+            if not ev.cuda_event:  # torch creates the HIP event on first use
+                ev.record()
+            handles[i] = ev.cuda_event
+        _check(_load().tbe_backward_timed(*args, handles), "tbe_backward_timed")
     return outputs

@@ -82,6 +82,7 @@ def test_null_arguments_rejected_without_a_device():
     n = ctypes.c_size_t()
     assert lib.tbe_backward_workspace_bytes(None, 10, ctypes.byref(n)) == -1
     assert lib.tbe_backward(None, *([None] * 3), 0, None, None, 0, None, 0, *([None] * 6)) == -1
+    assert lib.tbe_backward_timed(None, *([None] * 3), 0, None, None, 0, None, 0, *([None] * 7)) == -1
     assert lib.tbe_plan_destroy(None) == 0
     assert lib.tbe_plan_info(None, None, None, None) == -1
 

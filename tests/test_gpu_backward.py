@@ -117,6 +117,26 @@ def test_workspace_contents_ignored(fill):
     assert float(oracle.summation_error(rows.numpy(), ref, ab).max()) <= GRAD_RTOL
 
 
+def test_phase_events():
+    """tbe_backward_timed gives the same outputs as tbe_backward and records
+    every phase boundary in order."""
+    spec = workloads.small_config(5, seed=17, T=3, B=300)
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    plan = plan_for(spec)
+    status = torch.zeros(1, dtype=torch.int32, device=device())
+    plain = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], status=status)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(tbe.NUM_PHASES + 1)]
+    timed = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], status=status, phase_events=evs)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for x, y in zip(plain.trimmed(), timed.trimmed()):
+        assert torch.equal(x, y)
+    times = [evs[i].elapsed_time(evs[i + 1]) for i in range(tbe.NUM_PHASES)]
+    assert all(t >= 0 for t in times), times
+    with pytest.raises(ValueError):
+        tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], status=status, phase_events=evs[:2])
+
+
 def test_all_tables_one_row():
     spec = dataclasses.replace(workloads.small_config(5, seed=7, T=2, B=200), rows=np.array([1, 1], np.int64))
     check(spec)
@@ -194,6 +214,16 @@ def test_workspace_too_small_rejected():
     ws = torch.empty(16, dtype=torch.uint8, device=device())
     with pytest.raises(tbe.TBEError):
         tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], workspace=ws)
+
+
+@pytest.mark.slow
+def test_grad_out_past_2gib():
+    """grad_out of more than 2 GiB (rows addressed with 64-bit pointers
+    instead of 32-bit buffer offsets): one-hot bags over two wide tables."""
+    base = workloads.small_config(2, seed=16, T=2, B=220000)
+    spec = dataclasses.replace(base, dims=np.array([1536, 1024], np.int32), name="bwd-wide")
+    assert spec.B * int(spec.dims.sum()) * 4 >= 2 ** 31
+    check(spec)
 
 
 @pytest.mark.slow
