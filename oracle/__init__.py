@@ -36,6 +36,8 @@ def _load():
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         lib.oracle_forward.restype = ctypes.c_int
         lib.oracle_forward.argtypes = [i32, i64, P, P, i32, P, P, P, i64, P, P, P]
+        lib.oracle_weight_grad.restype = ctypes.c_int
+        lib.oracle_weight_grad.argtypes = [i32, i64, P, P, i32, P, P, P, i64, P, P, P]
         lib.oracle_backward_segments.restype = ctypes.c_int
         lib.oracle_backward_segments.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, P, P]
         lib.oracle_backward_rows.restype = ctypes.c_int
@@ -90,6 +92,28 @@ def forward(rows: Sequence[int], dims: Sequence[int], dtype: str, tables: Sequen
     if rc != 0:
         raise OracleError(f"oracle_forward returned {rc}")
     return out, absout
+
+
+def weight_grad(rows: Sequence[int], dims: Sequence[int], dtype: str, tables: Sequence[np.ndarray],
+                indices, offsets, B: int, grad_out):
+    """Gradient of the pooled output with respect to the per-sample weights,
+    in binary64: grad_w[j] = <grad_out[b(j), slice of t(j)], W_t[idx_j]>.
+    Tables as in forward(); grad_out is float32 [B, total_dim].  Returns
+    (grad_w, abs_terms), each [N] float64."""
+    lib = _load()
+    T = len(rows)
+    rows_a, dims_a = _c(rows, np.int64), _c(dims, np.int32)
+    tabs = [np.ascontiguousarray(t) for t in tables]
+    ptrs = (ctypes.c_void_p * T)(*[t.ctypes.data for t in tabs])
+    idx, off = _c(indices, np.int64), _c(offsets, np.int64)
+    g = _c(grad_out, np.float32)
+    gw = np.zeros(idx.size, np.float64)
+    ab = np.zeros(idx.size, np.float64)
+    rc = lib.oracle_weight_grad(T, B, _p(rows_a), _p(dims_a), DTYPE_CODES[dtype], ptrs, _p(idx), _p(off),
+                                idx.size, _p(g), _p(gw), _p(ab))
+    if rc != 0:
+        raise OracleError(f"oracle_weight_grad returned {rc}")
+    return gw, ab
 
 
 def backward_segments(rows, dims, indices, offsets, B: int):

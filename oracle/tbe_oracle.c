@@ -33,6 +33,9 @@
  * binary64.  Alongside each output the oracle returns sum_j |w_j * x_j|, the
  * scale against which a lower-precision result is judged.
  *
+ * The gradient with respect to the per-sample weights (oracle_weight_grad) is
+ * the derivative of the same definition; see there.
+ *
  * Parity is pinned (in the CPU tests) by: brute-force dense one-hot products
  * A_t W_t and A_t^T G_t in numpy; torch's embedding_bag on the CPU; numpy's
  * unique / stable argsort for the integer outputs; hand-worked fixtures; and
@@ -171,6 +174,66 @@ int oracle_forward(int32_t T, int64_t B, const int64_t *rows, const int32_t *dim
                 o[d] += term;
                 a[d] += term < 0 ? -term : term;
             }
+        }
+    }
+    free(dim_off);
+    return ORC_OK;
+}
+
+/*
+ * Gradient with respect to the per-sample weights (a weighted sparse feature
+ * pairs every id with an fp32 score: Background, "Feature Types and Memory
+ * Layout").  The pooled output is linear in each w_j, with derivative
+ * W_t[idx_j, :] placed in the columns of the lookup's bag (t, b); by the chain
+ * rule, for the gradient G of the output,
+ *
+ *     grad_w[j] = sum_{d < D_t} G[b, dim_off[t] + d] * W_t[idx_j, d],
+ *
+ * summed in column order in binary64 (every product exact).  absout[j] is
+ * sum_d |G * W|.  Same inputs and errors as oracle_forward; grad_out is fp32
+ * [B x total_dim].
+ */
+int oracle_weight_grad(int32_t T, int64_t B, const int64_t *rows, const int32_t *dims, int32_t dtype,
+                       const void *const *tables, const int64_t *indices, const int64_t *offsets,
+                       int64_t N, const float *grad_out, double *gw, double *absgw)
+{
+    int64_t total_dim = 0, *dim_off;
+    int64_t k;
+    int t, rc;
+    if (T <= 0 || B < 0 || N < 0) return ORC_ERR_ARG;
+    rc = check_offsets((int64_t)T * B, offsets, N);
+    if (rc) return rc;
+    dim_off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
+    if (!dim_off) return ORC_ERR_ARG;
+    for (t = 0; t < T; t++) {
+        dim_off[t] = total_dim;
+        total_dim += dims[t];
+    }
+    dim_off[T] = total_dim;
+    for (t = 0; t < T; t++) {
+        int64_t j;
+        for (j = offsets[(int64_t)t * B]; j < offsets[(int64_t)(t + 1) * B]; j++)
+            if (indices[j] < 0 || indices[j] >= rows[t]) {
+                free(dim_off);
+                return ORC_ERR_INDEX;
+            }
+    }
+
+#pragma omp parallel for schedule(dynamic, 64)
+    for (k = 0; k < (int64_t)T * B; k++) {
+        int64_t tt = k / B, b = k % B, j;
+        int64_t D = dims[tt];
+        const float *g = grad_out + b * total_dim + dim_off[tt];
+        for (j = offsets[k]; j < offsets[k + 1]; j++) {
+            double acc = 0.0, aabs = 0.0;
+            int64_t d;
+            for (d = 0; d < D; d++) {
+                double term = (double)g[d] * table_elem(tables[tt], dtype, indices[j] * D + d);
+                acc += term;
+                aabs += term < 0 ? -term : term;
+            }
+            gw[j] = acc;
+            absgw[j] = aabs;
         }
     }
     free(dim_off);
