@@ -155,6 +155,50 @@ def cpu_baseline(spec, d, target_s: float):
                       f"({n} lookups, {dt:.1f} s, binary64, OpenMP over bags)"}
 
 
+def weight_grad_bytes(spec, offsets_host: np.ndarray) -> int:
+    """Algorithmic bytes of one per-sample-weight-gradient launch: each lookup
+    reads its row (D_t * elem_size) and int64 index and writes one fp32; each
+    bag reads its offset and its fp32 grad_out slice (4 * D_t) once."""
+    B = spec.B
+    per_table = offsets_host[np.arange(1, spec.T + 1) * B] - offsets_host[np.arange(spec.T) * B]
+    dims = spec.dims.astype(np.int64)
+    n = int(offsets_host[-1])
+    return int((per_table * dims).sum()) * spec.elem_size + 12 * n + 8 * (spec.T * B + 1) + 4 * B * int(dims.sum())
+
+
+def bench_weight_grad(args, spec, dev):
+    spec = __import__("dataclasses").replace(spec, grad=True)
+    log(f"[bench] weight_grad on {spec.name}: {spec.table_bytes / 1e9:.2f} GB of tables")
+    d = workloads.gen_all(spec, dev)
+    torch.cuda.synchronize()
+    plan = tbe.Plan(spec.rows, spec.dims, spec.torch_dtype, spec.B, bounds_check=True, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    gw = torch.empty(d["N"], dtype=torch.float32, device=dev)
+    for _ in range(args.warmup):
+        tbe.weight_grad(plan, d["tables"], d["grad_out"], d["indices"], d["offsets"], out=gw, status=status)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for e0, e1 in evs:
+        e0.record()
+        tbe.weight_grad(plan, d["tables"], d["grad_out"], d["indices"], d["offsets"], out=gw, status=status)
+        e1.record()
+    torch.cuda.synchronize()
+    if int(status.item()) != 0:
+        raise RuntimeError(f"device status {int(status.item())}")
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs]))
+    nbytes = weight_grad_bytes(spec, d["offsets"].cpu().numpy())
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "per-sample-weight gradient: lookups/s and effective HBM GB/s", "op": "weight_grad",
+        "value": d["N"] / (ms * 1e-3), "unit": "lookups/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "dtype": "f32",
+        "data": "synthetic (seeded counter-based draws; no production data)",
+        "config": {"workload": f"{DESCRIPTIONS[args.config]}; grad_out N(0,1) fp32", "lookups": d["N"]},
+        "roofline": {"bound": "hbm", "kernel": "weight_grad_kernel", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -164,6 +208,9 @@ def main():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--op", default="step", choices=["step", "weight_grad"],
+                    help="step: forward (+ backward for cfg5), the default; weight_grad: the per-sample-weight "
+                         "gradient alone (use --config 4)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only copy a device buffer of this size 3 times (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -184,6 +231,8 @@ def main():
         print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
         return
     spec = workloads.make_config(args.config, args.seed)
+    if args.op == "weight_grad":
+        return bench_weight_grad(args, spec, dev)
     log(f"[bench] generating {spec.name}: {spec.table_bytes / 1e9:.2f} GB of tables")
     t0 = time.time()
     d = workloads.gen_all(spec, dev)

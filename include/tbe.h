@@ -134,6 +134,26 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *ind
                     const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
                     float *out, int32_t *status, void *stream);
 
+/*
+ * Gradient with respect to the per-sample weights of a weighted sparse
+ * feature (each id paired with an fp32 score).  The pooled output is linear in
+ * each weight, so for lookup j of bag (t, b)
+ *     grad_weights[j] = sum_{d < D_t} grad_out[b, dim_off[t] + d] * W_t[idx_j, d].
+ *   tables, indices, offsets, num_indices   as in tbe_forward
+ *   grad_out            device fp32 [B x total_dim] row-major, 16-byte aligned
+ *   grad_weights        device fp32 [num_indices]; every entry of every bag is
+ *                       written (0 for a lookup whose index fails the bounds
+ *                       check, which also sets TBE_STATUS_INDEX_OOB)
+ *   status              as in tbe_forward; with TBE_STATUS_OFFSETS set the
+ *                       output is unspecified
+ * One wavefront per bag; each entry has one writer and a fixed summation
+ * order (per lane in column order, then a fixed tree across lanes), so results
+ * are bitwise reproducible.
+ */
+int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out,
+                        const int64_t *indices, const int64_t *offsets, int64_t num_indices,
+                        float *grad_weights, int32_t *status, void *stream);
+
 /* Bytes of device workspace tbe_backward needs for num_indices lookups. */
 int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, size_t *bytes);
 

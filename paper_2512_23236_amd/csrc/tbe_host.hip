@@ -169,6 +169,26 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *ind
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
 }
 
+int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out, const int64_t *indices,
+                        const int64_t *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
+                        void *stream) {
+    const tbe::Plan *p = plan_of(plan);
+    if (!p) return TBE_ERR_NULL;
+    if (num_indices < 0) return TBE_ERR_SHAPE;
+    const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
+    if (!offsets && nbags > 0) return TBE_ERR_NULL;
+    if (nbags == 0 || num_indices == 0) return TBE_OK;  // nothing to write
+    if (!tables || !grad_out || !indices || !grad_weights) return TBE_ERR_NULL;
+    if (p->bounds_check && !status) return TBE_ERR_NULL;
+    if (!aligned16(tables) || !aligned16(grad_out)) return TBE_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(indices) & 7u) || (reinterpret_cast<uintptr_t>(offsets) & 7u) ||
+        (reinterpret_cast<uintptr_t>(grad_weights) & 3u))
+        return TBE_ERR_ALIGN;
+    const hipError_t e = tbe::launch_weight_grad(*p, tables, grad_out, indices, offsets, num_indices, grad_weights,
+                                                 status, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
 int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, size_t *bytes) {
     const tbe::Plan *p = plan_of(plan);
     if (!p || !bytes) return TBE_ERR_NULL;

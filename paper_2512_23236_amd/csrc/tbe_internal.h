@@ -49,6 +49,11 @@ hipError_t launch_forward(const Plan &p, const void *tables, const int64_t *indi
                           const int64_t *offsets, int64_t num_indices, const float *weights,
                           float *out, int32_t *status, hipStream_t stream);
 
+// Gradient with respect to the per-sample weights.
+hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const int64_t *indices,
+                              const int64_t *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
+                              hipStream_t stream);
+
 // Backward: workspace size and the full sort + segmented-reduce pipeline.
 size_t backward_workspace_bytes(const Plan &p, int64_t num_indices);
 hipError_t launch_backward(const Plan &p, const float *grad_out, const int64_t *indices,

@@ -1,0 +1,154 @@
+// Gradient of the pooled lookup with respect to the per-sample weights, for
+// gfx950 (CDNA4, wave64).
+//
+// The pooled output is linear in each weight w_j, with derivative
+// W_t[idx_j, :] in the columns of the lookup's bag (t, b), so for the output
+// gradient G
+//     grad_w[j] = sum_{d < D_t} G[b, dim_off[t] + d] * W_t[idx_j, d].
+//
+// One wave per bag.  A table row is read as in the forward: nvec 16-byte
+// vectors, one per lane of a lane group of LPR lanes, 64 / LPR groups per
+// wave.  The wave keeps the bag's slice of G (the same for all its lookups)
+// in registers, loads up to 64 of the bag's indices with one coalesced load,
+// then issues the row loads of kAhead lookups per lane group before using
+// any, so rows stream with several loads in flight.  Each lane multiplies its
+// vector by the matching G columns in fp32 (fixed order), a fixed xor tree
+// sums across the lane group, and the group's first lane writes grad_w[j]:
+// one writer, fixed order, bitwise reproducible.  Like the forward the work
+// is bound by the row gathers (HBM, L2 and the Infinity Cache).
+
+#include "tbe_internal.h"
+
+namespace tbe {
+namespace {
+
+constexpr int kWgWaves = 4;
+constexpr int kAhead = 8;  // row loads in flight per lane group
+
+// Widen element i (of kPerVec) of a 16-byte vector of table elements.
+template <int DT>
+struct Wide;
+
+template <>
+struct Wide<TBE_F32> {
+    static constexpr int kPerVec = 4;
+    __device__ static inline float at(const uint4 v, int i) {
+        const uint32_t q = i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+        return __uint_as_float(q);
+    }
+};
+
+template <>
+struct Wide<TBE_F16> {
+    static constexpr int kPerVec = 8;
+    __device__ static inline float at(const uint4 v, int i) {
+        const uint32_t q = (i >> 1) == 0 ? v.x : (i >> 1) == 1 ? v.y : (i >> 1) == 2 ? v.z : v.w;
+        const uint16_t h = static_cast<uint16_t>((i & 1) ? q >> 16 : q & 0xffffu);
+        return static_cast<float>(__builtin_bit_cast(_Float16, h));
+    }
+};
+
+// bfloat16 is the upper half of an fp32 word: widening is a shift.
+template <>
+struct Wide<TBE_BF16> {
+    static constexpr int kPerVec = 8;
+    __device__ static inline float at(const uint4 v, int i) {
+        const uint32_t q = (i >> 1) == 0 ? v.x : (i >> 1) == 1 ? v.y : (i >> 1) == 2 ? v.z : v.w;
+        return __uint_as_float((i & 1) ? (q & 0xffff0000u) : (q << 16));
+    }
+};
+
+template <int DT>
+__global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
+    const TableMeta *__restrict__ meta, const char *__restrict__ tables, const int64_t *__restrict__ indices,
+    const int64_t *__restrict__ offsets, const float *__restrict__ grad_out, float *__restrict__ grad_w,
+    int32_t *status, int64_t B, int64_t nbags, int64_t N, int64_t total_dim, int check,
+    const char *__restrict__ zero_page) {
+    constexpr int KV = Wide<DT>::kPerVec;
+    constexpr int ES = DT == TBE_F32 ? 4 : 2;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t k = static_cast<int64_t>(blockIdx.x) * kWgWaves + wave;
+    if (k >= nbags) return;
+    const int64_t t = k / B, b = k - t * B;
+    const TableMeta m = meta[t];
+    int64_t s = offsets[k], e = offsets[k + 1];
+    if (check) {
+        // malformed offsets: flag, and keep every access inside [0, N)
+        const int64_t cs = s < 0 ? 0 : (s > N ? N : s);
+        const int64_t ce = e < cs ? cs : (e > N ? N : e);
+        if ((cs != s || ce != e) && lane == 0) atomicOr(status, TBE_STATUS_OFFSETS);
+        s = cs;
+        e = ce;
+    }
+    if (e <= s) return;
+    const int lpr_log2 = m.lpr_log2;
+    const int LPR = 1 << lpr_log2, G = 64 >> lpr_log2;
+    const int g = lane >> lpr_log2, v = lane & (LPR - 1);
+    const int64_t row_bytes = static_cast<int64_t>(m.nvec) * 16;
+    const char *tab = tables + m.elem_offset * ES;
+    const float *grow = grad_out + b * total_dim + m.dim_off;
+    bool oob = false;
+    for (int c0 = 0; c0 < m.nvec; c0 += LPR) {  // chunks of 64 vectors (one chunk unless D is large)
+        const bool vact = c0 + v < m.nvec;
+        float gc[KV];
+#pragma unroll
+        for (int i = 0; i < KV; ++i) gc[i] = vact ? grow[(c0 + v) * KV + i] : 0.f;
+        for (int64_t base = s; base < e; base += 64) {
+            const int cnt = e - base < 64 ? static_cast<int>(e - base) : 64;
+            const int64_t my_idx = lane < cnt ? indices[base + lane] : 0;
+            for (int r0 = 0; r0 < cnt; r0 += G * kAhead) {
+                uint4 rowv[kAhead];
+                bool keep[kAhead];
+#pragma unroll
+                for (int u = 0; u < kAhead; ++u) {
+                    const int i = r0 + u * G + g;
+                    const int64_t idx = __shfl(my_idx, i & 63);
+                    const bool in = i < cnt;
+                    const bool ok = in && (!check || (idx >= 0 && idx < m.rows));
+                    oob |= in && !ok;
+                    keep[u] = in;
+                    const char *addr = (ok && vact) ? tab + idx * row_bytes + static_cast<int64_t>(c0 + v) * 16
+                                                    : zero_page + v * 16;
+                    rowv[u] = *reinterpret_cast<const uint4 *>(addr);
+                }
+#pragma unroll
+                for (int u = 0; u < kAhead; ++u) {
+                    float dot = 0.f;
+#pragma unroll
+                    for (int i = 0; i < KV; ++i) dot = __builtin_fmaf(gc[i], Wide<DT>::at(rowv[u], i), dot);
+                    for (int off = LPR >> 1; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
+                    if (keep[u] && v == 0) {
+                        float *dst = grad_w + base + r0 + u * G + g;
+                        *dst = c0 == 0 ? dot : *dst + dot;
+                    }
+                }
+            }
+        }
+    }
+    if (check && __ballot(oob) && lane == 0) atomicOr(status, TBE_STATUS_INDEX_OOB);
+}
+
+}  // namespace
+
+hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const int64_t *indices,
+                              const int64_t *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
+                              hipStream_t stream) {
+    const int64_t nbags = static_cast<int64_t>(p.T) * p.B;
+    if (nbags == 0) return hipSuccess;
+    const dim3 grid(static_cast<unsigned>((nbags + kWgWaves - 1) / kWgWaves)), block(64 * kWgWaves);
+    const char *tb = static_cast<const char *>(tables);
+    const char *zp = static_cast<const char *>(p.zero_page);
+#define TBE_LAUNCH(DT)                                                                                        \
+    hipLaunchKernelGGL((weight_grad_kernel<DT>), grid, block, 0, stream, p.meta_dev, tb, indices, offsets,     \
+                       grad_out, grad_weights, status, p.B, nbags, num_indices, p.total_dim, p.bounds_check, zp)
+    switch (p.dtype) {
+        case TBE_F32: TBE_LAUNCH(TBE_F32); break;
+        case TBE_F16: TBE_LAUNCH(TBE_F16); break;
+        default: TBE_LAUNCH(TBE_BF16); break;
+    }
+#undef TBE_LAUNCH
+    return hipGetLastError();
+}
+
+}  // namespace tbe

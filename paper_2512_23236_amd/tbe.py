@@ -66,6 +66,8 @@ def _load():
         lib.tbe_plan_info.argtypes = [P, P, P, P]
         lib.tbe_forward.restype = i32
         lib.tbe_forward.argtypes = [P, P, P, P, i64, P, P, P, P]
+        lib.tbe_weight_grad.restype = i32
+        lib.tbe_weight_grad.argtypes = [P, P, P, P, P, i64, P, P, P]
         lib.tbe_backward_workspace_bytes.restype = i32
         lib.tbe_backward_workspace_bytes.argtypes = [P, i64, P]
         lib.tbe_backward.restype = i32
@@ -173,6 +175,30 @@ def forward(plan: Plan, tables: torch.Tensor, indices: torch.Tensor, offsets: to
     rc = _load().tbe_forward(plan.handle, _ptr(tables), _ptr(indices), _ptr(offsets), indices.numel(),
                              _ptr(per_sample_weights), _ptr(out), _ptr(status), _stream(plan.device))
     _check(rc, "tbe_forward")
+    return out
+
+
+def weight_grad(plan: Plan, tables: torch.Tensor, grad_out: torch.Tensor, indices: torch.Tensor,
+                offsets: torch.Tensor, out: Optional[torch.Tensor] = None,
+                status: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Gradient with respect to the per-sample weights: fp32 [N] (queued on the current stream)."""
+    N = indices.numel()
+    _dev_tensor(tables, plan.dtype, "tables", plan)
+    _dev_tensor(grad_out, torch.float32, "grad_out", plan)
+    _dev_tensor(indices, torch.int64, "indices", plan)
+    _dev_tensor(offsets, torch.int64, "offsets", plan)
+    if grad_out.numel() != plan.B * plan.total_dim:
+        raise ValueError("grad_out must be [B, total_dim]")
+    if offsets.numel() != plan.T * plan.B + 1:
+        raise ValueError("offsets must have T*B+1 entries")
+    if out is None:
+        out = torch.empty(N, dtype=torch.float32, device=plan.device)
+    _dev_tensor(out, torch.float32, "out", plan)
+    if out.numel() != N:
+        raise ValueError("out must have num_indices entries")
+    rc = _load().tbe_weight_grad(plan.handle, _ptr(tables), _ptr(grad_out), _ptr(indices), _ptr(offsets), N,
+                                 _ptr(out), _ptr(status), _stream(plan.device))
+    _check(rc, "tbe_weight_grad")
     return out
 
 
