@@ -36,6 +36,8 @@ def _load():
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         lib.oracle_forward.restype = ctypes.c_int
         lib.oracle_forward.argtypes = [i32, i64, P, P, i32, P, P, P, i64, P, P, P]
+        lib.oracle_map_ids.restype = ctypes.c_int
+        lib.oracle_map_ids.argtypes = [P, i64, P, i64, P]
         lib.oracle_weight_grad.restype = ctypes.c_int
         lib.oracle_weight_grad.argtypes = [i32, i64, P, P, i32, P, P, P, i64, P, P, P]
         lib.oracle_backward_segments.restype = ctypes.c_int
@@ -114,6 +116,18 @@ def weight_grad(rows: Sequence[int], dims: Sequence[int], dtype: str, tables: Se
     if rc != 0:
         raise OracleError(f"oracle_weight_grad returned {rc}")
     return gw, ab
+
+
+def map_ids(values, mapping) -> np.ndarray:
+    """MapId preprocessing: 1-based position of each value in the sorted
+    mapping, 0 for an unknown value (int64 [n])."""
+    lib = _load()
+    v, mp = _c(values, np.int64), _c(mapping, np.int64)
+    out = np.empty(v.size, np.int64)
+    rc = lib.oracle_map_ids(_p(v), v.size, _p(mp), mp.size, _p(out))
+    if rc != 0:
+        raise OracleError(f"oracle_map_ids returned {rc}")
+    return out
 
 
 def backward_segments(rows, dims, indices, offsets, B: int):

@@ -417,3 +417,38 @@ int oracle_backward_rows(int32_t T, int64_t B, const int64_t *rows, const int32_
     free(out_off);
     return ORC_OK;
 }
+
+/* ---------------------------------------------------------------------- */
+/* MapId preprocessing                                                      */
+
+/*
+ * Remap raw categorical ids to dense 1-based ids for the embedding lookup,
+ * 0 for an id that is not known (Evaluation, "MapId Transform": the
+ * algorithm's three steps and its worked example).  For a mapping M of m
+ * known ids in non-decreasing order and each value v:
+ *   1. p = the insertion point of v in M: the number of entries of M that
+ *      are less than v (counted one by one here);
+ *   2. p = min(p, m - 1);
+ *   3. out = p + 1 if M[p] == v, else 0.
+ * An empty mapping maps every value to 0.
+ */
+int oracle_map_ids(const int64_t *values, int64_t n, const int64_t *mapping, int64_t m, int64_t *out)
+{
+    int64_t i;
+    if (n < 0 || m < 0) return ORC_ERR_ARG;
+#pragma omp parallel for schedule(static)
+    for (i = 0; i < n; i++) {
+        const int64_t v = values[i];
+        int64_t p = 0, r;
+        if (m == 0) {
+            out[i] = 0;
+            continue;
+        }
+        for (r = 0; r < m; r++)
+            if (mapping[r] < v) p++;
+        if (p > m - 1) p = m - 1;
+        out[i] = mapping[p] == v ? p + 1 : 0;
+    }
+    return ORC_OK;
+}
+
