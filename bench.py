@@ -199,6 +199,43 @@ def bench_weight_grad(args, spec, dev):
     }), flush=True)
 
 
+def bench_map_ids(args, dev, n_unique=10000, batch=50000):
+    d = workloads.gen_map_ids(n_unique, batch, device=dev)
+    out = torch.empty_like(d["values"])
+    for _ in range(args.warmup):
+        tbe.map_ids(d["values"], d["mapping"], out=out)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for e0, e1 in evs:
+        e0.record()
+        tbe.map_ids(d["values"], d["mapping"], out=out)
+        e1.record()
+    torch.cuda.synchronize()
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs]))
+    # algorithmic bytes: each value read and its id written (int64), the mapping read once
+    nbytes = 16 * batch + 8 * int(d["mapping"].numel())
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    res = {
+        "metric": "MapId preprocessing: values/s", "op": "map_ids", "value": batch / (ms * 1e-3),
+        "unit": "values/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "dtype": "int64", "data": "synthetic (seeded counter-based draws)",
+        "config": {"workload": f"MapId: {n_unique} known ids x {batch} values, 80% known"},
+        "roofline": {"bound": "hbm", "kernel": "map_ids_kernel", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes},
+        "context": "launch-bound at this size: the evaluation's shapes move under 1 MB",
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        v, m = d["values"].cpu().numpy(), d["mapping"].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.map_ids(v, m)
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": batch / dt, "unit": "values/s",
+                               "cores": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1)),
+                               "kind": "oracle", "sample": f"the whole workload ({batch} values, {dt:.2f} s)"}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -208,9 +245,10 @@ def main():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", default="step", choices=["step", "weight_grad"],
+    ap.add_argument("--op", default="step", choices=["step", "weight_grad", "map_ids"],
                     help="step: forward (+ backward for cfg5), the default; weight_grad: the per-sample-weight "
-                         "gradient alone (use --config 4)")
+                         "gradient alone (use --config 4); map_ids: the MapId preprocessing step at the "
+                         "evaluation's largest shape (10000 ids x 50000 values)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only copy a device buffer of this size 3 times (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -230,6 +268,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
         return
+    if args.op == "map_ids":
+        return bench_map_ids(args, dev)
     spec = workloads.make_config(args.config, args.seed)
     if args.op == "weight_grad":
         return bench_weight_grad(args, spec, dev)

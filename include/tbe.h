@@ -154,6 +154,23 @@ int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *g
                         const int64_t *indices, const int64_t *offsets, int64_t num_indices,
                         float *grad_weights, int32_t *status, void *stream);
 
+/*
+ * MapId preprocessing (the paper's Evaluation section, "MapId Transform"):
+ * remaps raw categorical ids to dense ids for the embedding lookup.  For a
+ * mapping of known raw ids in non-decreasing order, value v maps to p + 1,
+ * where p is the number of mapping entries less than v clamped to
+ * mapping_size - 1, if mapping[p] == v, and to 0 otherwise: the 1-based
+ * position of v's first occurrence, 0 for an unknown id.
+ *   values        device int64 [num_values]
+ *   mapping       device int64 [mapping_size], non-decreasing (not checked:
+ *                 an unsorted mapping gives unspecified ids); may be NULL
+ *                 when mapping_size == 0, which maps every value to 0
+ *   out           device int64 [num_values]
+ * Needs no plan; all work goes on `stream`.
+ */
+int32_t tbe_map_ids(const int64_t *values, int64_t num_values, const int64_t *mapping,
+                    int64_t mapping_size, int64_t *out, void *stream);
+
 /* Bytes of device workspace tbe_backward needs for num_indices lookups. */
 int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, size_t *bytes);
 

@@ -169,6 +169,19 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *ind
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
 }
 
+int32_t tbe_map_ids(const int64_t *values, int64_t num_values, const int64_t *mapping, int64_t mapping_size,
+                    int64_t *out, void *stream) {
+    if (num_values < 0 || mapping_size < 0) return TBE_ERR_SHAPE;
+    if (num_values == 0) return TBE_OK;
+    if (!values || !out || (mapping_size > 0 && !mapping)) return TBE_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(values) & 7u) || (reinterpret_cast<uintptr_t>(mapping) & 7u) ||
+        (reinterpret_cast<uintptr_t>(out) & 7u))
+        return TBE_ERR_ALIGN;
+    const hipError_t e = tbe::launch_map_ids(values, num_values, mapping, mapping_size, out,
+                                             static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
 int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out, const int64_t *indices,
                         const int64_t *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                         void *stream) {

@@ -49,6 +49,10 @@ hipError_t launch_forward(const Plan &p, const void *tables, const int64_t *indi
                           const int64_t *offsets, int64_t num_indices, const float *weights,
                           float *out, int32_t *status, hipStream_t stream);
 
+// MapId preprocessing: raw ids to dense 1-based ids against a sorted mapping.
+hipError_t launch_map_ids(const int64_t *values, int64_t n, const int64_t *mapping, int64_t m, int64_t *out,
+                          hipStream_t stream);
+
 // Gradient with respect to the per-sample weights.
 hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const int64_t *indices,
                               const int64_t *offsets, int64_t num_indices, float *grad_weights, int32_t *status,

@@ -66,6 +66,8 @@ def _load():
         lib.tbe_plan_info.argtypes = [P, P, P, P]
         lib.tbe_forward.restype = i32
         lib.tbe_forward.argtypes = [P, P, P, P, i64, P, P, P, P]
+        lib.tbe_map_ids.restype = i32
+        lib.tbe_map_ids.argtypes = [P, i64, P, i64, P, P]
         lib.tbe_weight_grad.restype = i32
         lib.tbe_weight_grad.argtypes = [P, P, P, P, P, i64, P, P, P]
         lib.tbe_backward_workspace_bytes.restype = i32
@@ -175,6 +177,24 @@ def forward(plan: Plan, tables: torch.Tensor, indices: torch.Tensor, offsets: to
     rc = _load().tbe_forward(plan.handle, _ptr(tables), _ptr(indices), _ptr(offsets), indices.numel(),
                              _ptr(per_sample_weights), _ptr(out), _ptr(status), _stream(plan.device))
     _check(rc, "tbe_forward")
+    return out
+
+
+def map_ids(values: torch.Tensor, mapping: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """MapId preprocessing: 1-based position of each raw id in the sorted
+    mapping, 0 when unknown (int64, queued on the current stream)."""
+    for t, name in ((values, "values"), (mapping, "mapping")):
+        if t.dtype != torch.int64 or not t.is_contiguous() or t.device.type != "cuda":
+            raise TypeError(f"{name} must be a contiguous int64 device tensor")
+    if mapping.device != values.device:
+        raise ValueError("values and mapping must be on the same device")
+    if out is None:
+        out = torch.empty_like(values)
+    if out.dtype != torch.int64 or out.numel() != values.numel() or out.device != values.device:
+        raise ValueError("out must be int64 with one entry per value")
+    rc = _load().tbe_map_ids(_ptr(values), values.numel(), _ptr(mapping), mapping.numel(), _ptr(out),
+                             _stream(values.device))
+    _check(rc, "tbe_map_ids")
     return out
 
 

@@ -2,8 +2,8 @@
 
 This package is shared by the CPU oracle's tests and by the GPU path's tests
 and benchmark.  It only draws inputs (table values, bag lengths, indices,
-per-sample weights, output gradients); it holds none of the lookup, pooling
-or gradient arithmetic.
+per-sample weights, output gradients, raw ids for the MapId step); it holds
+none of the lookup, pooling, gradient or id-mapping arithmetic.
 """
 from .gen import (  # noqa: F401
     Spec,
@@ -21,4 +21,5 @@ from .gen import (  # noqa: F401
     gen_grad_out_rows,
     gen_indices_at,
     gen_all,
+    gen_map_ids,
 )

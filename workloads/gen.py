@@ -59,6 +59,7 @@ MIX1 = 0xBF58476D1CE4E5B9
 MIX2 = 0x94D049BB133111EB
 
 ROLE_TABLE, ROLE_LEN, ROLE_EMPTY, ROLE_IDX, ROLE_W, ROLE_GRAD, ROLE_PERM = 1, 2, 3, 4, 5, 6, 7
+ROLE_MAPID = 8
 
 DTYPES = {"f32": (torch.float32, 4), "f16": (torch.float16, 2), "bf16": (torch.bfloat16, 2)}
 
@@ -456,3 +457,28 @@ def gen_all(spec: Spec, device="cpu") -> dict:
     if spec.grad:
         d["grad_out"] = gen_grad_out(spec, device)
     return d
+
+
+# --------------------------------------------------------------------------
+# MapId preprocessing inputs
+
+
+def gen_map_ids(n_unique: int, batch: int, seed: int = 7, hit_p: float = 0.8, device="cpu") -> dict:
+    """Inputs of the MapId preprocessing step, shaped as its evaluation
+    (UniqueIDs x Batch): `mapping` holds n_unique distinct raw 62-bit ids in
+    ascending order (SplitMix64 draws; a repeat is dropped, so the count can
+    in principle fall short); each of the `batch` values is, with probability
+    hit_p, a mapping entry chosen uniformly, else a fresh 62-bit id (unknown
+    with overwhelming probability)."""
+    n = torch.arange(n_unique, dtype=torch.int64, device=device)
+    raw = splitmix64(stream_key(seed, ROLE_MAPID, 0), n) & ((1 << 62) - 1)
+    mapping = torch.unique(raw)  # ascending
+    i = torch.arange(batch, dtype=torch.int64, device=device)
+    pick = splitmix64(stream_key(seed, ROLE_MAPID, 1), i)
+    fresh = splitmix64(stream_key(seed, ROLE_MAPID, 2), i) & ((1 << 62) - 1)
+    if mapping.numel() == 0:
+        return {"values": fresh, "mapping": mapping}
+    hit = _bits(pick, 11, 24).to(torch.float64) * (2.0 ** -24) < hit_p
+    pos = (_bits(pick, 32, 32) * mapping.numel()) >> 32
+    return {"values": torch.where(hit, mapping[pos], fresh), "mapping": mapping}
+
