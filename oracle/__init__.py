@@ -36,6 +36,11 @@ def _load():
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         lib.oracle_forward.restype = ctypes.c_int
         lib.oracle_forward.argtypes = [i32, i64, P, P, i32, P, P, P, i64, P, P, P]
+        lib.oracle_encode.restype = ctypes.c_int
+        lib.oracle_encode.argtypes = [ctypes.c_double, i32, P]
+        lib.oracle_apply_gradient.restype = ctypes.c_int
+        lib.oracle_apply_gradient.argtypes = [i32, P, P, i32, P, i32, ctypes.c_double, ctypes.c_double, P, P, P, P,
+                                              i64]
         lib.oracle_map_ids.restype = ctypes.c_int
         lib.oracle_map_ids.argtypes = [P, i64, P, i64, P]
         lib.oracle_weight_grad.restype = ctypes.c_int
@@ -116,6 +121,45 @@ def weight_grad(rows: Sequence[int], dims: Sequence[int], dtype: str, tables: Se
     if rc != 0:
         raise OracleError(f"oracle_weight_grad returned {rc}")
     return gw, ab
+
+
+SGD, ROWWISE_ADAGRAD = 0, 1
+
+
+def encode(value: float, dtype: str) -> int:
+    """The oracle's rounding of one binary64 value to the table format, as the
+    stored bit pattern (uint32 for f32, uint16 otherwise)."""
+    out = np.zeros(1, np.uint32 if dtype == "f32" else np.uint16)
+    rc = _load().oracle_encode(float(value), DTYPE_CODES[dtype], _p(out))
+    if rc != 0:
+        raise OracleError(f"oracle_encode returned {rc}")
+    return int(out[0])
+
+
+def apply_gradient(rows, dims, dtype: str, tables, kind: int, lr: float, eps: float, state, grad_idx,
+                   grad_row_offsets, grad_rows):
+    """One optimizer step (SGD or row-wise Adagrad) on the listed rows, in
+    binary64 with one rounding per stored element.  Updates `tables` (raw
+    storage arrays, as in forward()) and `state` (float64 [sum R], Adagrad
+    only) in place."""
+    lib = _load()
+    T = len(rows)
+    rows_a, dims_a = _c(rows, np.int64), _c(dims, np.int32)
+    for t in tables:
+        if not (t.flags.c_contiguous and t.flags.writeable):
+            raise ValueError("tables must be writeable contiguous arrays")
+    ptrs = (ctypes.c_void_p * T)(*[t.ctypes.data for t in tables])
+    gidx, gro = _c(grad_idx, np.int64), _c(grad_row_offsets, np.int64)
+    gr = _c(grad_rows, np.float32)
+    st = None
+    if state is not None:
+        if state.dtype != np.float64 or not state.flags.c_contiguous:
+            raise ValueError("state must be contiguous float64")
+        st = state
+    rc = lib.oracle_apply_gradient(T, _p(rows_a), _p(dims_a), DTYPE_CODES[dtype], ptrs, kind, float(lr), float(eps),
+                                   _p(st), _p(gidx), _p(gro), _p(gr), gidx.size)
+    if rc != 0:
+        raise OracleError(f"oracle_apply_gradient returned {rc}")
 
 
 def map_ids(values, mapping) -> np.ndarray:

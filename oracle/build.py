@@ -13,7 +13,7 @@ SRC = os.path.join(HERE, "tbe_oracle.c")
 def build(verbose: bool = False) -> str:
     tmp = LIB_PATH + f".tmp{os.getpid()}"
     cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
-           "-shared", "-fPIC", SRC, "-o", tmp]
+           "-shared", "-fPIC", SRC, "-o", tmp, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)

@@ -45,6 +45,7 @@
  *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -shared -fPIC (no fast-math).
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -449,6 +450,119 @@ int oracle_map_ids(const int64_t *values, int64_t n, const int64_t *mapping, int
         if (p > m - 1) p = m - 1;
         out[i] = mapping[p] == v ? p + 1 : 0;
     }
+    return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Sparse optimizer step on the looked-up rows                              */
+
+/*
+ * binary64 -> binary16 / bfloat16, rounded to nearest, ties to even, from the
+ * formats' definitions (no detour through binary32, which would round twice).
+ * A format with p fraction bits and minimum normal exponent emin holds
+ * +-(1 + q/2^p) 2^e for emin <= e <= emax, and +-(q/2^p) 2^emin below that.
+ * rint() rounds to nearest even in the default rounding mode; every scaled
+ * value below is exact in binary64.
+ */
+static uint16_t encode_small(double x, int p, int emin, int emax, int ebias)
+{
+    uint16_t sign = (uint16_t)(signbit(x) ? 0x8000u : 0u);
+    double a = fabs(x);
+    int e;
+    double q;
+    uint32_t bits;
+    const uint32_t inf_bits = (uint32_t)(emax + ebias + 1) << p;
+    if (isnan(a)) return (uint16_t)(inf_bits | (1u << (p - 1)));
+    if (a == 0.0) return sign;
+    frexp(a, &e);  /* a = f * 2^e, 0.5 <= f < 1 */
+    e -= 1;        /* a = (1 + ...) * 2^e */
+    if (e < emin) {
+        q = rint(ldexp(a, p - emin));  /* multiples of 2^(emin - p) */
+        bits = (uint32_t)q;            /* q == 2^p gives the smallest normal */
+    } else {
+        q = rint(ldexp(a, p - e));     /* in [2^p, 2^(p+1)] */
+        if (q == ldexp(1.0, p + 1)) {
+            q = ldexp(1.0, p);
+            e += 1;
+        }
+        if (e > emax) return (uint16_t)(sign | inf_bits);
+        bits = ((uint32_t)(e + ebias) << p) | ((uint32_t)q - (1u << p));
+    }
+    return (uint16_t)(sign | bits);
+}
+
+static void store_elem(void *table, int32_t dtype, int64_t i, double v)
+{
+    if (dtype == ORC_F32)
+        ((float *)table)[i] = (float)v; /* C conversion: round to nearest even */
+    else if (dtype == ORC_F16)
+        ((uint16_t *)table)[i] = encode_small(v, 10, -14, 15, 15);
+    else
+        ((uint16_t *)table)[i] = encode_small(v, 7, -126, 127, 127);
+}
+
+/* Encode one value so the tests can pin the rounding itself. */
+int oracle_encode(double v, int32_t dtype, void *out)
+{
+    if (dtype < ORC_F32 || dtype > ORC_BF16) return ORC_ERR_ARG;
+    store_elem(out, dtype, 0, v);
+    return ORC_OK;
+}
+
+/*
+ * One optimizer step on the rows of a sparse gradient (the unique rows
+ * grad_idx[u] with rows grad_rows[grad_row_offsets[u] ..], as tbe_backward
+ * lists them).  The paper names training but no optimizer; the two updates
+ * are the usual ones for embedding tables:
+ *   kind 0, SGD:                W[r] <- W[r] - lr * g
+ *   kind 1, row-wise Adagrad:   s[r] <- s[r] + mean_d g_d^2
+ *                               W[r] <- W[r] - lr * g / (sqrt(s[r]) + eps)
+ * in binary64, each new element rounded once to the table's format; the
+ * per-row state s (indexed by global row id) is kept in binary64.  Rows not
+ * listed are untouched.  Returns ORC_ERR_INDEX for a row id out of range.
+ */
+int oracle_apply_gradient(int32_t T, const int64_t *rows, const int32_t *dims, int32_t dtype,
+                          void *const *tables, int32_t kind, double lr, double eps, double *state,
+                          const int64_t *grad_idx, const int64_t *grad_row_offsets, const float *grad_rows,
+                          int64_t U)
+{
+    int64_t *row_base, total = 0, u;
+    int t;
+    if (T <= 0 || U < 0 || (kind != 0 && kind != 1) || (kind == 1 && !state)) return ORC_ERR_ARG;
+    row_base = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
+    if (!row_base) return ORC_ERR_ARG;
+    for (t = 0; t < T; t++) {
+        row_base[t] = total;
+        total += rows[t];
+    }
+    row_base[T] = total;
+    for (u = 0; u < U; u++)
+        if (grad_idx[u] < 0 || grad_idx[u] >= total) {
+            free(row_base);
+            return ORC_ERR_INDEX;
+        }
+#pragma omp parallel for schedule(dynamic, 64)
+    for (u = 0; u < U; u++) {
+        int64_t g = grad_idx[u], r, d, D;
+        int tt = table_of_row(T, row_base, g);
+        const float *gr = grad_rows + grad_row_offsets[u];
+        double step;
+        D = dims[tt];
+        r = g - row_base[tt];
+        if (kind == 1) {
+            double sq = 0.0;
+            for (d = 0; d < D; d++) sq += (double)gr[d] * (double)gr[d];
+            state[g] += sq / (double)D;
+            step = lr / (sqrt(state[g]) + eps);
+        } else {
+            step = lr;
+        }
+        for (d = 0; d < D; d++) {
+            double w = table_elem(tables[tt], dtype, r * D + d);
+            store_elem(tables[tt], dtype, r * D + d, w - step * (double)gr[d]);
+        }
+    }
+    free(row_base);
     return ORC_OK;
 }
 
