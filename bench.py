@@ -199,6 +199,55 @@ def bench_weight_grad(args, spec, dev):
     }), flush=True)
 
 
+def bench_optimizer(args, spec, dev):
+    """The optimizer step alone on the sparse gradient of one backward of the
+    training configuration (cfg5: 7 M unique rows of 64-256 columns)."""
+    spec = __import__("dataclasses").replace(spec, grad=True)
+    log(f"[bench] {args.op} on the sparse gradient of {spec.name}")
+    d = workloads.gen_all(spec, dev)
+    plan = tbe.Plan(spec.rows, spec.dims, spec.torch_dtype, spec.B, bounds_check=True, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    g = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], d["weights"], status=status)
+    torch.cuda.synchronize()
+    U = g.num_unique()
+    del d["grad_out"]
+    kind = tbe.SGD if args.op == "sgd" else tbe.ROWWISE_ADAGRAD
+    state = torch.zeros(int(spec.rows.sum()), dtype=torch.float32, device=dev) if kind else None
+    tables = d["tables"]
+    lr = 1e-3  # small: repeated steps keep the tables in range
+
+    def once():
+        tbe.apply_gradient(plan, tables, g, kind, lr, 1e-8, state=state, max_unique=U)
+
+    for _ in range(args.warmup):
+        once()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for e0, e1 in evs:
+        e0.record()
+        once()
+        e1.record()
+    torch.cuda.synchronize()
+    if int(status.item()) != 0:
+        raise RuntimeError(f"device status {int(status.item())}")
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs]))
+    floats = int(g.grad_row_offsets[U].item())
+    # algorithmic bytes: each listed row's table elements read and written, its
+    # fp32 gradient row read, its id and offset read (+ the state word read and written)
+    nbytes = floats * (2 * spec.elem_size + 4) + 16 * U + (8 * U if kind else 0)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": f"sparse {args.op} step: rows/s and effective HBM GB/s", "op": args.op,
+        "value": U / (ms * 1e-3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "dtype": "f32",
+        "data": "synthetic (seeded counter-based draws; no production data)",
+        "config": {"workload": f"{args.op} on the sparse gradient of one {DESCRIPTIONS[args.config]}",
+                   "unique_rows": U, "gradient_floats": floats},
+        "roofline": {"bound": "hbm", "kernel": "apply_kernel", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes},
+    }), flush=True)
+
+
 def bench_map_ids(args, dev, n_unique=10000, batch=50000):
     d = workloads.gen_map_ids(n_unique, batch, device=dev)
     out = torch.empty_like(d["values"])
@@ -245,10 +294,11 @@ def main():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", default="step", choices=["step", "weight_grad", "map_ids"],
+    ap.add_argument("--op", default="step", choices=["step", "weight_grad", "map_ids", "sgd", "adagrad"],
                     help="step: forward (+ backward for cfg5), the default; weight_grad: the per-sample-weight "
                          "gradient alone (use --config 4); map_ids: the MapId preprocessing step at the "
-                         "evaluation's largest shape (10000 ids x 50000 values)")
+                         "evaluation's largest shape (10000 ids x 50000 values); sgd / adagrad: the optimizer "
+                         "step alone, on the sparse gradient of one cfg5 backward")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only copy a device buffer of this size 3 times (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -273,6 +323,8 @@ def main():
     spec = workloads.make_config(args.config, args.seed)
     if args.op == "weight_grad":
         return bench_weight_grad(args, spec, dev)
+    if args.op in ("sgd", "adagrad"):
+        return bench_optimizer(args, spec, dev)
     log(f"[bench] generating {spec.name}: {spec.table_bytes / 1e9:.2f} GB of tables")
     t0 = time.time()
     d = workloads.gen_all(spec, dev)

@@ -171,6 +171,40 @@ int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *g
 int32_t tbe_map_ids(const int64_t *values, int64_t num_values, const int64_t *mapping,
                     int64_t mapping_size, int64_t *out, void *stream);
 
+/* Optimizer of tbe_apply_gradient. */
+enum tbe_optimizer_kind {
+    TBE_OPT_SGD = 0,             /* W[r] -= lr * g                                     */
+    TBE_OPT_ROWWISE_ADAGRAD = 1  /* s[r] += mean(g^2); W[r] -= lr * g / (sqrt(s[r]) + eps) */
+};
+
+typedef struct tbe_optimizer {
+    int32_t kind;        /* enum tbe_optimizer_kind                            */
+    float learning_rate; /* lr                                                 */
+    float eps;           /* row-wise Adagrad only                              */
+} tbe_optimizer;
+
+/*
+ * One optimizer step on the tables, applied to the rows a sparse gradient
+ * lists, in the form tbe_backward writes it (the step that follows the
+ * backward in training).
+ *   tables              device, the plan's flat buffer; listed rows updated
+ *                       in place, every other element untouched
+ *   opt                 host, read during the call
+ *   state               device fp32 [total_rows] indexed by global row id
+ *                       (row-wise Adagrad's per-row sum, updated in place);
+ *                       may be NULL for SGD
+ *   grad_idx, grad_row_offsets, grad_rows   device, as tbe_backward writes them
+ *   num_unique          device int64 scalar U, as tbe_backward writes it
+ *   max_unique          host upper bound on U (at most this many rows are
+ *                       updated), e.g. the backward's num_indices
+ * Arithmetic is fp32 (the new element is one fma, rounded to nearest even to
+ * the table's format).  One wavefront per row: every row and its state have a
+ * single writer, so the step is bitwise reproducible.
+ */
+int32_t tbe_apply_gradient(const tbe_plan *plan, void *tables, const tbe_optimizer *opt, float *state,
+                           const int64_t *grad_idx, const int64_t *grad_row_offsets, const float *grad_rows,
+                           const int64_t *num_unique, int64_t max_unique, void *stream);
+
 /* Bytes of device workspace tbe_backward needs for num_indices lookups. */
 int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, size_t *bytes);
 

@@ -169,6 +169,26 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *ind
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
 }
 
+int32_t tbe_apply_gradient(const tbe_plan *plan, void *tables, const tbe_optimizer *opt, float *state,
+                           const int64_t *grad_idx, const int64_t *grad_row_offsets, const float *grad_rows,
+                           const int64_t *num_unique, int64_t max_unique, void *stream) {
+    const tbe::Plan *p = plan_of(plan);
+    if (!p || !opt) return TBE_ERR_NULL;
+    if (opt->kind != TBE_OPT_SGD && opt->kind != TBE_OPT_ROWWISE_ADAGRAD) return TBE_ERR_SHAPE;
+    if (max_unique < 0) return TBE_ERR_SHAPE;
+    if (max_unique == 0) return TBE_OK;
+    if (!tables || !grad_idx || !grad_row_offsets || !grad_rows || !num_unique) return TBE_ERR_NULL;
+    if (opt->kind == TBE_OPT_ROWWISE_ADAGRAD && !state) return TBE_ERR_NULL;
+    if (!aligned16(tables) || (reinterpret_cast<uintptr_t>(grad_idx) & 7u) ||
+        (reinterpret_cast<uintptr_t>(grad_row_offsets) & 7u) || (reinterpret_cast<uintptr_t>(num_unique) & 7u) ||
+        (reinterpret_cast<uintptr_t>(grad_rows) & 3u) || (reinterpret_cast<uintptr_t>(state) & 3u))
+        return TBE_ERR_ALIGN;
+    const hipError_t e = tbe::launch_apply_gradient(*p, tables, opt->kind, opt->learning_rate, opt->eps, state,
+                                                    grad_idx, grad_row_offsets, grad_rows, num_unique, max_unique,
+                                                    static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
 int32_t tbe_map_ids(const int64_t *values, int64_t num_values, const int64_t *mapping, int64_t mapping_size,
                     int64_t *out, void *stream) {
     if (num_values < 0 || mapping_size < 0) return TBE_ERR_SHAPE;

@@ -49,6 +49,11 @@ hipError_t launch_forward(const Plan &p, const void *tables, const int64_t *indi
                           const int64_t *offsets, int64_t num_indices, const float *weights,
                           float *out, int32_t *status, hipStream_t stream);
 
+// One optimizer step on the rows of a sparse gradient.
+hipError_t launch_apply_gradient(const Plan &p, void *tables, int32_t kind, float lr, float eps, float *state,
+                                 const int64_t *grad_idx, const int64_t *grad_row_offsets, const float *grad_rows,
+                                 const int64_t *num_unique, int64_t max_unique, hipStream_t stream);
+
 // MapId preprocessing: raw ids to dense 1-based ids against a sorted mapping.
 hipError_t launch_map_ids(const int64_t *values, int64_t n, const int64_t *mapping, int64_t m, int64_t *out,
                           hipStream_t stream);

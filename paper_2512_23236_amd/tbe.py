@@ -48,6 +48,13 @@ class _Desc(ctypes.Structure):
     ]
 
 
+class _Opt(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("learning_rate", ctypes.c_float), ("eps", ctypes.c_float)]
+
+
+SGD, ROWWISE_ADAGRAD = 0, 1  # tbe_optimizer_kind
+
+
 def _load():
     global _lib
     if _lib is None:
@@ -66,6 +73,8 @@ def _load():
         lib.tbe_plan_info.argtypes = [P, P, P, P]
         lib.tbe_forward.restype = i32
         lib.tbe_forward.argtypes = [P, P, P, P, i64, P, P, P, P]
+        lib.tbe_apply_gradient.restype = i32
+        lib.tbe_apply_gradient.argtypes = [P, P, ctypes.POINTER(_Opt), P, P, P, P, P, i64, P]
         lib.tbe_map_ids.restype = i32
         lib.tbe_map_ids.argtypes = [P, i64, P, i64, P, P]
         lib.tbe_weight_grad.restype = i32
@@ -178,6 +187,28 @@ def forward(plan: Plan, tables: torch.Tensor, indices: torch.Tensor, offsets: to
                              _ptr(per_sample_weights), _ptr(out), _ptr(status), _stream(plan.device))
     _check(rc, "tbe_forward")
     return out
+
+
+def apply_gradient(plan: Plan, tables: torch.Tensor, grad: "SparseGrad", kind: int, lr: float, eps: float = 0.0,
+                   state: Optional[torch.Tensor] = None, max_unique: Optional[int] = None) -> None:
+    """One optimizer step (SGD or row-wise Adagrad) on the rows `grad` lists,
+    in place on `tables` (and `state`, fp32 [total_rows], for Adagrad)."""
+    _dev_tensor(tables, plan.dtype, "tables", plan)
+    for t, dt, name in ((grad.grad_idx, torch.int64, "grad_idx"), (grad.grad_row_offsets, torch.int64,
+                        "grad_row_offsets"), (grad.grad_rows, torch.float32, "grad_rows"),
+                        (grad.num_unique_dev, torch.int64, "num_unique")):
+        _dev_tensor(t, dt, name, plan)
+    if state is not None:
+        _dev_tensor(state, torch.float32, "state", plan)
+        if state.numel() != int(plan.rows.sum()):
+            raise ValueError("state must have one entry per table row (total_rows)")
+    if max_unique is None:
+        max_unique = grad.grad_idx.numel()
+    opt = _Opt(int(kind), float(lr), float(eps))
+    rc = _load().tbe_apply_gradient(plan.handle, _ptr(tables), ctypes.byref(opt), _ptr(state), _ptr(grad.grad_idx),
+                                    _ptr(grad.grad_row_offsets), _ptr(grad.grad_rows), _ptr(grad.num_unique_dev),
+                                    int(max_unique), _stream(plan.device))
+    _check(rc, "tbe_apply_gradient")
 
 
 def map_ids(values: torch.Tensor, mapping: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
