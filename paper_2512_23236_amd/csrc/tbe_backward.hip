@@ -285,28 +285,37 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__
                                                               const Range *__restrict__ ranges, int T,
                                                               const Ctl *__restrict__ ctl, int shift, int nbits,
                                                               uint32_t *__restrict__ hist) {
-    __shared__ uint32_t cnt[kBuckets];
+    // counts only (order does not matter here): one LDS histogram per wave,
+    // plain atomic increments, summed at the end
+    __shared__ uint32_t cnt[kWaves][kBuckets];
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    cnt[tid] = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) cnt[w][tid] = 0;
     __syncthreads();
     const uint32_t mask = (1u << nbits) - 1u;
     const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
-#pragma unroll 4
+    uint32_t k[kItems];
+#pragma unroll
     for (int r = 0; r < kItems; ++r) {
         const int64_t pos = wbase + r * 64 + lane;
-        const bool valid = pos < ti.p_hi;
-        const uint32_t d = valid ? digit_of(keys[pos], shift, mask) : 0u;
-        const uint64_t peers = match_digit(d, valid, nbits);
-        if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&cnt[d], static_cast<uint32_t>(__popcll(peers)));
+        k[r] = pos < ti.p_hi ? keys[pos] : 0u;
+    }
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+        const int64_t pos = wbase + r * 64 + lane;
+        if (pos < ti.p_hi) atomicAdd(&cnt[wave][digit_of(k[r], shift, mask)], 1u);
     }
     __syncthreads();
+    uint32_t c = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) c += cnt[w][tid];
     // layout: table-major, digit-major, tile-minor
     const int64_t base = ranges[ti.t].tile_base * kBuckets;
-    hist[base + static_cast<int64_t>(tid) * ti.ntiles + ti.local] = cnt[tid];
+    hist[base + static_cast<int64_t>(tid) * ti.ntiles + ti.local] = c;
 }
 
 // Exclusive scan over `count` u32 values in place: chunk sums, a one-block
@@ -457,11 +466,42 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
 
 // --------------------------------------------------------------- segments
 
-// Flags of sorted position pos (inside table range [start, end)).
-__device__ inline void seg_flags(const uint32_t *__restrict__ keys, int64_t pos, int64_t start, uint32_t key,
-                                 bool &kept, bool &is_start) {
-    kept = key != kSentinel;
-    is_start = kept && (pos == start || keys[pos - 1] != key);
+// A tile is read in rounds: wave w takes positions p_lo + w * kTile / kWaves
+// + r * 64 + lane for r < kItems (coalesced).  A position is kept unless it
+// holds the drop key, and starts a segment when it is kept and is the table's
+// first position or its key differs from the previous position's.  The
+// previous key comes from the next lower lane (lane 0 reads it).
+struct RoundFlags {
+    uint64_t start, kept;  // ballots over the round's 64 positions
+};
+
+// All kItems rounds' keys of this lane (and, for lane 0, each round's
+// previous key) are loaded before any is used, so the loads overlap.
+struct TileKeys {
+    uint32_t key[kItems];
+    uint32_t prev0[kItems];  // lane 0: key before the round's first position
+};
+
+__device__ inline void load_tile_keys(const uint32_t *__restrict__ keys, const TileInfo &ti, int64_t wbase,
+                                      TileKeys &k) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+        const int64_t pos = wbase + r * 64 + lane;
+        k.key[r] = pos < ti.p_hi ? keys[pos] : kSentinel;
+        k.prev0[r] = (lane == 0 && pos > ti.start && pos < ti.p_hi) ? keys[pos - 1] : kSentinel;
+    }
+}
+
+__device__ inline RoundFlags round_flags(const TileKeys &k, const TileInfo &ti, int64_t wbase, int r) {
+    const int lane = threadIdx.x & 63;
+    const int64_t pos = wbase + r * 64 + lane;
+    const uint32_t key = k.key[r];
+    uint32_t prev = __shfl_up(key, 1);
+    if (lane == 0) prev = k.prev0[r];
+    const bool kept = pos < ti.p_hi && key != kSentinel;
+    const bool st = kept && (pos == ti.start || prev != key);
+    return RoundFlags{__ballot(st), __ballot(kept)};
 }
 
 __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t *__restrict__ keys,
@@ -469,23 +509,36 @@ __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t *__r
                                                              const Range *__restrict__ ranges, int T,
                                                              const Ctl *__restrict__ ctl,
                                                              TileSeg *__restrict__ tseg) {
-    __shared__ uint32_t lds[kWaves];
+    __shared__ uint32_t wsum[2][kWaves];
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
+    TileKeys tk;
+    load_tile_keys(keys, ti, wbase, tk);
     uint32_t ns = 0, nk = 0;
-    for (int64_t pos = ti.p_lo + threadIdx.x; pos < ti.p_hi; pos += kThreads) {
-        bool kept, st;
-        seg_flags(keys, pos, ti.start, keys[pos], kept, st);
-        ns += st;
-        nk += kept;
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+        const RoundFlags f = round_flags(tk, ti, wbase, r);
+        ns += static_cast<uint32_t>(__popcll(f.start));
+        nk += static_cast<uint32_t>(__popcll(f.kept));
     }
-    uint32_t ts, tk;
-    block_excl_scan<uint32_t>(ns, lds, &ts);
-    block_excl_scan<uint32_t>(nk, lds, &tk);
-    if (threadIdx.x == 0)
+    if (lane == 0) {
+        wsum[0][wave] = ns;
+        wsum[1][wave] = nk;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t ts = 0, tk = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            ts += wsum[0][w];
+            tk += wsum[1][w];
+        }
         tseg[tile] = TileSeg{ts, tk, static_cast<uint64_t>(ts) * static_cast<uint64_t>(meta[ti.t].dim), 0};
+    }
 }
 
 __global__ __launch_bounds__(kThreads) void seg_scan_kernel(TileSeg *__restrict__ tseg, Ctl *ctl,
@@ -529,44 +582,53 @@ __global__ __launch_bounds__(kThreads) void seg_write_kernel(const uint32_t *__r
                                                              int64_t *__restrict__ grad_idx,
                                                              int64_t *__restrict__ seg_offsets,
                                                              int64_t *__restrict__ grad_row_offsets) {
-    __shared__ uint32_t lds[kWaves];
+    __shared__ uint32_t wsum[2][kWaves];
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
     const TileSeg pre = tseg[tile];
     const TableMeta m = meta[ti.t];
-    // blocked: thread i owns positions p_lo + i*kItems .. +kItems
-    const int64_t my = ti.p_lo + static_cast<int64_t>(threadIdx.x) * kItems;
-    uint32_t k[kItems];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint64_t lt = lanemask_lt();
+    const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
+    TileKeys tk;
+    load_tile_keys(keys, ti, wbase, tk);
+    uint64_t st[kItems], kp[kItems];
     uint32_t ns = 0, nk = 0;
-    uint32_t fl = 0;  // bit 2q: kept, bit 2q+1: start
 #pragma unroll
-    for (int q = 0; q < kItems; ++q) {
-        const int64_t pos = my + q;
-        bool kept = false, st = false;
-        if (pos < ti.p_hi) {
-            k[q] = keys[pos];
-            seg_flags(keys, pos, ti.start, k[q], kept, st);
-        }
-        fl |= (kept ? 1u : 0u) << (2 * q);
-        fl |= (st ? 1u : 0u) << (2 * q + 1);
-        ns += st;
-        nk += kept;
+    for (int r = 0; r < kItems; ++r) {
+        const RoundFlags f = round_flags(tk, ti, wbase, r);
+        st[r] = f.start;
+        kp[r] = f.kept;
+        ns += static_cast<uint32_t>(__popcll(f.start));
+        nk += static_cast<uint32_t>(__popcll(f.kept));
     }
-    uint32_t ts, tk;
-    uint32_t rs = block_excl_scan<uint32_t>(ns, lds, &ts);
-    uint32_t rk = block_excl_scan<uint32_t>(nk, lds, &tk);
+    if (lane == 0) {
+        wsum[0][wave] = ns;
+        wsum[1][wave] = nk;
+    }
+    __syncthreads();
+    uint32_t rs = 0, rk = 0;  // starts and kept positions of the tile before this wave
 #pragma unroll
-    for (int q = 0; q < kItems; ++q) {
-        if ((fl >> (2 * q + 1)) & 1u) {
-            const int64_t u = static_cast<int64_t>(pre.starts) + rs;
-            grad_idx[u] = m.row_base + static_cast<int64_t>(k[q]);
-            seg_offsets[u] = static_cast<int64_t>(pre.kept) + rk;
-            grad_row_offsets[u] = static_cast<int64_t>(pre.dimsum) + static_cast<int64_t>(rs) * m.dim;
-            ++rs;
+    for (int w = 0; w < kWaves; ++w) {
+        if (w < wave) {
+            rs += wsum[0][w];
+            rk += wsum[1][w];
         }
-        rk += (fl >> (2 * q)) & 1u;
+    }
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+        if ((st[r] >> lane) & 1ull) {
+            const uint32_t s_here = rs + static_cast<uint32_t>(__popcll(st[r] & lt));
+            const uint32_t k_here = rk + static_cast<uint32_t>(__popcll(kp[r] & lt));
+            const int64_t u = static_cast<int64_t>(pre.starts) + s_here;
+            grad_idx[u] = m.row_base + static_cast<int64_t>(tk.key[r]);
+            seg_offsets[u] = static_cast<int64_t>(pre.kept) + k_here;
+            grad_row_offsets[u] = static_cast<int64_t>(pre.dimsum) + static_cast<int64_t>(s_here) * m.dim;
+        }
+        rs += static_cast<uint32_t>(__popcll(st[r]));
+        rk += static_cast<uint32_t>(__popcll(kp[r]));
     }
 }
 
@@ -845,27 +907,24 @@ __global__ __launch_bounds__(kThreads) void edges_kernel(const uint32_t *__restr
     if (!tile_info(ranges, T, tile, ti)) return;
     const TileSeg pre = tseg[tile];
     const int tid = threadIdx.x;
-    // segment starts per block of kBlk positions (8 threads x 16 positions)
-    if (tid < kBlksPerTile) blk_cnt[tid] = 0;
-    __syncthreads();
+    // segment starts per block of kBlk positions: wave w, round r covers
+    // positions of block w * kBlksPerWave + r / 2 (two rounds per block)
     {
-        // all 17 keys go out before any is used (clamped, unconditional loads)
-        const int64_t my = ti.p_lo + static_cast<int64_t>(tid) * kItems;
-        uint32_t k[kItems + 1];
+        const int lane = tid & 63, wave = tid >> 6;
+        const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
+        TileKeys tk;
+        load_tile_keys(keys, ti, wbase, tk);
+        uint32_t c = 0;
 #pragma unroll
-        for (int q = 0; q <= kItems; ++q) {
-            int64_t pos = my + q - 1;
-            pos = pos < ti.start ? ti.start : (pos >= ti.p_hi ? ti.p_hi - 1 : pos);
-            k[q] = keys[pos];
+        for (int r = 0; r < kItems; ++r) {
+            const RoundFlags f = round_flags(tk, ti, wbase, r);
+            c += static_cast<uint32_t>(__popcll(f.start));
+            if ((r & 1) && lane == 0) {
+                blk_cnt[wave * kBlksPerWave + (r >> 1)] = c;
+                c = 0;
+            }
         }
-        uint32_t ns = 0;
-#pragma unroll
-        for (int q = 0; q < kItems; ++q) {
-            const int64_t pos = my + q;
-            const bool st = pos < ti.p_hi && k[q + 1] != kSentinel && (pos == ti.start || k[q] != k[q + 1]);
-            ns += st;
-        }
-        if (ns) atomicAdd(&blk_cnt[tid / (kBlk / kItems)], ns);
+        static_assert(kItems == 2 * kBlksPerWave, "two rounds of 64 positions per block");
     }
     __syncthreads();
     if (tid < 64) {
