@@ -16,8 +16,9 @@ import numpy as np
 
 from .build import LIB_PATH, build
 
-F32, F16, BF16 = 0, 1, 2
-DTYPE_CODES = {"f32": F32, "f16": F16, "bf16": BF16}
+F32, F16, BF16, U8_ROWWISE = 0, 1, 2, 3
+DTYPE_CODES = {"f32": F32, "f16": F16, "bf16": BF16, "u8": U8_ROWWISE}
+POOLING_CODES = {"sum": 0, "mean": 1}
 
 _lib = None
 
@@ -35,7 +36,7 @@ def _load():
         P = ctypes.c_void_p
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         lib.oracle_forward.restype = ctypes.c_int
-        lib.oracle_forward.argtypes = [i32, i64, P, P, i32, P, P, P, i64, P, P, P]
+        lib.oracle_forward.argtypes = [i32, i64, P, P, i32, P, P, P, i64, P, i32, P, P]
         lib.oracle_encode.restype = ctypes.c_int
         lib.oracle_encode.argtypes = [ctypes.c_double, i32, P]
         lib.oracle_apply_gradient.restype = ctypes.c_int
@@ -48,9 +49,11 @@ def _load():
         lib.oracle_backward_segments.restype = ctypes.c_int
         lib.oracle_backward_segments.argtypes = [i32, i64, P, P, P, P, i64, P, P, P, P, P, P]
         lib.oracle_backward_rows.restype = ctypes.c_int
-        lib.oracle_backward_rows.argtypes = [i32, i64, P, P, P, P, P, P, P, P, i64, P, P, P]
+        lib.oracle_backward_rows.argtypes = [i32, i64, P, P, P, P, P, P, P, P, i64, P, i32, P, P]
         lib.oracle_decode.restype = ctypes.c_double
         lib.oracle_decode.argtypes = [P, i32, i64]
+        lib.oracle_decode_row.restype = ctypes.c_double
+        lib.oracle_decode_row.argtypes = [P, i32, i64, i64, i64]
         _lib = lib
     return _lib
 
@@ -75,14 +78,24 @@ def decode(words: np.ndarray, dtype: str) -> np.ndarray:
     return np.array([lib.oracle_decode(_p(w), DTYPE_CODES[dtype], i) for i in range(w.size)])
 
 
+def decode_row(table: np.ndarray, dtype: str, D: int, r: int, d: int) -> float:
+    """Element (r, d) of a table with rows of D values, decoded by the oracle
+    (for "u8", rows of D codes then an fp32 scale and bias)."""
+    t = np.ascontiguousarray(table)
+    return _load().oracle_decode_row(_p(t), DTYPE_CODES[dtype], D, r, d)
+
+
 def forward(rows: Sequence[int], dims: Sequence[int], dtype: str, tables: Sequence[np.ndarray],
-            indices, offsets, B: int, weights=None):
+            indices, offsets, B: int, weights=None, pooling: str = "sum"):
     """Pooled lookup in binary64.
 
     tables[t] is table t as a [R_t, D_t] array of raw element storage: float32
     for "f32", and 16-bit words (uint16 / float16 / any 2-byte dtype, read as
-    the raw bit pattern) for "f16" and "bf16".  Returns (out, absout), each
-    [B, total_dim] float64.
+    the raw bit pattern) for "f16" and "bf16"; for "u8" an [R_t, D_t + 8]
+    uint8 array (each row's D_t codes, then its fp32 scale and bias).
+    Indices and offsets of any integer type are taken as int64 values.
+    pooling is "sum" or "mean" (mean takes no weights).  Returns (out,
+    absout), each [B, total_dim] float64.
     """
     lib = _load()
     T = len(rows)
@@ -95,7 +108,7 @@ def forward(rows: Sequence[int], dims: Sequence[int], dtype: str, tables: Sequen
     out = np.zeros((B, total_dim), np.float64)
     absout = np.zeros((B, total_dim), np.float64)
     rc = lib.oracle_forward(T, B, _p(rows_a), _p(dims_a), DTYPE_CODES[dtype], ptrs, _p(idx), _p(off),
-                            idx.size, _p(w), _p(out), _p(absout))
+                            idx.size, _p(w), POOLING_CODES[pooling], _p(out), _p(absout))
     if rc != 0:
         raise OracleError(f"oracle_forward returned {rc}")
     return out, absout
@@ -200,8 +213,10 @@ def backward_segments(rows, dims, indices, offsets, B: int):
             "seg_offsets": seg[: u + 1], "grad_row_offsets": gro[: u + 1], "U": u}
 
 
-def backward_rows(rows, dims, offsets, B: int, grad_out, seg: dict, weights=None, sel=None):
-    """Gradient rows (binary64) of the selected unique ids (default: all).
+def backward_rows(rows, dims, offsets, B: int, grad_out, seg: dict, weights=None, sel=None,
+                  pooling: str = "sum"):
+    """Gradient rows (binary64) of the selected unique ids (default: all),
+    for sum or mean pooling (mean takes no weights).
 
     Returns (rows_packed, abs_packed, row_offsets) where row s of the
     selection occupies rows_packed[row_offsets[s]:row_offsets[s+1]].
@@ -226,7 +241,7 @@ def backward_rows(rows, dims, offsets, B: int, grad_out, seg: dict, weights=None
     absout = np.zeros(max(total, 1), np.float64)
     rc = lib.oracle_backward_rows(T, B, _p(rows_a), _p(dims_a), _p(off), _p(w), _p(g),
                                   _p(_c(seg["perm"], np.int64)), _p(gidx), _p(_c(seg["seg_offsets"], np.int64)),
-                                  n_sel, _p(sel_a), _p(out), _p(absout))
+                                  n_sel, _p(sel_a), POOLING_CODES[pooling], _p(out), _p(absout))
     if rc != 0:
         raise OracleError(f"oracle_backward_rows returned {rc}")
     return out[:total], absout[:total], ro

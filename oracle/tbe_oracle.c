@@ -36,6 +36,17 @@
  * The gradient with respect to the per-sample weights (oracle_weight_grad) is
  * the derivative of the same definition; see there.
  *
+ * Variants.  Mean pooling divides each bag's sum by its number of lookups
+ * (an empty bag gives 0), and its gradient passes grad_out / L to every
+ * lookup of the bag.  Tables may also be stored in an 8-bit row-wise
+ * quantised format (a row of D codes followed by its fp32 scale and bias; see
+ * row_elem), the kind of quantised operation the paper names for early-stage
+ * ranking (Introduction, "Model Diversity Across Ranking Stages").  Narrower
+ * int32 indices and offsets (the int64 -> int32 downcast of hashed ids that
+ * the paper lists among sparse preprocessing steps, Background,
+ * "Preprocessing Transformation Categories") hold the same values, so the
+ * oracle takes them widened to int64.
+ *
  * Parity is pinned (in the CPU tests) by: brute-force dense one-hot products
  * A_t W_t and A_t^T G_t in numpy; torch's embedding_bag on the CPU; numpy's
  * unique / stable argsort for the integer outputs; hand-worked fixtures; and
@@ -53,6 +64,10 @@
 #define ORC_F32 0
 #define ORC_F16 1
 #define ORC_BF16 2
+#define ORC_U8_ROWWISE 3
+
+#define ORC_POOL_SUM 0
+#define ORC_POOL_MEAN 1
 
 #define ORC_OK 0
 #define ORC_ERR_ARG (-1)
@@ -101,6 +116,25 @@ static double table_elem(const void *table, int32_t dtype, int64_t i)
     return bf16_to_double(((const uint16_t *)table)[i]);
 }
 
+/*
+ * Element d of row r of a table whose rows hold D values.  For the 8-bit
+ * row-wise format (ORC_U8_ROWWISE) a row is stored as D unsigned 8-bit codes
+ * followed by an fp32 scale and an fp32 bias (D + 8 bytes, little-endian), and
+ * element d is scale * code[d] + bias.  The product of an fp32 scale and an
+ * 8-bit code is exact in binary64; adding the bias rounds once in binary64.
+ */
+static double row_elem(const void *table, int32_t dtype, int64_t D, int64_t r, int64_t d)
+{
+    if (dtype == ORC_U8_ROWWISE) {
+        const uint8_t *row = (const uint8_t *)table + r * (D + 8);
+        float scale, bias;
+        memcpy(&scale, row + D, sizeof scale);
+        memcpy(&bias, row + D + 4, sizeof bias);
+        return (double)scale * (double)row[d] + (double)bias;
+    }
+    return table_elem(table, dtype, r * D + d);
+}
+
 static int check_offsets(int64_t nbags, const int64_t *offsets, int64_t n)
 {
     int64_t k;
@@ -113,7 +147,14 @@ static int check_offsets(int64_t nbags, const int64_t *offsets, int64_t n)
 /* Decode one element so the tests can pin the format conversion itself. */
 double oracle_decode(const void *table, int32_t dtype, int64_t i)
 {
+    if (dtype < ORC_F32 || dtype > ORC_BF16) return 0.0 / 0.0;
     return table_elem(table, dtype, i);
+}
+
+/* Element (r, d) of a table with rows of D values, any format. */
+double oracle_decode_row(const void *table, int32_t dtype, int64_t D, int64_t r, int64_t d)
+{
+    return row_elem(table, dtype, D, r, d);
 }
 
 /*
@@ -125,18 +166,25 @@ double oracle_decode(const void *table, int32_t dtype, int64_t i)
  *   indices[N]      lookup indices, local to their table
  *   offsets[T*B+1]  CSR bag boundaries, bag k = t*B + b
  *   weights[N]      per-sample weights, or NULL for plain sum pooling
- *   out, absout     [B x total_dim] binary64: the pooled sums and sum |w x|
+ *   pooling         ORC_POOL_SUM, or ORC_POOL_MEAN: the bag's sum divided by
+ *                   its number of lookups L = offsets[k+1] - offsets[k] (an
+ *                   empty bag gives 0); mean pooling takes no weights
+ *   out, absout     [B x total_dim] binary64: the pooled values and the sum of
+ *                   the absolute values of the pooled terms (w x, or x / L)
  * Returns ORC_OK, or an error (nothing guaranteed written) for an index out of
  * range or offsets that are not a monotone CSR array ending at N.
  */
 int oracle_forward(int32_t T, int64_t B, const int64_t *rows, const int32_t *dims, int32_t dtype,
                    const void *const *tables, const int64_t *indices, const int64_t *offsets,
-                   int64_t N, const float *weights, double *out, double *absout)
+                   int64_t N, const float *weights, int32_t pooling, double *out, double *absout)
 {
     int64_t total_dim = 0, *dim_off;
     int64_t k;
     int t, rc;
     if (T <= 0 || B < 0 || N < 0) return ORC_ERR_ARG;
+    if (pooling != ORC_POOL_SUM && pooling != ORC_POOL_MEAN) return ORC_ERR_ARG;
+    if (pooling == ORC_POOL_MEAN && weights) return ORC_ERR_ARG;
+    if (dtype < ORC_F32 || dtype > ORC_U8_ROWWISE) return ORC_ERR_ARG;
     rc = check_offsets((int64_t)T * B, offsets, N);
     if (rc) return rc;
     dim_off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
@@ -171,9 +219,16 @@ int oracle_forward(int32_t T, int64_t B, const int64_t *rows, const int32_t *dim
         for (j = offsets[k]; j < offsets[k + 1]; j++) {
             double w = weights ? (double)weights[j] : 1.0;
             for (d = 0; d < D; d++) {
-                double term = w * table_elem(tables[tt], dtype, indices[j] * D + d);
+                double term = w * row_elem(tables[tt], dtype, D, indices[j], d);
                 o[d] += term;
                 a[d] += term < 0 ? -term : term;
+            }
+        }
+        if (pooling == ORC_POOL_MEAN && offsets[k + 1] > offsets[k]) {
+            double L = (double)(offsets[k + 1] - offsets[k]);
+            for (d = 0; d < D; d++) {
+                o[d] /= L;
+                a[d] /= L;
             }
         }
     }
@@ -202,6 +257,7 @@ int oracle_weight_grad(int32_t T, int64_t B, const int64_t *rows, const int32_t 
     int64_t k;
     int t, rc;
     if (T <= 0 || B < 0 || N < 0) return ORC_ERR_ARG;
+    if (dtype < ORC_F32 || dtype > ORC_U8_ROWWISE) return ORC_ERR_ARG;
     rc = check_offsets((int64_t)T * B, offsets, N);
     if (rc) return rc;
     dim_off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
@@ -229,7 +285,7 @@ int oracle_weight_grad(int32_t T, int64_t B, const int64_t *rows, const int32_t 
             double acc = 0.0, aabs = 0.0;
             int64_t d;
             for (d = 0; d < D; d++) {
-                double term = (double)g[d] * table_elem(tables[tt], dtype, indices[j] * D + d);
+                double term = (double)g[d] * row_elem(tables[tt], dtype, D, indices[j], d);
                 acc += term;
                 aabs += term < 0 ? -term : term;
             }
@@ -352,8 +408,11 @@ int oracle_backward_segments(int32_t T, int64_t B, const int64_t *rows, const in
  * Gradient rows of selected unique rows (all of them when sel == NULL):
  *   g_u[d] = sum over i in [seg_offsets[u], seg_offsets[u+1]) of
  *            w_{perm[i]} * grad_out[b(perm[i]), dim_off[t_u] + d],
- * summed in sorted (= lookup position) order, in binary64.
- *   grad_out  [B x total_dim] fp32;  weights [N] or NULL
+ * summed in sorted (= lookup position) order, in binary64.  With mean
+ * pooling each lookup of a bag of L lookups passes grad_out / L instead (the
+ * derivative of the bag's mean with respect to each of its rows).
+ *   grad_out  [B x total_dim] fp32;  weights [N] or NULL (NULL for mean)
+ *   pooling   ORC_POOL_SUM or ORC_POOL_MEAN
  *   perm, grad_idx, seg_offsets  from oracle_backward_segments
  *   n_sel, sel    unique ids u to compute (or sel == NULL: u = 0..n_sel-1)
  *   out, absout   the selected rows packed one after another (row s starts
@@ -362,12 +421,14 @@ int oracle_backward_segments(int32_t T, int64_t B, const int64_t *rows, const in
 int oracle_backward_rows(int32_t T, int64_t B, const int64_t *rows, const int32_t *dims,
                          const int64_t *offsets, const float *weights, const float *grad_out,
                          const int64_t *perm, const int64_t *grad_idx, const int64_t *seg_offsets,
-                         int64_t n_sel, const int64_t *sel, double *out, double *absout)
+                         int64_t n_sel, const int64_t *sel, int32_t pooling, double *out, double *absout)
 {
     int64_t *row_base, *dim_off, *out_off;
     int64_t s, total_dim;
     int t;
     if (T <= 0 || B < 0 || n_sel < 0) return ORC_ERR_ARG;
+    if (pooling != ORC_POOL_SUM && pooling != ORC_POOL_MEAN) return ORC_ERR_ARG;
+    if (pooling == ORC_POOL_MEAN && weights) return ORC_ERR_ARG;
     row_base = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
     dim_off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
     out_off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n_sel + 1));
@@ -405,9 +466,10 @@ int oracle_backward_rows(int32_t T, int64_t B, const int64_t *rows, const int32_
             int64_t k = bag_of_lookup((int64_t)T * B, offsets, j);
             int64_t b = k % B;
             double w = weights ? (double)weights[j] : 1.0;
+            double L = (double)(offsets[k + 1] - offsets[k]);
             const float *g = grad_out + b * total_dim + dim_off[tu];
             for (d = 0; d < D; d++) {
-                double term = w * (double)g[d];
+                double term = pooling == ORC_POOL_MEAN ? (double)g[d] / L : w * (double)g[d];
                 o[d] += term;
                 a[d] += term < 0 ? -term : term;
             }
@@ -529,6 +591,7 @@ int oracle_apply_gradient(int32_t T, const int64_t *rows, const int32_t *dims, i
     int64_t *row_base, total = 0, u;
     int t;
     if (T <= 0 || U < 0 || (kind != 0 && kind != 1) || (kind == 1 && !state)) return ORC_ERR_ARG;
+    if (dtype < ORC_F32 || dtype > ORC_BF16) return ORC_ERR_ARG;
     row_base = (int64_t *)malloc(sizeof(int64_t) * (size_t)(T + 1));
     if (!row_base) return ORC_ERR_ARG;
     for (t = 0; t < T; t++) {

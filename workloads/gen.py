@@ -26,6 +26,10 @@ synthetic stand-ins for production DLRM sparse features:
         per-sample weights U(0,1) fp32; ids Zipf(1.2) over a permutation
   cfg5  cfg3's inputs plus an output gradient N(0,1) fp32 [B x total_dim]
 
+Any configuration can be redrawn with dtype "u8" (8-bit row-wise tables):
+each row is D uniform 8-bit codes plus a per-row fp32 scale U(2e-4, 6e-4)
+and bias U(-0.06, -0.04), about what quantising U(-0.05, 0.05) rows gives.
+
 Distribution recipes (the recipe is the definition):
   * uniform fp value in [lo, hi): u = 24 random bits as fp32 (exact),
     x = fl32(fl32(u * fl32((hi-lo)/2^24)) + fl32(lo)), then rounded to
@@ -60,8 +64,15 @@ MIX2 = 0x94D049BB133111EB
 
 ROLE_TABLE, ROLE_LEN, ROLE_EMPTY, ROLE_IDX, ROLE_W, ROLE_GRAD, ROLE_PERM = 1, 2, 3, 4, 5, 6, 7
 ROLE_MAPID = 8
+ROLE_QPARAM = 9
 
-DTYPES = {"f32": (torch.float32, 4), "f16": (torch.float16, 2), "bf16": (torch.bfloat16, 2)}
+# name -> (torch storage dtype, bytes per stored element); "u8" is the 8-bit
+# row-wise format: a row of D codes followed by its fp32 scale and bias.
+DTYPES = {"f32": (torch.float32, 4), "f16": (torch.float16, 2), "bf16": (torch.bfloat16, 2),
+          "u8": (torch.uint8, 1)}
+U8_ROW_EXTRA = 8  # bytes of scale and bias after a u8 row's codes
+U8_SCALE = (2e-4, 6e-4)    # per-row scale range: about (0.1 / 255) x [0.5, 1.5]
+U8_BIAS = (-0.06, -0.04)   # per-row bias range: about the minimum of U(-0.05, 0.05)
 
 _CHUNK = 1 << 25
 
@@ -144,6 +155,12 @@ class Spec:
         return DTYPES[self.dtype][1]
 
     @property
+    def row_elems(self) -> np.ndarray:
+        """Stored elements per row of each table (D_t, or D_t + 8 bytes for "u8")."""
+        extra = U8_ROW_EXTRA if self.dtype == "u8" else 0
+        return self.dims.astype(np.int64) + extra
+
+    @property
     def dim_off(self) -> np.ndarray:
         return np.concatenate([[0], np.cumsum(self.dims.astype(np.int64))])
 
@@ -158,12 +175,12 @@ class Spec:
     @property
     def table_offsets(self) -> np.ndarray:
         """Element offset of each table in a flat buffer, tables packed in order."""
-        sizes = self.rows.astype(np.int64) * self.dims.astype(np.int64)
+        sizes = self.rows.astype(np.int64) * self.row_elems
         return np.concatenate([[0], np.cumsum(sizes)])[:-1]
 
     @property
     def table_elems(self) -> int:
-        return int((self.rows.astype(np.int64) * self.dims.astype(np.int64)).sum())
+        return int((self.rows.astype(np.int64) * self.row_elems).sum())
 
     @property
     def table_bytes(self) -> int:
@@ -382,9 +399,34 @@ def _normal12(key: int, n: torch.Tensor) -> torch.Tensor:
     return (s - 6 * 65536).to(torch.float32) * (2.0 ** -16)
 
 
+def _u8_rows(spec: Spec, t: int, r: torch.Tensor) -> torch.Tensor:
+    """Rows r of 8-bit row-wise table t as stored bytes [len(r), D_t + 8]: D_t
+    uniform 8-bit codes, then an fp32 scale drawn from U8_SCALE and an fp32
+    bias drawn from U8_BIAS (little-endian), both per row."""
+    D = int(spec.dims[t])
+    r = r.view(-1, 1)
+    n = r * D + torch.arange(D, dtype=torch.int64, device=r.device).view(1, -1)
+    codes = _bits(splitmix64(stream_key(spec.seed, ROLE_TABLE, t), n.reshape(-1)), 56, 8).to(torch.uint8)
+    key = stream_key(spec.seed, ROLE_QPARAM, t)
+    rr = r.reshape(-1)
+    scale = _value_draw(("uniform",) + U8_SCALE, key, 2 * rr)
+    bias = _value_draw(("uniform",) + U8_BIAS, key, 2 * rr + 1)
+    sb = torch.stack([scale, bias], 1).contiguous().view(torch.uint8)
+    return torch.cat([codes.view(-1, D), sb], 1)
+
+
 def gen_table(spec: Spec, t: int, device="cpu", out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Table t, [R_t, D_t] in the spec's dtype (row-major)."""
+    """Table t, [R_t, D_t] in the spec's dtype (row-major); for "u8" the
+    stored bytes [R_t, D_t + 8]."""
     R, D = int(spec.rows[t]), int(spec.dims[t])
+    if spec.dtype == "u8":
+        if out is None:
+            out = torch.empty((R, D + U8_ROW_EXTRA), dtype=torch.uint8, device=device)
+        step = max(1, _CHUNK // (D + U8_ROW_EXTRA))
+        for r0 in range(0, R, step):
+            r1 = min(R, r0 + step)
+            out[r0:r1] = _u8_rows(spec, t, torch.arange(r0, r1, dtype=torch.int64, device=out.device))
+        return out
     if out is None:
         out = torch.empty((R, D), dtype=spec.torch_dtype, device=device)
     flat = out.view(-1)
@@ -399,6 +441,8 @@ def gen_table_rows(spec: Spec, t: int, row_ids, device="cpu") -> torch.Tensor:
     """Rows row_ids of table t, [len(row_ids), D_t] (same bits as gen_table)."""
     D = int(spec.dims[t])
     r = torch.as_tensor(row_ids, dtype=torch.int64, device=device).view(-1, 1)
+    if spec.dtype == "u8":
+        return _u8_rows(spec, t, r)
     n = r * D + torch.arange(D, dtype=torch.int64, device=device).view(1, -1)
     return _values(spec, t, n.reshape(-1)).view(-1, D)
 
@@ -407,9 +451,10 @@ def gen_tables_flat(spec: Spec, device="cpu") -> torch.Tensor:
     """All tables packed in table order into one flat buffer (spec.table_offsets)."""
     flat = torch.empty(spec.table_elems, dtype=spec.torch_dtype, device=device)
     offs = spec.table_offsets
+    re = spec.row_elems
     for t in range(spec.T):
-        R, D = int(spec.rows[t]), int(spec.dims[t])
-        gen_table(spec, t, device, out=flat[int(offs[t]): int(offs[t]) + R * D].view(R, D))
+        R, E = int(spec.rows[t]), int(re[t])
+        gen_table(spec, t, device, out=flat[int(offs[t]): int(offs[t]) + R * E].view(R, E))
     return flat
 
 
