@@ -15,7 +15,8 @@
  * bag k = t*B + b holding lookups j in [offsets[k], offsets[k+1]):
  *
  *   forward   out[b, dim_off[t] + d] = sum_j w_j * W_t[indices[j], d]
- *             (w_j = per_sample_weights[j], or 1), accumulated in fp32;
+ *             (w_j = per_sample_weights[j], or 1), accumulated in fp32
+ *             (mean pooling: the sum times fl32(1/L), L lookups in the bag);
  *   backward  for every distinct global row id g = row_base[t] + indices[j]
  *             that occurs, in ascending order, the row
  *             grad[g][d] = sum over lookups j of g, in lookup order,
@@ -48,22 +49,44 @@
 extern "C" {
 #endif
 
-#define TBE_ABI_VERSION 1
+#define TBE_ABI_VERSION 2
 
-/* Element type of every table. */
-enum tbe_dtype { TBE_F32 = 0, TBE_F16 = 1, TBE_BF16 = 2 };
+/*
+ * Element types.  Tables may use any of them; the forward output F32, F16 or
+ * BF16.  TBE_U8_ROWWISE is an 8-bit row-wise quantised table (the paper names
+ * quantised operations among early-stage ranking's kernels: Introduction,
+ * "Model Diversity Across Ranking Stages"): a row of D_t values is stored as
+ * D_t unsigned 8-bit codes followed by an fp32 scale and an fp32 bias, D_t + 8
+ * bytes, and value d is scale * code[d] + bias (one fp32 fma).
+ */
+enum tbe_dtype { TBE_F32 = 0, TBE_F16 = 1, TBE_BF16 = 2, TBE_U8_ROWWISE = 3 };
+
+/* Pooling of a bag's rows.  Mean divides the sum by the bag's number of
+ * lookups L = offsets[k+1] - offsets[k] (an empty bag gives 0), as a multiply
+ * by fl32(1/L); its gradient passes fl32(1/L) * grad_out to every lookup of the
+ * bag.  Mean pooling takes no per-sample weights. */
+enum tbe_pooling { TBE_POOL_SUM = 0, TBE_POOL_MEAN = 1 };
+
+/* Integer type of `indices` and `offsets`.  int32 is the downcast of hashed
+ * ids that sparse preprocessing applies (Background, "Preprocessing
+ * Transformation Categories"); it halves the index bytes per lookup. */
+enum tbe_index_type { TBE_INDEX_I64 = 0, TBE_INDEX_I32 = 1 };
 
 /* Host-detected errors (return values). */
 enum tbe_error {
     TBE_OK = 0,
     TBE_ERR_NULL = -1,      /* a required pointer is NULL                        */
     TBE_ERR_SHAPE = -2,     /* a count, size or shape is out of range           */
-    TBE_ERR_DTYPE = -3,     /* unknown element type                             */
-    TBE_ERR_ALIGN = -4,     /* D_t * elem_size not a multiple of 16 bytes, or a
-                               table / output / buffer not 16-byte aligned       */
+    TBE_ERR_DTYPE = -3,     /* unknown table, output or index type              */
+    TBE_ERR_ALIGN = -4,     /* a row width or table offset breaks the layout
+                               rules of tbe_desc, or a buffer is misaligned
+                               (tables, out, grad_out, grad_rows: 16 bytes;
+                               indices / offsets: their element size)           */
     TBE_ERR_WORKSPACE = -5, /* backward workspace smaller than required          */
     TBE_ERR_HIP = -6,       /* a HIP runtime call failed                         */
-    TBE_ERR_NOMEM = -7      /* host allocation failed                            */
+    TBE_ERR_NOMEM = -7,     /* host allocation failed                            */
+    TBE_ERR_UNSUPPORTED = -8 /* an unknown pooling mode, or the plan's options
+                               do not support this call (see the entry point)   */
 };
 
 /* Device-detected errors (bits OR-ed into *status). */
@@ -76,18 +99,27 @@ enum tbe_status_bits {
 /* Description of the tables; read during tbe_plan_create only. */
 typedef struct tbe_desc {
     int32_t num_tables;           /* T >= 1                                       */
-    int32_t dtype;                /* enum tbe_dtype                               */
+    int32_t dtype;                /* enum tbe_dtype of every table                */
     int64_t batch_size;           /* B >= 0                                       */
     const int64_t *rows;          /* host [T]: R_t >= 1                           */
-    const int32_t *dims;          /* host [T]: D_t >= 1, D_t*elem_size % 16 == 0  */
+    const int32_t *dims;          /* host [T]: D_t >= 1, D_t*elem_size % 16 == 0
+                                     (TBE_U8_ROWWISE: D_t % 8 == 0)               */
     const int64_t *table_offsets; /* host [T]: element offset of table t in the
                                      flat tables buffer (row-major R_t x D_t,
-                                     16-byte aligned); NULL = tables packed in
-                                     order with no gaps                          */
-    int64_t table_elems;          /* elements in the flat tables buffer; every
-                                     table must lie inside it                    */
+                                     16-byte aligned; TBE_U8_ROWWISE: byte
+                                     offset of R_t rows of D_t + 8 bytes, 8-byte
+                                     aligned); NULL = tables packed in order
+                                     with no gaps                                */
+    int64_t table_elems;          /* elements (TBE_U8_ROWWISE: bytes) in the flat
+                                     tables buffer; every table must lie inside  */
     int32_t bounds_check;         /* 1 = check indices and offsets on the GPU,
                                      0 = trust them                              */
+    int32_t pooling;              /* enum tbe_pooling (0: sum)                    */
+    int32_t index_type;           /* enum tbe_index_type of indices and offsets
+                                     (0: int64)                                  */
+    int32_t out_dtype;            /* enum tbe_dtype of the forward output: F32,
+                                     F16 or BF16 (0: fp32); rounded to nearest
+                                     even from the fp32 result                   */
 } tbe_desc;
 
 /* Validated description plus its per-table metadata on the device
@@ -119,20 +151,24 @@ int32_t tbe_plan_info(const tbe_plan *plan, int64_t *total_dim, int64_t *total_r
 /*
  * Forward pooled lookup.
  *   tables              device, the flat buffer described by the plan
- *   indices             device int64 [num_indices], local to each bag's table
- *   offsets             device int64 [T*B + 1], CSR bag boundaries, k = t*B + b
+ *   indices             device [num_indices] of the plan's index_type, local to
+ *                       each bag's table
+ *   offsets             device [T*B + 1] of the plan's index_type, CSR bag
+ *                       boundaries, k = t*B + b
  *   num_indices         N = offsets[T*B]
- *   per_sample_weights  device fp32 [N], or NULL for plain sum pooling
- *   out                 device fp32 [B x total_dim] row-major, 16-byte aligned;
- *                       every element is written (an empty bag gives +0.0)
+ *   per_sample_weights  device fp32 [N], or NULL for unweighted pooling (must be
+ *                       NULL with mean pooling: TBE_ERR_UNSUPPORTED)
+ *   out                 device [B x total_dim] of the plan's out_dtype,
+ *                       row-major, 16-byte aligned; every element is written
+ *                       (an empty bag gives +0.0)
  *   status              device int32, OR-ed with TBE_STATUS_* bits; may be NULL
  *                       only when the plan does not check bounds
- * One wavefront pools one (bag, table); the output has exactly one writer
- * per element, so results are bitwise reproducible.
+ * A lane group pools one (bag, table) in fp32, in lookup order; the output has
+ * exactly one writer per element, so results are bitwise reproducible.
  */
-int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *indices,
-                    const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
-                    float *out, int32_t *status, void *stream);
+int32_t tbe_forward(const tbe_plan *plan, const void *tables, const void *indices, const void *offsets,
+                    int64_t num_indices, const float *per_sample_weights, void *out, int32_t *status,
+                    void *stream);
 
 /*
  * Gradient with respect to the per-sample weights of a weighted sparse
@@ -146,13 +182,14 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *ind
  *                       check, which also sets TBE_STATUS_INDEX_OOB)
  *   status              as in tbe_forward; with TBE_STATUS_OFFSETS set the
  *                       output is unspecified
+ * Needs sum pooling and fp32 / fp16 / bf16 tables (else TBE_ERR_UNSUPPORTED).
  * One wavefront per bag; each entry has one writer and a fixed summation
  * order (per lane in column order, then a fixed tree across lanes), so results
  * are bitwise reproducible.
  */
-int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out,
-                        const int64_t *indices, const int64_t *offsets, int64_t num_indices,
-                        float *grad_weights, int32_t *status, void *stream);
+int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out, const void *indices,
+                        const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
+                        void *stream);
 
 /*
  * MapId preprocessing (the paper's Evaluation section, "MapId Transform"):
@@ -199,7 +236,8 @@ typedef struct tbe_optimizer {
  *                       updated), e.g. the backward's num_indices
  * Arithmetic is fp32 (the new element is one fma, rounded to nearest even to
  * the table's format).  One wavefront per row: every row and its state have a
- * single writer, so the step is bitwise reproducible.
+ * single writer, so the step is bitwise reproducible.  8-bit row-wise tables
+ * are not updated in place (TBE_ERR_UNSUPPORTED).
  */
 int32_t tbe_apply_gradient(const tbe_plan *plan, void *tables, const tbe_optimizer *opt, float *state,
                            const int64_t *grad_idx, const int64_t *grad_row_offsets, const float *grad_rows,
@@ -211,7 +249,10 @@ int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, 
 /*
  * Sparse gradient of the tables.
  *   grad_out            device fp32 [B x total_dim], the gradient of `out`
- *   indices, offsets, num_indices, per_sample_weights   as in tbe_forward
+ *                       (fp32 whatever the plan's out_dtype)
+ *   indices, offsets, num_indices, per_sample_weights   as in tbe_forward; with
+ *                       mean pooling each lookup of a bag of L lookups carries
+ *                       the weight fl32(1/L)
  *   workspace           device, >= tbe_backward_workspace_bytes, 256-byte aligned;
  *                       scratch only, its contents are not part of the result
  *   grad_rows           device fp32, capacity grad_rows_capacity floats: the
@@ -228,11 +269,12 @@ int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, 
  *                       gradient row written) if grad_row_offsets[U] exceeds
  *                       grad_rows_capacity
  * Entries past U of grad_idx / seg_offsets / grad_row_offsets are unspecified.
+ * The tables themselves are not read, so any table type is accepted.
  * Every gradient row has a single writer and a fixed summation order, so the
  * result is bitwise reproducible.
  */
-int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t *indices,
-                     const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const void *indices,
+                     const void *offsets, int64_t num_indices, const float *per_sample_weights,
                      void *workspace, size_t workspace_bytes, float *grad_rows,
                      int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                      int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream);
@@ -257,8 +299,8 @@ enum tbe_backward_phase {
  * this tbe_backward.  A failed record returns TBE_ERR_HIP.
  * For callers that time the parts of the backward (profilers, benchmarks).
  */
-int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const int64_t *indices,
-                           const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const void *indices,
+                           const void *offsets, int64_t num_indices, const float *per_sample_weights,
                            void *workspace, size_t workspace_bytes, float *grad_rows,
                            int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                            int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream,

@@ -164,7 +164,8 @@ __device__ inline uint64_t match_digit(uint32_t d, bool valid, int nbits) {
 
 // ------------------------------------------------------------------ setup
 
-__global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restrict__ offsets,
+template <typename IT>
+__global__ __launch_bounds__(kThreads) void setup_kernel(const IT *__restrict__ offsets,
                                                          const TableMeta *__restrict__ meta, int T, int64_t B,
                                                          int64_t N, int check, Ctl *ctl, Range *ranges,
                                                          int32_t *status, int64_t *num_unique,
@@ -174,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restri
     __shared__ int bad;
     if (tid == 0) {
         bad = 0;
-        if (check && (offsets[0] != 0 || offsets[static_cast<int64_t>(T) * B] != N)) bad = 1;
+        if (check && (offsets[0] != 0 || static_cast<int64_t>(offsets[static_cast<int64_t>(T) * B]) != N)) bad = 1;
         *num_unique = 0;
         seg_offsets[0] = 0;
         grad_row_offsets[0] = 0;
@@ -185,8 +186,8 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restri
         const int t = base + tid;
         int64_t s = 0, e = 0, nt = 0, nw = 0;
         if (t < T) {
-            s = offsets[static_cast<int64_t>(t) * B];
-            e = offsets[static_cast<int64_t>(t + 1) * B];
+            s = static_cast<int64_t>(offsets[static_cast<int64_t>(t) * B]);
+            e = static_cast<int64_t>(offsets[static_cast<int64_t>(t + 1) * B]);
             if (check && (s < 0 || e < s || e > N)) {
                 bad = 1;
                 s = e = 0;
@@ -218,12 +219,14 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const int64_t *__restri
 // One workgroup per run of kKeyBags consecutive bags (table-major order).  The
 // run's offsets are staged in LDS; the threads then walk the run's lookups in
 // order, 256 at a time (coalesced loads and stores), and find each lookup's
-// bag by binary search over the staged offsets.
-template <typename V>
+// bag by binary search over the staged offsets.  With 64-bit values the
+// weight rides along: the per-sample weight, or fl32(1/L) under mean pooling
+// (L = the bag's lookup count, read from the staged offsets).
+template <typename V, typename IT>
 __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restrict__ meta,
-                                                        const int64_t *__restrict__ indices,
-                                                        const int64_t *__restrict__ offsets,
-                                                        const float *__restrict__ weights,
+                                                        const IT *__restrict__ indices,
+                                                        const IT *__restrict__ offsets,
+                                                        const float *__restrict__ weights, int mean,
                                                         const Range *__restrict__ ranges, int64_t B,
                                                         int64_t nbags, int check, Ctl *ctl,
                                                         uint32_t *__restrict__ keys, V *__restrict__ vals,
@@ -235,7 +238,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
     if (k0 >= nbags || ctl->abort) return;
     const int nk = nbags - k0 < kKeyBags ? static_cast<int>(nbags - k0) : kKeyBags;
     if (tid == 0) bad = 0;
-    for (int i = tid; i <= nk; i += kThreads) off[i] = offsets[k0 + i];
+    for (int i = tid; i <= nk; i += kThreads) off[i] = static_cast<int64_t>(offsets[k0 + i]);
     __syncthreads();
     if (check) {
         // each bag lies inside its table's range, in order
@@ -263,7 +266,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         }
         const int64_t k = k0 + lo;
         const int64_t t = k / B, b = k - t * B;
-        const int64_t idx = __builtin_nontemporal_load(indices + j);
+        const int64_t idx = static_cast<int64_t>(__builtin_nontemporal_load(indices + j));
         uint32_t key = static_cast<uint32_t>(idx);
         if (check && (idx < 0 || idx >= meta[t].rows)) {
             key = kSentinel;
@@ -271,7 +274,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         }
         keys[j] = key;
         if constexpr (sizeof(V) == 8) {
-            const float w = weights[j];
+            const float w = mean ? 1.0f / static_cast<float>(off[lo + 1] - off[lo]) : weights[j];
             vals[j] = static_cast<uint64_t>(b) | (static_cast<uint64_t>(__float_as_uint(w)) << 32);
         } else {
             vals[j] = static_cast<uint32_t>(b);
@@ -1146,8 +1149,8 @@ Layout layout(const Plan &p, int64_t N) {
     return L;
 }
 
-template <typename V>
-hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, const int64_t *offsets,
+template <typename V, typename IT>
+hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT *offsets,
                int64_t N, const float *weights, char *ws, const Layout &L, float *grad_rows, int64_t capacity,
                int64_t *grad_idx, int64_t *seg_offsets, int64_t *grad_row_offsets, int64_t *num_unique,
                int32_t *status, hipStream_t stream, void *const *phase_events) {
@@ -1178,15 +1181,16 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
     hipError_t me = mark(TBE_PHASE_KEYS);
     if (me != hipSuccess) return me;
 
-    hipLaunchKernelGGL(setup_kernel, dim3(1), dim3(kThreads), 0, stream, offsets, p.meta_dev, T, p.B, N, check, ctl,
+    hipLaunchKernelGGL(setup_kernel<IT>, dim3(1), dim3(kThreads), 0, stream, offsets, p.meta_dev, T, p.B, N, check, ctl,
                        ranges, status, num_unique, seg_offsets, grad_row_offsets);
     if (N == 0 || nbags == 0) {
         const hipError_t e = hipGetLastError();
         return e != hipSuccess ? e : mark(TBE_NUM_PHASES);
     }
-    hipLaunchKernelGGL(keys_kernel<V>, dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)), dim3(kThreads),
-                       0, stream, p.meta_dev, indices, offsets, weights, ranges, p.B, nbags, check, ctl, keys[0],
-                       vals[0], status);
+    const int mean = p.pooling == TBE_POOL_MEAN;
+    hipLaunchKernelGGL((keys_kernel<V, IT>), dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)),
+                       dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights, mean, ranges, p.B, nbags,
+                       check, ctl, keys[0], vals[0], status);
     // bits: every valid local key, and the drop key's low bits above them
     int64_t max_rows = 1;
     for (int t = 0; t < T; ++t) max_rows = p.meta_host[t].rows > max_rows ? p.meta_host[t].rows : max_rows;
@@ -1233,7 +1237,7 @@ hipError_t run(const Plan &p, const float *grad_out, const int64_t *indices, con
 
 size_t backward_workspace_bytes(const Plan &p, int64_t num_indices) { return layout(p, num_indices).total; }
 
-hipError_t launch_backward(const Plan &p, const float *grad_out, const int64_t *indices, const int64_t *offsets,
+hipError_t launch_backward(const Plan &p, const float *grad_out, const void *indices, const void *offsets,
                            int64_t num_indices, const float *weights, void *workspace, size_t workspace_bytes,
                            float *grad_rows, int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                            int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, hipStream_t stream,
@@ -1241,12 +1245,19 @@ hipError_t launch_backward(const Plan &p, const float *grad_out, const int64_t *
     (void)workspace_bytes;
     const Layout L = layout(p, num_indices);
     char *ws = static_cast<char *>(workspace);
-    if (weights)
-        return run<uint64_t>(p, grad_out, indices, offsets, num_indices, weights, ws, L, grad_rows,
-                             grad_rows_capacity, grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream,
-                             phase_events);
-    return run<uint32_t>(p, grad_out, indices, offsets, num_indices, nullptr, ws, L, grad_rows, grad_rows_capacity,
-                         grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream, phase_events);
+    // lookups carry a weight (64-bit sort values) when weighted or mean-pooled
+    const bool wide = weights != nullptr || p.pooling == TBE_POOL_MEAN;
+#define TBE_RUN(V, IT)                                                                                          \
+    return run<V, IT>(p, grad_out, static_cast<const IT *>(indices), static_cast<const IT *>(offsets), num_indices, \
+                      weights, ws, L, grad_rows, grad_rows_capacity, grad_idx, seg_offsets, grad_row_offsets,     \
+                      num_unique, status, stream, phase_events)
+    if (p.index_type == TBE_INDEX_I32) {
+        if (wide) TBE_RUN(uint64_t, int32_t);
+        TBE_RUN(uint32_t, int32_t);
+    }
+    if (wide) TBE_RUN(uint64_t, int64_t);
+    TBE_RUN(uint32_t, int64_t);
+#undef TBE_RUN
 }
 
 }  // namespace tbe

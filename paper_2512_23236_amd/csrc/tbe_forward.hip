@@ -12,6 +12,13 @@
 // writes the bag's pooled row when the bag's last lookup is consumed: every
 // output element has one writer and a fixed summation order.
 //
+// Variants: indices and offsets are int64 or int32 (a template parameter);
+// mean pooling multiplies a finished bag by fl32(1/L) as it is written; the
+// output is stored as fp32, or rounded to nearest even to fp16 / bf16; 8-bit
+// row-wise tables are read as 8-byte vectors of codes (a lane group of D/8
+// lanes per row), and every lane also loads its row's fp32 scale and bias
+// (the 8 bytes after the codes) into the same ring slot.
+//
 // The work is bound by memory latency and bandwidth (HBM and the L2 /
 // Infinity Cache that serve hot rows): about one fma per element read, far
 // below the fp32 vector ridge point.
@@ -24,15 +31,19 @@ namespace {
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = 64 * kWavesPerBlock;
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-// Adds w * (one 16-byte vector of table elements) to acc.
+// Adds w * (one load vector of table elements) to acc.  `sb` is the row's
+// (scale, bias) for 8-bit row-wise tables and unused otherwise.
 template <int DT>
 struct Elem;
 
 template <>
 struct Elem<TBE_F32> {
     static constexpr int kPerVec = 4;
-    __device__ static inline void fma(float *acc, const uint4 v, float w) {
+    using Vec = uint4;
+    __device__ static inline void fma(float *acc, const uint4 v, float w, float2) {
         acc[0] = __builtin_fmaf(w, __uint_as_float(v.x), acc[0]);
         acc[1] = __builtin_fmaf(w, __uint_as_float(v.y), acc[1]);
         acc[2] = __builtin_fmaf(w, __uint_as_float(v.z), acc[2]);
@@ -50,7 +61,8 @@ __device__ inline float half_hi(uint32_t x) {
 template <>
 struct Elem<TBE_F16> {
     static constexpr int kPerVec = 8;
-    __device__ static inline void fma(float *acc, const uint4 v, float w) {
+    using Vec = uint4;
+    __device__ static inline void fma(float *acc, const uint4 v, float w, float2) {
         const uint32_t q[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -64,7 +76,8 @@ struct Elem<TBE_F16> {
 template <>
 struct Elem<TBE_BF16> {
     static constexpr int kPerVec = 8;
-    __device__ static inline void fma(float *acc, const uint4 v, float w) {
+    using Vec = uint4;
+    __device__ static inline void fma(float *acc, const uint4 v, float w, float2) {
         const uint32_t q[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -74,6 +87,60 @@ struct Elem<TBE_BF16> {
     }
 };
 
+// 8-bit row-wise: value = scale * code + bias (one fma), then acc += w * value.
+template <>
+struct Elem<TBE_U8_ROWWISE> {
+    static constexpr int kPerVec = 8;
+    using Vec = uint2;
+    __device__ static inline void fma(float *acc, const uint2 v, float w, float2 sb) {
+        const uint32_t q[2] = {v.x, v.y};
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const float code = static_cast<float>((q[i] >> (8 * b)) & 0xffu);
+                acc[4 * i + b] = __builtin_fmaf(w, __builtin_fmaf(sb.x, code, sb.y), acc[4 * i + b]);
+            }
+        }
+    }
+};
+
+// fp32 -> bf16 bits, rounded to nearest even (a NaN stays a NaN).
+__device__ inline uint32_t bf16_bits(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t r = (u & 0x7fffffffu) > 0x7f800000u ? (u | 0x00400000u) : u + 0x7fffu + ((u >> 16) & 1u);
+    return r >> 16;
+}
+
+__device__ inline uint32_t f16_bits(float x) {
+    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(x)));  // nearest even
+}
+
+// Writes K pooled fp32 values to `o` in the output type (non-temporal stores).
+template <int K>
+__device__ inline void store_out(char *o, const float *val, int out_dt) {
+    if (out_dt == TBE_F32) {
+#pragma unroll
+        for (int q = 0; q < K / 4; ++q)
+            __builtin_nontemporal_store(f4{val[4 * q], val[4 * q + 1], val[4 * q + 2], val[4 * q + 3]},
+                                        reinterpret_cast<f4 *>(o) + q);
+        return;
+    }
+    uint32_t w[K / 2];
+#pragma unroll
+    for (int i = 0; i < K / 2; ++i)
+        w[i] = out_dt == TBE_F16 ? (f16_bits(val[2 * i]) | (f16_bits(val[2 * i + 1]) << 16))
+                                 : (bf16_bits(val[2 * i]) | (bf16_bits(val[2 * i + 1]) << 16));
+    if constexpr (K == 4) {
+        __builtin_nontemporal_store(u2{w[0], w[1]}, reinterpret_cast<u2 *>(o));
+    } else {
+#pragma unroll
+        for (int q = 0; q < K / 8; ++q)
+            __builtin_nontemporal_store(u4{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]},
+                                        reinterpret_cast<u4 *>(o) + q);
+    }
+}
+
 
 // Streams kBagsPerGroup bags per lane group: bags k0 + g*kBagsPerGroup + i of
 // one table (the unit holds nbags_unit bags, k0 first).  Inside the stream
@@ -81,14 +148,17 @@ struct Elem<TBE_BF16> {
 // load zeros from the zero page) and finished bags are parked in LDS, so the
 // loop holds no conditional vector-memory instruction and the ring's loads
 // are waited for one at a time, oldest first.
-template <int DT, int LPR, bool WEIGHTED>
+template <int DT, int LPR, bool WEIGHTED, typename IT>
 __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ table,
-                                 const int64_t *__restrict__ indices, const float *__restrict__ weights,
-                                 const int64_t *__restrict__ offsets, int64_t k0, int nbags_unit,
-                                 float *__restrict__ out, int64_t B, int64_t N, int64_t total_dim, bool check,
+                                 const IT *__restrict__ indices, const float *__restrict__ weights,
+                                 const IT *__restrict__ offsets, int64_t k0, int nbags_unit,
+                                 char *__restrict__ out, int64_t B, int64_t N, int64_t total_dim, bool check,
                                  int32_t *status, int lane, const char *__restrict__ zero_page,
-                                 float *__restrict__ stage) {
+                                 float *__restrict__ stage, int out_dt, bool mean) {
     using E = Elem<DT>;
+    using VT = typename E::Vec;
+    constexpr bool kQuant = DT == TBE_U8_ROWWISE;
+    constexpr int VB = sizeof(VT);  // bytes per load vector
     constexpr int U = LPR < 8 ? LPR : 8;  // row loads in flight per lane group
     constexpr int NB = kBagsPerGroup;
     constexpr uint32_t kSkip = 0xffffffffu;
@@ -99,7 +169,7 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
     // bag boundaries of this group, clamped monotone into [0, N] when checking
     int64_t bnd64[NB + 1];
 #pragma unroll
-    for (int i = 0; i <= NB; ++i) bnd64[i] = offsets[kg + (i < nbs ? i : nbs)];
+    for (int i = 0; i <= NB; ++i) bnd64[i] = static_cast<int64_t>(offsets[kg + (i < nbs ? i : nbs)]);
     if (check) {
         int64_t lo = 0;
         bool bad = false;
@@ -118,8 +188,9 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
     for (int i = 0; i <= NB; ++i) bnd[i] = static_cast<int32_t>(bnd64[i] - P);
     const int32_t Q = bnd[NB];
     const uint32_t b0 = static_cast<uint32_t>(kg % B);
-    float *out0 = out + static_cast<int64_t>(b0) * total_dim + m.dim_off;
-    const uint32_t row_bytes = static_cast<uint32_t>(m.nvec) * 16u;
+    const int oes = out_dt == TBE_F32 ? 4 : 2;
+    char *out0 = out + (static_cast<int64_t>(b0) * total_dim + m.dim_off) * oes;
+    const uint32_t row_bytes = static_cast<uint32_t>(m.row_bytes);
 
     // the wave walks the longest group's span
     int32_t span = Q;
@@ -132,7 +203,7 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
 
     for (int c0 = 0; c0 < m.nvec; c0 += LPR) {  // one pass unless rows exceed 1 KiB
         const bool vact = c0 + v < m.nvec;
-        const char *colp = table + static_cast<int64_t>(c0 + v) * 16;
+        const char *colp = table + static_cast<int64_t>(c0 + v) * VB;
         const char *zerop = zero_page + v * 16;
         // lane v of the group holds lookup rel + v (cur) and rel + LPR + v (nxt)
         // Index chunks of LPR lookups, lane v holding lookup rel + v: `cur`
@@ -145,7 +216,8 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
         auto load_chunk = [&](int32_t rel, int64_t &idx, float &w) {
             const int32_t rp = rel + v;
             const bool in = rp < Q;
-            idx = __builtin_nontemporal_load(in ? indices + P + rp : reinterpret_cast<const int64_t *>(zero_page));
+            idx = static_cast<int64_t>(
+                __builtin_nontemporal_load(in ? indices + P + rp : reinterpret_cast<const IT *>(zero_page)));
             w = 1.0f;
             if constexpr (WEIGHTED)
                 w = __builtin_nontemporal_load(in ? weights + P + rp : reinterpret_cast<const float *>(zero_page));
@@ -164,21 +236,28 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
         uint32_t nxt_r = check_chunk(LPR, far_idx);
         load_chunk(2 * LPR, far_idx, far_w);
 
-        uint4 ring[U];
+        VT ring[U];
         float ring_w[WEIGHTED ? U : 1];
-        auto issue = [&](int src_lane, bool from_next, uint4 &dst, float &dw) {
+        float2 ring_sb[kQuant ? U : 1];
+        auto issue = [&](int src_lane, bool from_next, VT &dst, float &dw, float2 &dsb) {
             const int src = g * LPR + src_lane;
             const uint32_t r = from_next ? __shfl(nxt_r, src) : __shfl(cur_r, src);
             const bool ok = r != kSkip && vact;
             const char *addr = ok ? colp + static_cast<uint64_t>(r) * row_bytes : zerop;
-            dst = *reinterpret_cast<const uint4 *>(addr);
+            dst = *reinterpret_cast<const VT *>(addr);
+            if constexpr (kQuant) {
+                // the row's scale and bias follow its D codes
+                const char *sba = ok ? table + static_cast<uint64_t>(r) * row_bytes + m.dim : zerop;
+                dsb = *reinterpret_cast<const float2 *>(sba);
+            }
             if constexpr (WEIGHTED) {
                 const float w = from_next ? __shfl(nxt_w, src) : __shfl(cur_w, src);
                 dw = ok ? w : 0.f;
             }
         };
 #pragma unroll
-        for (int sl = 0; sl < U; ++sl) issue(sl, false, ring[sl], ring_w[WEIGHTED ? sl : 0]);
+        for (int sl = 0; sl < U; ++sl)
+            issue(sl, false, ring[sl], ring_w[WEIGHTED ? sl : 0], ring_sb[kQuant ? sl : 0]);
 
         float acc[E::kPerVec];
 #pragma unroll
@@ -196,7 +275,8 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
 #pragma unroll
                 for (int sl = 0; sl < U; ++sl) {
                     const int32_t rp = base + s0 + sl;
-                    E::fma(acc, ring[sl], WEIGHTED ? ring_w[WEIGHTED ? sl : 0] : 1.0f);
+                    E::fma(acc, ring[sl], WEIGHTED ? ring_w[WEIGHTED ? sl : 0] : 1.0f,
+                           kQuant ? ring_sb[kQuant ? sl : 0] : float2{0.f, 0.f});
                     if (rp < Q && rp + 1 == bag_end) {
                         float *st = my_stage + bag * LPR * E::kPerVec;
 #pragma unroll
@@ -207,7 +287,8 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
                         while (bag + 1 < nbs && bag_end == rp + 1) bag_end = end_of(++bag);
                     }
                     const int ahead = s0 + sl + U;
-                    issue(ahead & (LPR - 1), ahead >= LPR, ring[sl], ring_w[WEIGHTED ? sl : 0]);
+                    issue(ahead & (LPR - 1), ahead >= LPR, ring[sl], ring_w[WEIGHTED ? sl : 0],
+                          ring_sb[kQuant ? sl : 0]);
                 }
             }
             cur_r = nxt_r;
@@ -217,20 +298,19 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
             load_chunk(base + 3 * LPR, far_idx, far_w);
         }
         if (oob) atomicOr(status, TBE_STATUS_INDEX_OOB);
-        // parked bags to memory; empty bags as +0.0
+        // parked bags to memory; empty bags as +0.0; mean pooling scales by fl32(1/L)
         if (vact) {
 #pragma unroll
             for (int i = 0; i < NB; ++i) {
                 if (i < nbs) {
-                    const bool empty = bnd[i] == bnd[i + 1];
+                    const int32_t L = bnd[i + 1] - bnd[i];
                     const float *st = my_stage + i * LPR * E::kPerVec;
-                    f4 *o = reinterpret_cast<f4 *>(out0 + static_cast<int64_t>(i) * total_dim + (c0 + v) * E::kPerVec);
+                    float val[E::kPerVec];
+                    const float inv = mean && L > 0 ? 1.0f / static_cast<float>(L) : 1.0f;
 #pragma unroll
-                    for (int q = 0; q < E::kPerVec / 4; ++q) {
-                        const f4 val = empty ? f4{0.f, 0.f, 0.f, 0.f}
-                                             : f4{st[4 * q], st[4 * q + 1], st[4 * q + 2], st[4 * q + 3]};
-                        __builtin_nontemporal_store(val, o + q);
-                    }
+                    for (int q = 0; q < E::kPerVec; ++q) val[q] = L == 0 ? 0.f : mean ? st[q] * inv : st[q];
+                    store_out<E::kPerVec>(out0 + (static_cast<int64_t>(i) * total_dim + (c0 + v) * E::kPerVec) * oes,
+                                          val, out_dt);
                 }
             }
         }
@@ -247,19 +327,19 @@ __device__ inline int table_of_unit(const TableMeta *__restrict__ meta, int T, i
     return lo;
 }
 
-template <int DT, bool WEIGHTED>
+template <int DT, bool WEIGHTED, typename IT>
 __global__ __launch_bounds__(kBlock) void forward_kernel(
-    const TableMeta *__restrict__ meta, int T, const char *__restrict__ tables,
-    const int64_t *__restrict__ indices, const int64_t *__restrict__ offsets,
-    const float *__restrict__ weights, float *__restrict__ out, int32_t *status, int64_t B,
-    int64_t nbags, int64_t N, int64_t total_dim, int64_t units, int check, const char *__restrict__ zero_page) {
+    const TableMeta *__restrict__ meta, int T, const char *__restrict__ tables, const IT *__restrict__ indices,
+    const IT *__restrict__ offsets, const float *__restrict__ weights, char *__restrict__ out, int32_t *status,
+    int64_t B, int64_t nbags, int64_t N, int64_t total_dim, int64_t units, int check,
+    const char *__restrict__ zero_page, int out_dt, int mean) {
     // finished bags of each lane group, parked until the stream ends
     __shared__ float stage_all[kWavesPerBlock][64 * kBagsPerGroup * 8];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t unit = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave;
     if (check && unit == 0 && lane == 0) {
-        if (offsets[0] != 0 || offsets[nbags] != N) atomicOr(status, TBE_STATUS_OFFSETS);
+        if (offsets[0] != 0 || static_cast<int64_t>(offsets[nbags]) != N) atomicOr(status, TBE_STATUS_OFFSETS);
     }
     if (unit >= units) return;
     const int t = table_of_unit(meta, T, unit);
@@ -267,14 +347,14 @@ __global__ __launch_bounds__(kBlock) void forward_kernel(
     const int64_t first = (unit - m.unit_base) * m.unit_bags;       // bag within the table
     const int nb = static_cast<int>(B - first < m.unit_bags ? B - first : m.unit_bags);
     const int64_t k0 = static_cast<int64_t>(t) * B + first;
-    constexpr int ES = DT == TBE_F32 ? 4 : 2;
+    constexpr int ES = DT == TBE_F32 ? 4 : DT == TBE_U8_ROWWISE ? 1 : 2;
     const char *table = tables + m.elem_offset * ES;
     float *stage = stage_all[wave];
     switch (m.lpr_log2) {
 #define TBE_POOL_CASE(L, LPR)                                                                                   \
     case L:                                                                                                     \
-        pool_unit<DT, LPR, WEIGHTED>(m, table, indices, weights, offsets, k0, nb, out, B, N, total_dim, check, \
-                                     status, lane, zero_page, stage);                                           \
+        pool_unit<DT, LPR, WEIGHTED, IT>(m, table, indices, weights, offsets, k0, nb, out, B, N, total_dim,    \
+                                         check, status, lane, zero_page, stage, out_dt, mean != 0);             \
         break;
         TBE_POOL_CASE(0, 1)
         TBE_POOL_CASE(1, 2)
@@ -290,24 +370,36 @@ __global__ __launch_bounds__(kBlock) void forward_kernel(
 
 }  // namespace
 
-hipError_t launch_forward(const Plan &p, const void *tables, const int64_t *indices,
-                          const int64_t *offsets, int64_t num_indices, const float *weights,
-                          float *out, int32_t *status, hipStream_t stream) {
+hipError_t launch_forward(const Plan &p, const void *tables, const void *indices, const void *offsets,
+                          int64_t num_indices, const float *weights, void *out, int32_t *status,
+                          hipStream_t stream) {
     const int64_t nbags = static_cast<int64_t>(p.T) * p.B;
     if (nbags == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>((p.fwd_units + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
     const char *tb = static_cast<const char *>(tables);
     const char *zp = static_cast<const char *>(p.zero_page);
-#define TBE_LAUNCH(DT, W)                                                                                    \
-    hipLaunchKernelGGL((forward_kernel<DT, W>), grid, block, 0, stream, p.meta_dev, p.T, tb, indices, offsets, \
-                       weights, out, status, p.B, nbags, num_indices, p.total_dim, p.fwd_units, p.bounds_check, \
-                       zp)
-    const bool w = weights != nullptr;
+    char *o = static_cast<char *>(out);
+    const int mean = p.pooling == TBE_POOL_MEAN;
+#define TBE_LAUNCH(DT, W, IT)                                                                                   \
+    hipLaunchKernelGGL((forward_kernel<DT, W, IT>), grid, block, 0, stream, p.meta_dev, p.T, tb,                \
+                       static_cast<const IT *>(indices), static_cast<const IT *>(offsets), weights, o, status, p.B, \
+                       nbags, num_indices, p.total_dim, p.fwd_units, p.bounds_check, zp, p.out_dtype, mean)
+#define TBE_LAUNCH_IT(DT, W)                                                                                    \
+    do {                                                                                                        \
+        if (p.index_type == TBE_INDEX_I32) TBE_LAUNCH(DT, W, int32_t); else TBE_LAUNCH(DT, W, int64_t);         \
+    } while (0)
+#define TBE_LAUNCH_W(DT)                                                                                        \
+    do {                                                                                                        \
+        if (weights) TBE_LAUNCH_IT(DT, true); else TBE_LAUNCH_IT(DT, false);                                    \
+    } while (0)
     switch (p.dtype) {
-        case TBE_F32: if (w) TBE_LAUNCH(TBE_F32, true); else TBE_LAUNCH(TBE_F32, false); break;
-        case TBE_F16: if (w) TBE_LAUNCH(TBE_F16, true); else TBE_LAUNCH(TBE_F16, false); break;
-        default: if (w) TBE_LAUNCH(TBE_BF16, true); else TBE_LAUNCH(TBE_BF16, false); break;
+        case TBE_F32: TBE_LAUNCH_W(TBE_F32); break;
+        case TBE_F16: TBE_LAUNCH_W(TBE_F16); break;
+        case TBE_BF16: TBE_LAUNCH_W(TBE_BF16); break;
+        default: TBE_LAUNCH_W(TBE_U8_ROWWISE); break;
     }
+#undef TBE_LAUNCH_W
+#undef TBE_LAUNCH_IT
 #undef TBE_LAUNCH
     return hipGetLastError();
 }

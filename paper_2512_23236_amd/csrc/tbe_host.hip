@@ -14,9 +14,24 @@ namespace {
 
 bool aligned16(const void *ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
 
+// indices / offsets: aligned to their element size
+bool index_aligned(const tbe::Plan &p, const void *ptr) {
+    const uintptr_t mask = p.index_type == TBE_INDEX_I32 ? 3u : 7u;
+    return (reinterpret_cast<uintptr_t>(ptr) & mask) == 0;
+}
+
+// the largest N that the plan's offsets can hold
+int64_t max_indices(const tbe::Plan &p) {
+    return p.index_type == TBE_INDEX_I32 ? (int64_t(1) << 31) - 1 : INT64_MAX;
+}
+
 int32_t validate_desc(const tbe_desc *d) {
     if (!d || !d->rows || !d->dims) return TBE_ERR_NULL;
-    if (d->dtype != TBE_F32 && d->dtype != TBE_F16 && d->dtype != TBE_BF16) return TBE_ERR_DTYPE;
+    if (d->dtype < TBE_F32 || d->dtype > TBE_U8_ROWWISE) return TBE_ERR_DTYPE;
+    if (d->out_dtype < TBE_F32 || d->out_dtype > TBE_BF16) return TBE_ERR_DTYPE;
+    if (d->index_type != TBE_INDEX_I64 && d->index_type != TBE_INDEX_I32) return TBE_ERR_DTYPE;
+    if (d->pooling != TBE_POOL_SUM && d->pooling != TBE_POOL_MEAN) return TBE_ERR_UNSUPPORTED;
+    const bool u8 = d->dtype == TBE_U8_ROWWISE;
     if (d->num_tables < 1 || d->batch_size < 0 || d->table_elems < 0) return TBE_ERR_SHAPE;
     if (d->bounds_check != 0 && d->bounds_check != 1) return TBE_ERR_SHAPE;
     // bag ids and output columns are kept in 32 bits on the device
@@ -27,12 +42,13 @@ int32_t validate_desc(const tbe_desc *d) {
         const int64_t R = d->rows[t];
         const int32_t D = d->dims[t];
         if (R < 1 || D < 1) return TBE_ERR_SHAPE;
-        if ((static_cast<int64_t>(D) * es) % 16 != 0) return TBE_ERR_ALIGN;
+        if (u8 ? D % 8 != 0 : (static_cast<int64_t>(D) * es) % 16 != 0) return TBE_ERR_ALIGN;
         if (R > (int64_t(1) << 40) || D > (1 << 20)) return TBE_ERR_SHAPE;
+        const int64_t row_elems = u8 ? D + 8 : D;
         const int64_t off = d->table_offsets ? d->table_offsets[t] : packed;
-        if (off < 0 || (off * es) % 16 != 0) return TBE_ERR_ALIGN;
-        if (off > d->table_elems || R * D > d->table_elems - off) return TBE_ERR_SHAPE;
-        packed += R * D;
+        if (off < 0 || (u8 ? off % 8 != 0 : (off * es) % 16 != 0)) return TBE_ERR_ALIGN;
+        if (off > d->table_elems || R * row_elems > d->table_elems - off) return TBE_ERR_SHAPE;
+        packed += R * row_elems;
         total_dim += D;
         total_rows += R;
         if (total_dim >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
@@ -59,6 +75,7 @@ const char *tbe_error_string(int32_t code) {
         case TBE_ERR_WORKSPACE: return "workspace smaller than required";
         case TBE_ERR_HIP: return "a HIP runtime call failed";
         case TBE_ERR_NOMEM: return "host allocation failed";
+        case TBE_ERR_UNSUPPORTED: return "the plan's options do not support this call";
         default: return "unknown error code";
     }
 }
@@ -76,6 +93,9 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
     p.dtype = desc->dtype;
     p.B = desc->batch_size;
     p.bounds_check = desc->bounds_check;
+    p.pooling = desc->pooling;
+    p.index_type = desc->index_type;
+    p.out_dtype = desc->out_dtype;
     p.table_elems = desc->table_elems;
     p.meta_host = new (std::nothrow) tbe::TableMeta[p.T];
     if (!p.meta_host) {
@@ -93,7 +113,9 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
         m.row_base = row_base;
         m.dim = D;
         m.dim_off = static_cast<int32_t>(dim_off);
-        m.nvec = static_cast<int32_t>(static_cast<int64_t>(D) * es / 16);
+        const bool u8 = p.dtype == TBE_U8_ROWWISE;
+        m.nvec = u8 ? D / 8 : static_cast<int32_t>(static_cast<int64_t>(D) * es / 16);
+        m.row_bytes = u8 ? D + 8 : D * es;
         int l = 0;
         while ((1 << l) < m.nvec && l < 6) ++l;
         m.lpr_log2 = l;
@@ -104,7 +126,7 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
         m.unit_base = p.fwd_units;
         p.fwd_units += (p.B + m.unit_bags - 1) / m.unit_bags;
         m.pad = 0;
-        packed += R * D;
+        packed += R * (u8 ? D + 8 : D);
         dim_off += D;
         row_base += R;
         if (D > p.max_dim) p.max_dim = D;
@@ -147,12 +169,13 @@ int32_t tbe_plan_info(const tbe_plan *plan, int64_t *total_dim, int64_t *total_r
     return TBE_OK;
 }
 
-int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *indices,
-                    const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
-                    float *out, int32_t *status, void *stream) {
+int32_t tbe_forward(const tbe_plan *plan, const void *tables, const void *indices, const void *offsets,
+                    int64_t num_indices, const float *per_sample_weights, void *out, int32_t *status,
+                    void *stream) {
     const tbe::Plan *p = plan_of(plan);
     if (!p) return TBE_ERR_NULL;
-    if (num_indices < 0) return TBE_ERR_SHAPE;
+    if (num_indices < 0 || num_indices > max_indices(*p)) return TBE_ERR_SHAPE;
+    if (p->pooling == TBE_POOL_MEAN && per_sample_weights) return TBE_ERR_UNSUPPORTED;
     const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
     if (!offsets && nbags > 0) return TBE_ERR_NULL;
     if (nbags == 0) return TBE_OK;  // empty output: nothing to write
@@ -160,7 +183,7 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const int64_t *ind
     if (num_indices > 0 && !indices) return TBE_ERR_NULL;
     if (p->bounds_check && !status) return TBE_ERR_NULL;
     if (!aligned16(tables) || !aligned16(out)) return TBE_ERR_ALIGN;
-    if ((reinterpret_cast<uintptr_t>(indices) & 7u) || (reinterpret_cast<uintptr_t>(offsets) & 7u) ||
+    if (!index_aligned(*p, indices) || !index_aligned(*p, offsets) ||
         (reinterpret_cast<uintptr_t>(per_sample_weights) & 3u))
         return TBE_ERR_ALIGN;
     const hipError_t e = tbe::launch_forward(*p, tables, indices, offsets, num_indices,
@@ -175,6 +198,7 @@ int32_t tbe_apply_gradient(const tbe_plan *plan, void *tables, const tbe_optimiz
     const tbe::Plan *p = plan_of(plan);
     if (!p || !opt) return TBE_ERR_NULL;
     if (opt->kind != TBE_OPT_SGD && opt->kind != TBE_OPT_ROWWISE_ADAGRAD) return TBE_ERR_SHAPE;
+    if (p->dtype == TBE_U8_ROWWISE) return TBE_ERR_UNSUPPORTED;
     if (max_unique < 0) return TBE_ERR_SHAPE;
     if (max_unique == 0) return TBE_OK;
     if (!tables || !grad_idx || !grad_row_offsets || !grad_rows || !num_unique) return TBE_ERR_NULL;
@@ -202,19 +226,20 @@ int32_t tbe_map_ids(const int64_t *values, int64_t num_values, const int64_t *ma
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
 }
 
-int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out, const int64_t *indices,
-                        const int64_t *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
+int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out, const void *indices,
+                        const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                         void *stream) {
     const tbe::Plan *p = plan_of(plan);
     if (!p) return TBE_ERR_NULL;
-    if (num_indices < 0) return TBE_ERR_SHAPE;
+    if (num_indices < 0 || num_indices > max_indices(*p)) return TBE_ERR_SHAPE;
+    if (p->pooling != TBE_POOL_SUM || p->dtype == TBE_U8_ROWWISE) return TBE_ERR_UNSUPPORTED;
     const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
     if (!offsets && nbags > 0) return TBE_ERR_NULL;
     if (nbags == 0 || num_indices == 0) return TBE_OK;  // nothing to write
     if (!tables || !grad_out || !indices || !grad_weights) return TBE_ERR_NULL;
     if (p->bounds_check && !status) return TBE_ERR_NULL;
     if (!aligned16(tables) || !aligned16(grad_out)) return TBE_ERR_ALIGN;
-    if ((reinterpret_cast<uintptr_t>(indices) & 7u) || (reinterpret_cast<uintptr_t>(offsets) & 7u) ||
+    if (!index_aligned(*p, indices) || !index_aligned(*p, offsets) ||
         (reinterpret_cast<uintptr_t>(grad_weights) & 3u))
         return TBE_ERR_ALIGN;
     const hipError_t e = tbe::launch_weight_grad(*p, tables, grad_out, indices, offsets, num_indices, grad_weights,
@@ -230,8 +255,8 @@ int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, 
     return TBE_OK;
 }
 
-int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t *indices,
-                     const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const void *indices,
+                     const void *offsets, int64_t num_indices, const float *per_sample_weights,
                      void *workspace, size_t workspace_bytes, float *grad_rows,
                      int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                      int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream) {
@@ -240,8 +265,8 @@ int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const int64_t 
                               grad_row_offsets, num_unique, status, stream, nullptr);
 }
 
-int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const int64_t *indices,
-                           const int64_t *offsets, int64_t num_indices, const float *per_sample_weights,
+int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const void *indices,
+                           const void *offsets, int64_t num_indices, const float *per_sample_weights,
                            void *workspace, size_t workspace_bytes, float *grad_rows,
                            int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                            int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream,
@@ -250,6 +275,7 @@ int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const in
     if (!p) return TBE_ERR_NULL;
     // sorted positions and segment ids are carried in 32 bits on the device
     if (num_indices < 0 || num_indices >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
+    if (p->pooling == TBE_POOL_MEAN && per_sample_weights) return TBE_ERR_UNSUPPORTED;
     // local row ids are 32-bit sort keys, with one key value kept for dropped lookups
     for (int32_t t = 0; t < p->T; ++t)
         if (p->meta_host[t].rows >= (int64_t(1) << 32) - 1) return TBE_ERR_SHAPE;
@@ -264,7 +290,7 @@ int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const in
     if (need > 0 && !workspace) return TBE_ERR_NULL;
     if ((reinterpret_cast<uintptr_t>(workspace) & 255u) || !aligned16(grad_rows) || !aligned16(grad_out))
         return TBE_ERR_ALIGN;
-    if ((reinterpret_cast<uintptr_t>(indices) & 7u) || (reinterpret_cast<uintptr_t>(offsets) & 7u) ||
+    if (!index_aligned(*p, indices) || !index_aligned(*p, offsets) ||
         (reinterpret_cast<uintptr_t>(grad_idx) & 7u) || (reinterpret_cast<uintptr_t>(seg_offsets) & 7u) ||
         (reinterpret_cast<uintptr_t>(grad_row_offsets) & 7u) ||
         (reinterpret_cast<uintptr_t>(num_unique) & 7u) ||

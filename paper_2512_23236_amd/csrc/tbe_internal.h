@@ -16,22 +16,27 @@ struct TableMeta {
     int64_t row_base;     // first global row id: sum of R_t' for t' < t
     int32_t dim;          // D_t
     int32_t dim_off;      // first output column: sum of D_t' for t' < t
-    int32_t nvec;         // 16-byte vectors per table row: D_t * elem_size / 16
+    int32_t nvec;         // load vectors per table row: D_t * elem_size / 16 (8-bit
+                          // row-wise tables: D_t / 8 vectors of 8 code bytes)
     int32_t lpr_log2;     // log2 of lanes per row: smallest power of two >= min(nvec, 64)
     int32_t glpr_log2;    // the same for an fp32 row of D_t (gradient rows): min(D_t / 4, 64)
     int32_t unit_bags;    // forward: bags per wave work unit (bags per lane group x groups per wave)
     int64_t unit_base;    // forward: work units of all tables before t
-    int64_t pad;
+    int32_t row_bytes;    // bytes per stored row (8-bit row-wise: D_t codes + scale + bias)
+    int32_t pad;
 };
 static_assert(sizeof(TableMeta) == 64, "TableMeta layout");
 
-inline int elem_size(int dtype) { return dtype == TBE_F32 ? 4 : 2; }
+inline int elem_size(int dtype) { return dtype == TBE_F32 ? 4 : dtype == TBE_U8_ROWWISE ? 1 : 2; }
 
 struct Plan {
     int32_t T = 0;
     int32_t dtype = 0;
     int32_t bounds_check = 0;
     int32_t key_bits = 0;      // bits of the largest global row id (>= 1)
+    int32_t pooling = 0;       // tbe_pooling
+    int32_t index_type = 0;    // tbe_index_type of indices and offsets
+    int32_t out_dtype = 0;     // tbe_dtype of the forward output
     int64_t B = 0;
     int64_t total_dim = 0;
     int64_t total_rows = 0;
@@ -45,9 +50,9 @@ struct Plan {
 };
 
 // Forward: queues the pooled lookup of every (bag, table) on `stream`.
-hipError_t launch_forward(const Plan &p, const void *tables, const int64_t *indices,
-                          const int64_t *offsets, int64_t num_indices, const float *weights,
-                          float *out, int32_t *status, hipStream_t stream);
+hipError_t launch_forward(const Plan &p, const void *tables, const void *indices, const void *offsets,
+                          int64_t num_indices, const float *weights, void *out, int32_t *status,
+                          hipStream_t stream);
 
 // One optimizer step on the rows of a sparse gradient.
 hipError_t launch_apply_gradient(const Plan &p, void *tables, int32_t kind, float lr, float eps, float *state,
@@ -59,14 +64,14 @@ hipError_t launch_map_ids(const int64_t *values, int64_t n, const int64_t *mappi
                           hipStream_t stream);
 
 // Gradient with respect to the per-sample weights.
-hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const int64_t *indices,
-                              const int64_t *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
+hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const void *indices,
+                              const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                               hipStream_t stream);
 
 // Backward: workspace size and the full sort + segmented-reduce pipeline.
 size_t backward_workspace_bytes(const Plan &p, int64_t num_indices);
-hipError_t launch_backward(const Plan &p, const float *grad_out, const int64_t *indices,
-                           const int64_t *offsets, int64_t num_indices, const float *weights,
+hipError_t launch_backward(const Plan &p, const float *grad_out, const void *indices,
+                           const void *offsets, int64_t num_indices, const float *weights,
                            void *workspace, size_t workspace_bytes, float *grad_rows,
                            int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                            int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status,

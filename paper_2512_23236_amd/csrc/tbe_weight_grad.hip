@@ -58,10 +58,10 @@ struct Wide<TBE_BF16> {
     }
 };
 
-template <int DT>
+template <int DT, typename IT>
 __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
-    const TableMeta *__restrict__ meta, const char *__restrict__ tables, const int64_t *__restrict__ indices,
-    const int64_t *__restrict__ offsets, const float *__restrict__ grad_out, float *__restrict__ grad_w,
+    const TableMeta *__restrict__ meta, const char *__restrict__ tables, const IT *__restrict__ indices,
+    const IT *__restrict__ offsets, const float *__restrict__ grad_out, float *__restrict__ grad_w,
     int32_t *status, int64_t B, int64_t nbags, int64_t N, int64_t total_dim, int check,
     const char *__restrict__ zero_page) {
     constexpr int KV = Wide<DT>::kPerVec;
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
     if (k >= nbags) return;
     const int64_t t = k / B, b = k - t * B;
     const TableMeta m = meta[t];
-    int64_t s = offsets[k], e = offsets[k + 1];
+    int64_t s = static_cast<int64_t>(offsets[k]), e = static_cast<int64_t>(offsets[k + 1]);
     if (check) {
         // malformed offsets: flag, and keep every access inside [0, N)
         const int64_t cs = s < 0 ? 0 : (s > N ? N : s);
@@ -96,7 +96,7 @@ __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
         for (int i = 0; i < KV; ++i) gc[i] = vact ? grow[(c0 + v) * KV + i] : 0.f;
         for (int64_t base = s; base < e; base += 64) {
             const int cnt = e - base < 64 ? static_cast<int>(e - base) : 64;
-            const int64_t my_idx = lane < cnt ? indices[base + lane] : 0;
+            const int64_t my_idx = lane < cnt ? static_cast<int64_t>(indices[base + lane]) : 0;
             for (int r0 = 0; r0 < cnt; r0 += G * kAhead) {
                 uint4 rowv[kAhead];
                 bool keep[kAhead];
@@ -131,23 +131,29 @@ __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
 
 }  // namespace
 
-hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const int64_t *indices,
-                              const int64_t *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
+hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const void *indices,
+                              const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                               hipStream_t stream) {
     const int64_t nbags = static_cast<int64_t>(p.T) * p.B;
     if (nbags == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>((nbags + kWgWaves - 1) / kWgWaves)), block(64 * kWgWaves);
     const char *tb = static_cast<const char *>(tables);
     const char *zp = static_cast<const char *>(p.zero_page);
+#define TBE_LAUNCH_IT(DT, IT)                                                                                 \
+    hipLaunchKernelGGL((weight_grad_kernel<DT, IT>), grid, block, 0, stream, p.meta_dev, tb,                   \
+                       static_cast<const IT *>(indices), static_cast<const IT *>(offsets), grad_out, grad_weights, \
+                       status, p.B, nbags, num_indices, p.total_dim, p.bounds_check, zp)
 #define TBE_LAUNCH(DT)                                                                                        \
-    hipLaunchKernelGGL((weight_grad_kernel<DT>), grid, block, 0, stream, p.meta_dev, tb, indices, offsets,     \
-                       grad_out, grad_weights, status, p.B, nbags, num_indices, p.total_dim, p.bounds_check, zp)
+    do {                                                                                                      \
+        if (p.index_type == TBE_INDEX_I32) TBE_LAUNCH_IT(DT, int32_t); else TBE_LAUNCH_IT(DT, int64_t);       \
+    } while (0)
     switch (p.dtype) {
         case TBE_F32: TBE_LAUNCH(TBE_F32); break;
         case TBE_F16: TBE_LAUNCH(TBE_F16); break;
         default: TBE_LAUNCH(TBE_BF16); break;
     }
 #undef TBE_LAUNCH
+#undef TBE_LAUNCH_IT
     return hipGetLastError();
 }
 

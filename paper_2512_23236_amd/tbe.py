@@ -16,10 +16,15 @@ import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtbe.so")
-ABI_VERSION = 1
+ABI_VERSION = 2
 
-F32, F16, BF16 = 0, 1, 2
-DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+F32, F16, BF16, U8_ROWWISE = 0, 1, 2, 3
+# table storage type -> tbe_dtype; torch.uint8 tables are 8-bit row-wise (rows of
+# D codes followed by an fp32 scale and bias)
+DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16, torch.uint8: U8_ROWWISE}
+OUT_DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+POOLING_CODE = {"sum": 0, "mean": 1}
+INDEX_TYPE_CODE = {torch.int64: 0, torch.int32: 1}
 
 STATUS_INDEX_OOB, STATUS_OFFSETS, STATUS_CAPACITY = 1, 2, 4
 PHASES = ("keys", "sort", "segments", "reduce", "combine")  # tbe_backward_phase order
@@ -45,6 +50,9 @@ class _Desc(ctypes.Structure):
         ("table_offsets", ctypes.c_void_p),
         ("table_elems", ctypes.c_int64),
         ("bounds_check", ctypes.c_int32),
+        ("pooling", ctypes.c_int32),
+        ("index_type", ctypes.c_int32),
+        ("out_dtype", ctypes.c_int32),
     ]
 
 
@@ -113,23 +121,31 @@ class Plan:
 
     def __init__(self, rows: Sequence[int], dims: Sequence[int], dtype: torch.dtype, batch_size: int,
                  table_offsets: Optional[Sequence[int]] = None, table_elems: Optional[int] = None,
-                 bounds_check: bool = True, device=None):
+                 bounds_check: bool = True, device=None, pooling: str = "sum",
+                 index_dtype: torch.dtype = torch.int64, out_dtype: torch.dtype = torch.float32):
         lib_ = _load()
         self.rows = np.ascontiguousarray(rows, dtype=np.int64)
         self.dims = np.ascontiguousarray(dims, dtype=np.int32)
         self.T = int(self.rows.size)
         self.B = int(batch_size)
         self.dtype = dtype
+        self.pooling = pooling
+        self.index_dtype = index_dtype
+        self.out_dtype = out_dtype
         self.bounds_check = bool(bounds_check)
         self.table_offsets = None if table_offsets is None else np.ascontiguousarray(table_offsets, dtype=np.int64)
         if table_elems is None:
-            table_elems = int((self.rows * self.dims.astype(np.int64)).sum())
+            extra = 8 if dtype == torch.uint8 else 0
+            table_elems = int((self.rows * (self.dims.astype(np.int64) + extra)).sum())
         self.table_elems = int(table_elems)
-        if dtype not in DTYPE_CODE:
+        if dtype not in DTYPE_CODE or out_dtype not in OUT_DTYPE_CODE or index_dtype not in INDEX_TYPE_CODE:
             raise TBEError(-3, "Plan")
+        if pooling not in POOLING_CODE:
+            raise TBEError(-8, "Plan")
         d = _Desc(self.T, DTYPE_CODE[dtype], self.B, self.rows.ctypes.data, self.dims.ctypes.data,
                   None if self.table_offsets is None else self.table_offsets.ctypes.data,
-                  self.table_elems, int(self.bounds_check))
+                  self.table_elems, int(self.bounds_check), POOLING_CODE[pooling], INDEX_TYPE_CODE[index_dtype],
+                  OUT_DTYPE_CODE[out_dtype])
         self.device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
         self._h = ctypes.c_void_p()
         with torch.cuda.device(self.device):
@@ -166,10 +182,11 @@ def _dev_tensor(t: torch.Tensor, dtype, name: str, plan: Plan):
 def forward(plan: Plan, tables: torch.Tensor, indices: torch.Tensor, offsets: torch.Tensor,
             per_sample_weights: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
             status: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Pooled lookup: returns out [B, total_dim] fp32 (written on the current stream)."""
+    """Pooled lookup: returns out [B, total_dim] of the plan's out_dtype
+    (written on the current stream)."""
     _dev_tensor(tables, plan.dtype, "tables", plan)
-    _dev_tensor(indices, torch.int64, "indices", plan)
-    _dev_tensor(offsets, torch.int64, "offsets", plan)
+    _dev_tensor(indices, plan.index_dtype, "indices", plan)
+    _dev_tensor(offsets, plan.index_dtype, "offsets", plan)
     if offsets.numel() != plan.T * plan.B + 1:
         raise ValueError(f"offsets has {offsets.numel()} entries, expected T*B+1 = {plan.T * plan.B + 1}")
     if per_sample_weights is not None:
@@ -177,8 +194,8 @@ def forward(plan: Plan, tables: torch.Tensor, indices: torch.Tensor, offsets: to
         if per_sample_weights.numel() != indices.numel():
             raise ValueError("per_sample_weights must have one weight per index")
     if out is None:
-        out = torch.empty((plan.B, plan.total_dim), dtype=torch.float32, device=plan.device)
-    _dev_tensor(out, torch.float32, "out", plan)
+        out = torch.empty((plan.B, plan.total_dim), dtype=plan.out_dtype, device=plan.device)
+    _dev_tensor(out, plan.out_dtype, "out", plan)
     if out.numel() != plan.B * plan.total_dim:
         raise ValueError("out must be [B, total_dim]")
     if status is not None:
@@ -236,8 +253,8 @@ def weight_grad(plan: Plan, tables: torch.Tensor, grad_out: torch.Tensor, indice
     N = indices.numel()
     _dev_tensor(tables, plan.dtype, "tables", plan)
     _dev_tensor(grad_out, torch.float32, "grad_out", plan)
-    _dev_tensor(indices, torch.int64, "indices", plan)
-    _dev_tensor(offsets, torch.int64, "offsets", plan)
+    _dev_tensor(indices, plan.index_dtype, "indices", plan)
+    _dev_tensor(offsets, plan.index_dtype, "offsets", plan)
     if grad_out.numel() != plan.B * plan.total_dim:
         raise ValueError("grad_out must be [B, total_dim]")
     if offsets.numel() != plan.T * plan.B + 1:
@@ -292,8 +309,8 @@ def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets:
     the backward (tbe_backward_timed); event i .. i+1 brackets phase i."""
     N = indices.numel()
     _dev_tensor(grad_out, torch.float32, "grad_out", plan)
-    _dev_tensor(indices, torch.int64, "indices", plan)
-    _dev_tensor(offsets, torch.int64, "offsets", plan)
+    _dev_tensor(indices, plan.index_dtype, "indices", plan)
+    _dev_tensor(offsets, plan.index_dtype, "offsets", plan)
     if grad_out.numel() != plan.B * plan.total_dim:
         raise ValueError("grad_out must be [B, total_dim]")
     if offsets.numel() != plan.T * plan.B + 1:
@@ -305,7 +322,7 @@ def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets:
         if grad_rows_capacity is None:
             # bound: every lookup its own row; needs the per-table lookup counts
             # (one small device-to-host copy of T+1 offsets)
-            bounds = offsets[:: plan.B].cpu().numpy() if plan.B else np.zeros(plan.T + 1, np.int64)
+            bounds = offsets[:: plan.B].cpu().numpy().astype(np.int64) if plan.B else np.zeros(plan.T + 1, np.int64)
             grad_rows_capacity = int((np.diff(bounds) * plan.dims.astype(np.int64)).sum()) if N else 0
         outputs = SparseGrad(
             torch.empty(max(grad_rows_capacity, 1), dtype=torch.float32, device=dev),

@@ -12,8 +12,9 @@ import workloads
 from paper_2512_23236_amd import tbe
 
 # Tolerances under the summation-normalised error |y - y_ref| / sum|terms|:
-# 1e-5 for fp32 tables and 2e-3 for fp16 / bf16 tables.
-RTOL = {"f32": 1e-5, "f16": 2e-3, "bf16": 2e-3}
+# 1e-5 for fp32 tables and for 8-bit row-wise tables (dequantised by one fp32
+# fma, then the same fp32 accumulation), 2e-3 for fp16 / bf16 tables.
+RTOL = {"f32": 1e-5, "f16": 2e-3, "bf16": 2e-3, "u8": 1e-5}
 
 
 def note(msg: str):
@@ -28,12 +29,21 @@ def device():
 def raw_tables(spec, flat_host: torch.Tensor):
     """Per-table numpy views of the flat buffer in the oracle's storage form."""
     offs = spec.table_offsets
+    re = spec.row_elems
     tabs = []
     for t in range(spec.T):
-        R, D = int(spec.rows[t]), int(spec.dims[t])
-        v = flat_host[int(offs[t]): int(offs[t]) + R * D].view(R, D)
-        tabs.append(v.numpy() if spec.dtype == "f32" else v.view(torch.int16).numpy())
+        R, E = int(spec.rows[t]), int(re[t])
+        v = flat_host[int(offs[t]): int(offs[t]) + R * E].view(R, E)
+        tabs.append(_storage(spec, v))
     return tabs
+
+
+def _storage(spec, v: torch.Tensor) -> np.ndarray:
+    """A table slice as the oracle reads it: fp32 as is, 16-bit types as raw
+    words, 8-bit row-wise rows as bytes."""
+    if spec.dtype in ("f32", "u8"):
+        return v.numpy()
+    return v.view(torch.int16).numpy()
 
 
 def plan_for(spec, bounds_check=True):
@@ -48,14 +58,14 @@ def run_forward(spec, d, bounds_check=True):
     return out, int(status.item())
 
 
-def oracle_forward_full(spec, d):
+def oracle_forward_full(spec, d, pooling="sum"):
     h = {k: (v.cpu() if torch.is_tensor(v) else v) for k, v in d.items()}
     w = None if h.get("weights") is None else h["weights"].numpy()
     return oracle.forward(spec.rows, spec.dims, spec.dtype, raw_tables(spec, h["tables"]), h["indices"].numpy(),
-                          h["offsets"].numpy(), spec.B, w)
+                          h["offsets"].numpy(), spec.B, w, pooling=pooling)
 
 
-def oracle_forward_bags(spec, d, bags):
+def oracle_forward_bags(spec, d, bags, pooling="sum"):
     """Oracle results of selected bags k = t*B + b only, from the rows those
     bags touch (copied from the generated tables).  Returns {k: (ref, abs)}."""
     off = d["offsets"]
@@ -66,16 +76,17 @@ def oracle_forward_bags(spec, d, bags):
         s, e = int(bounds[k]), int(bounds[k + 1])
         idx = d["indices"][s:e].cpu().numpy()
         uniq, inv = np.unique(idx, return_inverse=True)
-        R, D = int(spec.rows[t]), int(spec.dims[t])
+        R, D, E = int(spec.rows[t]), int(spec.dims[t]), int(spec.row_elems[t])
         base = int(spec.table_offsets[t])
-        full = d["tables"][base: base + R * D].view(R, D)
+        full = d["tables"][base: base + R * E].view(R, E)
         rows = full[torch.as_tensor(uniq, device=full.device)].cpu() if len(uniq) else full[:0].cpu()
-        tab = rows.numpy() if spec.dtype == "f32" else rows.view(torch.int16).numpy()
+        tab = _storage(spec, rows)
         w = None if d.get("weights") is None else d["weights"][s:e].cpu().numpy()
         n_rows = max(len(uniq), 1)
         if len(uniq) == 0:
-            tab = np.zeros((1, D), tab.dtype)
-        ref, ab = oracle.forward([n_rows], [D], spec.dtype, [tab], inv.astype(np.int64), [0, e - s], 1, w)
+            tab = np.zeros((1, E), tab.dtype)
+        ref, ab = oracle.forward([n_rows], [D], spec.dtype, [tab], inv.astype(np.int64), [0, e - s], 1, w,
+                                 pooling=pooling)
         res[int(k)] = (ref[0], ab[0])
     return res
 

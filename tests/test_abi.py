@@ -33,14 +33,16 @@ def test_library_exports_every_declared_symbol():
     assert tbe.lib().tbe_abi_version() == tbe.ABI_VERSION
 
 
-def _desc(rows=(100, 50), dims=(64, 128), dtype=tbe.F16, B=4, offs=None, elems=None, check=1, T=None):
+def _desc(rows=(100, 50), dims=(64, 128), dtype=tbe.F16, B=4, offs=None, elems=None, check=1, T=None,
+          pooling=0, index_type=0, out_dtype=0):
     r = np.ascontiguousarray(rows, np.int64)
     d = np.ascontiguousarray(dims, np.int32)
     o = None if offs is None else np.ascontiguousarray(offs, np.int64)
     if elems is None:
-        elems = int((r * d.astype(np.int64)).sum())
+        extra = 8 if dtype == tbe.U8_ROWWISE else 0
+        elems = int((r * (d.astype(np.int64) + extra)).sum())
     desc = tbe._Desc(len(r) if T is None else T, dtype, B, r.ctypes.data, d.ctypes.data,
-                     None if o is None else o.ctypes.data, elems, check)
+                     None if o is None else o.ctypes.data, elems, check, pooling, index_type, out_dtype)
     desc._keep = (r, d, o)
     return desc
 
@@ -63,6 +65,13 @@ def _create(desc):
     (dict(offs=(0, 6408)), -2),                 # table 1 runs past the end of the buffer
     (dict(check=2), -2),
     (dict(B=1 << 30), -2),                      # T*B beyond 32-bit bag ids
+    (dict(pooling=2), -8),                      # unknown pooling mode
+    (dict(index_type=2), -3),                   # unknown index type
+    (dict(out_dtype=3), -3),                    # 8-bit row-wise is a table format only
+    (dict(out_dtype=-1), -3),
+    (dict(dtype=tbe.U8_ROWWISE, dims=(64, 12)), -4),          # 8-bit rows need D % 8 == 0
+    (dict(dtype=tbe.U8_ROWWISE, offs=(0, 7204)), -4),         # 8-bit table offsets are 8-byte aligned
+    (dict(dtype=tbe.U8_ROWWISE, offs=(0, 7200), elems=7200 + 50 * 136 - 1), -2),  # last row past the end
 ])
 def test_plan_create_rejects_bad_descriptors(kwargs, code):
     rc, h = _create(_desc(**kwargs))
@@ -89,7 +98,7 @@ def test_null_arguments_rejected_without_a_device():
 
 def test_error_strings():
     lib = tbe.lib()
-    for code in range(0, -8, -1):
+    for code in range(0, -9, -1):
         s = lib.tbe_error_string(code)
         assert s and s != b"unknown error code"
     assert lib.tbe_error_string(-99) == b"unknown error code"
