@@ -44,32 +44,35 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def forward_bytes(spec, offsets_host: np.ndarray) -> int:
-    """Algorithmic bytes of one forward launch: each lookup reads its row
-    (D_t * elem_size) and its int64 index (+ a 4-byte weight when weighted);
-    each bag reads one int64 offset and writes D_t fp32 outputs."""
+def forward_bytes(spec, offsets_host: np.ndarray, index_bytes: int = 8, out_bytes: int = 4) -> int:
+    """Algorithmic bytes of one forward launch: each lookup reads its stored
+    row (D_t * elem_size; D_t + 8 for an 8-bit row-wise row with its scale and
+    bias) and its index (+ a 4-byte weight when weighted); each bag reads one
+    offset and writes D_t outputs."""
     B = spec.B
     per_table_lookups = offsets_host[np.arange(1, spec.T + 1) * B] - offsets_host[np.arange(spec.T) * B]
     dims = spec.dims.astype(np.int64)
-    rows = int((per_table_lookups * dims).sum()) * spec.elem_size
+    rows = int((per_table_lookups * spec.row_elems).sum()) * spec.elem_size
     n = int(offsets_host[-1])
-    idx = 8 * n + (4 * n if spec.weighted else 0)
-    bags = 8 * (spec.T * B + 1) + 4 * B * int(dims.sum())
+    idx = index_bytes * n + (4 * n if spec.weighted else 0)
+    bags = index_bytes * (spec.T * B + 1) + out_bytes * B * int(dims.sum())
     return rows + idx + bags
 
 
-def backward_bytes(spec, N: int, U: int, grad_floats: int) -> int:
-    """Compulsory bytes of one backward: int64 indices and offsets read, the
-    fp32 output gradient read once, int64 row ids, segment offsets and row
-    offsets written, and the fp32 gradient rows written."""
-    return 8 * N + 8 * (spec.T * spec.B + 1) + 4 * spec.B * spec.total_dim + 3 * 8 * (U + 1) + 4 * grad_floats
+def backward_bytes(spec, N: int, U: int, grad_floats: int, index_bytes: int = 8) -> int:
+    """Compulsory bytes of one backward: indices and offsets read, the fp32
+    output gradient read once, int64 row ids, segment offsets and row offsets
+    written, and the fp32 gradient rows written."""
+    return (index_bytes * N + index_bytes * (spec.T * spec.B + 1) + 4 * spec.B * spec.total_dim
+            + 3 * 8 * (U + 1) + 4 * grad_floats)
 
 
-def reduce_bytes(spec, N: int, grad_floats: int) -> int:
+def reduce_bytes(spec, N: int, grad_floats: int, carries_weight: bool) -> int:
     """Algorithmic bytes of one segmented-reduce launch: each sorted lookup's
-    key and batch row (4 + 4 bytes, + 4 for its weight), the fp32 output
-    gradient read once, and the fp32 gradient rows written."""
-    return (8 + (4 if spec.weighted else 0)) * N + 4 * spec.B * spec.total_dim + 4 * grad_floats
+    key and batch row (4 + 4 bytes, + 4 for its weight: the per-sample weight,
+    or 1/L under mean pooling), the fp32 output gradient read once, and the
+    fp32 gradient rows written."""
+    return (8 + (4 if carries_weight else 0)) * N + 4 * spec.B * spec.total_dim + 4 * grad_floats
 
 
 # Counter-derived HBM traffic per launch, with the hash of the kernel source it
@@ -109,7 +112,7 @@ def measured_traffic(kernel: str, workload: str):
         return None
 
 
-def cpu_baseline(spec, d, target_s: float):
+def cpu_baseline(spec, d, target_s: float, pooling: str = "sum"):
     """The CPU oracle on a bounded sample: the first b_s bags of every table,
     their rows copied into compact host tables; b_s is sized so the oracle
     runs for roughly target_s seconds."""
@@ -122,13 +125,13 @@ def cpu_baseline(spec, d, target_s: float):
         tabs, idx_parts, lens, rows, w_parts = [], [], [], [], []
         for t in range(spec.T):
             s, e = int(off[t * spec.B]), int(off[t * spec.B + bs])
-            idx = d["indices"][s:e].cpu().numpy()
+            idx = d["indices"][s:e].cpu().numpy().astype(np.int64)
             uniq, inv = np.unique(idx, return_inverse=True)
-            R, D = int(spec.rows[t]), int(spec.dims[t])
+            R, E = int(spec.rows[t]), int(spec.row_elems[t])
             base = int(spec.table_offsets[t])
-            full = d["tables"][base: base + R * D].view(R, D)
+            full = d["tables"][base: base + R * E].view(R, E)
             sel = full[torch.as_tensor(uniq, device=full.device)].cpu() if len(uniq) else full[:1].cpu()
-            tabs.append(sel.numpy() if spec.dtype == "f32" else sel.view(torch.int16).numpy())
+            tabs.append(sel.numpy() if spec.dtype in ("f32", "u8") else sel.view(torch.int16).numpy())
             rows.append(max(len(uniq), 1))
             idx_parts.append(inv.astype(np.int64))
             lens.append(np.diff(off[t * spec.B: t * spec.B + bs + 1]))
@@ -142,7 +145,7 @@ def cpu_baseline(spec, d, target_s: float):
     def run(bs):
         tabs, rows, indices, offsets, w = sample(bs)
         t0 = time.perf_counter()
-        oracle.forward(rows, spec.dims, spec.dtype, tabs, indices, offsets, bs, w)
+        oracle.forward(rows, spec.dims, spec.dtype, tabs, indices, offsets, bs, w, pooling=pooling)
         return time.perf_counter() - t0, indices.size
 
     bs = max(1, min(spec.B, 64))
@@ -285,6 +288,34 @@ def bench_map_ids(args, dev, n_unique=10000, batch=50000):
     print(json.dumps(res), flush=True)
 
 
+def variant_tag(args, spec) -> str:
+    """Suffix naming the non-default options (traffic summaries are per variant)."""
+    tag = ""
+    if args.table_dtype and args.table_dtype != workloads.make_config(args.config, args.seed).dtype:
+        tag += f"_{spec.dtype}"
+    if args.pooling != "sum":
+        tag += f"_{args.pooling}"
+    if args.index_type != "i64":
+        tag += f"_{args.index_type}"
+    if args.out_dtype != "f32":
+        tag += f"_out{args.out_dtype}"
+    return tag
+
+
+def variant_text(args, spec) -> str:
+    parts = []
+    if args.table_dtype and args.table_dtype != workloads.make_config(args.config, args.seed).dtype:
+        parts.append(f"tables redrawn as {spec.dtype}" + (" (8-bit row-wise: codes + fp32 scale/bias per row)"
+                                                         if spec.dtype == "u8" else ""))
+    if args.pooling != "sum":
+        parts.append(f"{args.pooling} pooling")
+    if args.index_type != "i64":
+        parts.append("int32 indices and offsets")
+    if args.out_dtype != "f32":
+        parts.append(f"{args.out_dtype} output")
+    return ("; " + ", ".join(parts)) if parts else ""
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -299,6 +330,13 @@ def main():
                          "gradient alone (use --config 4); map_ids: the MapId preprocessing step at the "
                          "evaluation's largest shape (10000 ids x 50000 values); sgd / adagrad: the optimizer "
                          "step alone, on the sparse gradient of one cfg5 backward")
+    ap.add_argument("--pooling", default="sum", choices=["sum", "mean"])
+    ap.add_argument("--index-type", default="i64", choices=["i64", "i32"],
+                    help="integer type of indices and offsets")
+    ap.add_argument("--out-dtype", default="f32", choices=["f32", "f16", "bf16"],
+                    help="element type of the forward output")
+    ap.add_argument("--table-dtype", default=None, choices=["f32", "f16", "bf16", "u8"],
+                    help="redraw the configuration's tables in this type (u8: 8-bit row-wise)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only copy a device buffer of this size 3 times (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -321,6 +359,10 @@ def main():
     if args.op == "map_ids":
         return bench_map_ids(args, dev)
     spec = workloads.make_config(args.config, args.seed)
+    if args.table_dtype:
+        spec = __import__("dataclasses").replace(spec, dtype=args.table_dtype)
+    if args.pooling == "mean" and spec.weighted:
+        spec = __import__("dataclasses").replace(spec, weighted=False)  # mean pooling takes no weights
     if args.op == "weight_grad":
         return bench_weight_grad(args, spec, dev)
     if args.op in ("sgd", "adagrad"):
@@ -328,16 +370,22 @@ def main():
     log(f"[bench] generating {spec.name}: {spec.table_bytes / 1e9:.2f} GB of tables")
     t0 = time.time()
     d = workloads.gen_all(spec, dev)
+    index_dtype = torch.int32 if args.index_type == "i32" else torch.int64
+    if args.index_type == "i32":
+        d["indices"] = d["indices"].to(torch.int32)
+        d["offsets"] = d["offsets"].to(torch.int32)
+    out_dtype = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[args.out_dtype]
     torch.cuda.synchronize()
     log(f"[bench] inputs ready in {time.time() - t0:.1f} s, N = {d['N']}")
-    plan = tbe.Plan(spec.rows, spec.dims, spec.torch_dtype, spec.B, bounds_check=True, device=dev)
+    plan = tbe.Plan(spec.rows, spec.dims, spec.torch_dtype, spec.B, bounds_check=True, device=dev,
+                    pooling=args.pooling, index_dtype=index_dtype, out_dtype=out_dtype)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
-    out = torch.empty((spec.B, plan.total_dim), dtype=torch.float32, device=dev)
+    out = torch.empty((spec.B, plan.total_dim), dtype=out_dtype, device=dev)
     training = spec.grad
     grads = None
     if training:
         N = d["N"]
-        bounds = d["offsets"][:: spec.B].cpu().numpy()
+        bounds = d["offsets"][:: spec.B].cpu().numpy().astype(np.int64)
         cap = int((np.diff(bounds) * spec.dims.astype(np.int64)).sum())
         grads = tbe.SparseGrad(torch.empty(cap, dtype=torch.float32, device=dev),
                                torch.empty(N, dtype=torch.int64, device=dev),
@@ -379,8 +427,9 @@ def main():
                 if training else None)
     ms_per_step = wall * 1e3 / args.steps
     N = d["N"]
-    off_host = d["offsets"].cpu().numpy()
-    fbytes = forward_bytes(spec, off_host)
+    off_host = d["offsets"].cpu().numpy().astype(np.int64)
+    ib = 4 if args.index_type == "i32" else 8
+    fbytes = forward_bytes(spec, off_host, ib, 4 if args.out_dtype == "f32" else 2)
     achieved = fbytes / (fwd_avg * 1e-3) / 1e9
 
     res = {
@@ -396,15 +445,16 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded counter-based draws; no production data)",
-        "config": {"workload": DESCRIPTIONS[args.config], "tables": spec.T, "batch": spec.B,
-                   "table_dtype": spec.dtype, "lookups": N, "table_bytes": spec.table_bytes,
-                   "total_dim": plan.total_dim, "seed": spec.seed, "training": training},
+        "config": {"workload": DESCRIPTIONS[args.config] + variant_text(args, spec), "tables": spec.T,
+                   "batch": spec.B, "table_dtype": spec.dtype, "lookups": N, "table_bytes": spec.table_bytes,
+                   "total_dim": plan.total_dim, "seed": spec.seed, "training": training,
+                   "pooling": args.pooling, "index_type": args.index_type, "out_dtype": args.out_dtype},
         "forward": {"ms": fwd_avg, "ms_p10": float(np.percentile(fwd_ms, 10)),
                     "ms_p90": float(np.percentile(fwd_ms, 90)), "lookups_per_s": N / (fwd_avg * 1e-3),
                     "algorithmic_bytes": fbytes, "effective_GBps": achieved,
                     "frac_of_hbm_peak": achieved / HBM_PEAK_GBS},
     }
-    workload = f"cfg{args.config}"
+    workload = f"cfg{args.config}" + variant_tag(args, spec)
     roof = {"forward_kernel": {"bound": "hbm", "kernel": "forward_kernel", "ms": fwd_avg, "achieved": achieved,
                                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                                "traffic": measured_traffic("forward_kernel", workload), "algorithmic_bytes": fbytes}}
@@ -412,7 +462,7 @@ def main():
         bwd_avg = float(np.mean(bwd_ms))
         U = grads.num_unique()
         gro_total = int(grads.grad_row_offsets[U].item())
-        bbytes = backward_bytes(spec, N, U, gro_total)
+        bbytes = backward_bytes(spec, N, U, gro_total, ib)
         res["backward"] = {"ms": bwd_avg, "ms_p10": float(np.percentile(bwd_ms, 10)),
                            "ms_p90": float(np.percentile(bwd_ms, 90)), "lookups_per_s": N / (bwd_avg * 1e-3),
                            "unique_rows": U, "compulsory_bytes": bbytes,
@@ -420,7 +470,7 @@ def main():
                            "frac_of_hbm_peak": bbytes / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
                            "phases_ms": {name: float(np.mean(t)) for name, t in zip(tbe.PHASES, phase_ms)}}
         red_ms = float(np.mean(phase_ms[tbe.PHASES.index("reduce")]))
-        rbytes = reduce_bytes(spec, N, gro_total)
+        rbytes = reduce_bytes(spec, N, gro_total, spec.weighted or args.pooling == "mean")
         red_gbs = rbytes / (red_ms * 1e-3) / 1e9
         roof["reduce_kernel"] = {"bound": "hbm", "kernel": "reduce_kernel", "ms": red_ms, "achieved": red_gbs,
                                  "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": red_gbs / HBM_PEAK_GBS,
@@ -434,7 +484,7 @@ def main():
         raise RuntimeError(f"device status {int(status.item())}")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
-        res["cpu_baseline"] = cpu_baseline(spec, d, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(spec, d, args.cpu_seconds, args.pooling)
     print(json.dumps(res), flush=True)
 
 
