@@ -80,7 +80,7 @@ def decode(words: np.ndarray, dtype: str) -> np.ndarray:
 
 def decode_row(table: np.ndarray, dtype: str, D: int, r: int, d: int) -> float:
     """Element (r, d) of a table with rows of D values, decoded by the oracle
-    (for "u8", rows of D codes then an fp32 scale and bias)."""
+    (for "u8", rows of D codes, an fp32 scale and bias, 8 padding bytes)."""
     t = np.ascontiguousarray(table)
     return _load().oracle_decode_row(_p(t), DTYPE_CODES[dtype], D, r, d)
 
@@ -91,8 +91,9 @@ def forward(rows: Sequence[int], dims: Sequence[int], dtype: str, tables: Sequen
 
     tables[t] is table t as a [R_t, D_t] array of raw element storage: float32
     for "f32", and 16-bit words (uint16 / float16 / any 2-byte dtype, read as
-    the raw bit pattern) for "f16" and "bf16"; for "u8" an [R_t, D_t + 8]
-    uint8 array (each row's D_t codes, then its fp32 scale and bias).
+    the raw bit pattern) for "f16" and "bf16"; for "u8" an [R_t, D_t + 16]
+    uint8 array (each row's D_t codes, its fp32 scale and bias, 8 bytes of
+    padding).
     Indices and offsets of any integer type are taken as int64 values.
     pooling is "sum" or "mean" (mean takes no weights).  Returns (out,
     absout), each [B, total_dim] float64.

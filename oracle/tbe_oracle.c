@@ -39,8 +39,8 @@
  * Variants.  Mean pooling divides each bag's sum by its number of lookups
  * (an empty bag gives 0), and its gradient passes grad_out / L to every
  * lookup of the bag.  Tables may also be stored in an 8-bit row-wise
- * quantised format (a row of D codes followed by its fp32 scale and bias; see
- * row_elem), the kind of quantised operation the paper names for early-stage
+ * quantised format (a row of D codes followed by its fp32 scale and bias and
+ * padding; see row_elem), the kind of quantised operation the paper names for early-stage
  * ranking (Introduction, "Model Diversity Across Ranking Stages").  Narrower
  * int32 indices and offsets (the int64 -> int32 downcast of hashed ids that
  * the paper lists among sparse preprocessing steps, Background,
@@ -118,15 +118,16 @@ static double table_elem(const void *table, int32_t dtype, int64_t i)
 
 /*
  * Element d of row r of a table whose rows hold D values.  For the 8-bit
- * row-wise format (ORC_U8_ROWWISE) a row is stored as D unsigned 8-bit codes
- * followed by an fp32 scale and an fp32 bias (D + 8 bytes, little-endian), and
- * element d is scale * code[d] + bias.  The product of an fp32 scale and an
- * 8-bit code is exact in binary64; adding the bias rounds once in binary64.
+ * row-wise format (ORC_U8_ROWWISE) a row is stored as D unsigned 8-bit codes,
+ * an fp32 scale, an fp32 bias and 8 bytes of padding (D + 16 bytes,
+ * little-endian), and element d is scale * code[d] + bias.  The product of an
+ * fp32 scale and an 8-bit code is exact in binary64; adding the bias rounds
+ * once in binary64.
  */
 static double row_elem(const void *table, int32_t dtype, int64_t D, int64_t r, int64_t d)
 {
     if (dtype == ORC_U8_ROWWISE) {
-        const uint8_t *row = (const uint8_t *)table + r * (D + 8);
+        const uint8_t *row = (const uint8_t *)table + r * (D + 16);
         float scale, bias;
         memcpy(&scale, row + D, sizeof scale);
         memcpy(&bias, row + D + 4, sizeof bias);

@@ -25,9 +25,10 @@ def _hand():
     D = g["dims"][0]
     rows = []
     for c, s, b in zip(g["codes"], g["scale"], g["bias"]):
-        rows.append(np.concatenate([np.array(c, np.uint8), np.array([s, b], np.float32).view(np.uint8)]))
+        rows.append(np.concatenate([np.array(c, np.uint8), np.array([s, b], np.float32).view(np.uint8),
+                                    np.zeros(8, np.uint8)]))
     g["u8_table"] = np.stack(rows)
-    assert g["u8_table"].shape == (g["rows"][0], D + 8)
+    assert g["u8_table"].shape == (g["rows"][0], D + 16)
     return g
 
 
@@ -190,7 +191,8 @@ def _u8_case(rng, exact: bool):
         else:
             scale = rng.uniform(1e-4, 1e-2, R).astype(np.float32)
             bias = rng.uniform(-0.1, 0.1, R).astype(np.float32)
-        u8.append(np.concatenate([codes, np.stack([scale, bias], 1).view(np.uint8)], 1))
+        pad = rng.integers(0, 256, (R, 8)).astype(np.uint8)  # padding bytes carry no meaning
+        u8.append(np.concatenate([codes, np.stack([scale, bias], 1).view(np.uint8), pad], 1))
         f32.append((codes.astype(np.float64) * scale[:, None].astype(np.float64)
                     + bias[:, None].astype(np.float64)))
     return case, u8, f32

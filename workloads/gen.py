@@ -28,7 +28,8 @@ synthetic stand-ins for production DLRM sparse features:
 
 Any configuration can be redrawn with dtype "u8" (8-bit row-wise tables):
 each row is D uniform 8-bit codes plus a per-row fp32 scale U(2e-4, 6e-4)
-and bias U(-0.06, -0.04), about what quantising U(-0.05, 0.05) rows gives.
+and bias U(-0.06, -0.04), about what quantising U(-0.05, 0.05) rows gives,
+then 8 zero bytes of padding.
 
 Distribution recipes (the recipe is the definition):
   * uniform fp value in [lo, hi): u = 24 random bits as fp32 (exact),
@@ -67,10 +68,10 @@ ROLE_MAPID = 8
 ROLE_QPARAM = 9
 
 # name -> (torch storage dtype, bytes per stored element); "u8" is the 8-bit
-# row-wise format: a row of D codes followed by its fp32 scale and bias.
+# row-wise format: a row of D codes, its fp32 scale and bias, 8 zero bytes.
 DTYPES = {"f32": (torch.float32, 4), "f16": (torch.float16, 2), "bf16": (torch.bfloat16, 2),
           "u8": (torch.uint8, 1)}
-U8_ROW_EXTRA = 8  # bytes of scale and bias after a u8 row's codes
+U8_ROW_EXTRA = 16  # bytes after a u8 row's codes: scale, bias, padding to 16
 U8_SCALE = (2e-4, 6e-4)    # per-row scale range: about (0.1 / 255) x [0.5, 1.5]
 U8_BIAS = (-0.06, -0.04)   # per-row bias range: about the minimum of U(-0.05, 0.05)
 
@@ -156,7 +157,7 @@ class Spec:
 
     @property
     def row_elems(self) -> np.ndarray:
-        """Stored elements per row of each table (D_t, or D_t + 8 bytes for "u8")."""
+        """Stored elements per row of each table (D_t, or D_t + 16 bytes for "u8")."""
         extra = U8_ROW_EXTRA if self.dtype == "u8" else 0
         return self.dims.astype(np.int64) + extra
 
@@ -400,9 +401,9 @@ def _normal12(key: int, n: torch.Tensor) -> torch.Tensor:
 
 
 def _u8_rows(spec: Spec, t: int, r: torch.Tensor) -> torch.Tensor:
-    """Rows r of 8-bit row-wise table t as stored bytes [len(r), D_t + 8]: D_t
-    uniform 8-bit codes, then an fp32 scale drawn from U8_SCALE and an fp32
-    bias drawn from U8_BIAS (little-endian), both per row."""
+    """Rows r of 8-bit row-wise table t as stored bytes [len(r), D_t + 16]:
+    D_t uniform 8-bit codes, an fp32 scale drawn from U8_SCALE and an fp32
+    bias drawn from U8_BIAS (little-endian), both per row, and 8 zero bytes."""
     D = int(spec.dims[t])
     r = r.view(-1, 1)
     n = r * D + torch.arange(D, dtype=torch.int64, device=r.device).view(1, -1)
@@ -411,13 +412,14 @@ def _u8_rows(spec: Spec, t: int, r: torch.Tensor) -> torch.Tensor:
     rr = r.reshape(-1)
     scale = _value_draw(("uniform",) + U8_SCALE, key, 2 * rr)
     bias = _value_draw(("uniform",) + U8_BIAS, key, 2 * rr + 1)
-    sb = torch.stack([scale, bias], 1).contiguous().view(torch.uint8)
+    pad = torch.zeros_like(scale)
+    sb = torch.stack([scale, bias, pad, pad], 1).contiguous().view(torch.uint8)
     return torch.cat([codes.view(-1, D), sb], 1)
 
 
 def gen_table(spec: Spec, t: int, device="cpu", out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Table t, [R_t, D_t] in the spec's dtype (row-major); for "u8" the
-    stored bytes [R_t, D_t + 8]."""
+    stored bytes [R_t, D_t + 16]."""
     R, D = int(spec.rows[t]), int(spec.dims[t])
     if spec.dtype == "u8":
         if out is None:
