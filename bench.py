@@ -45,14 +45,15 @@ def log(msg):
 
 
 def forward_bytes(spec, offsets_host: np.ndarray, index_bytes: int = 8, out_bytes: int = 4) -> int:
-    """Algorithmic bytes of one forward launch: each lookup reads its stored
-    row (D_t * elem_size; D_t + 8 for an 8-bit row-wise row with its scale and
-    bias) and its index (+ a 4-byte weight when weighted); each bag reads one
-    offset and writes D_t outputs."""
+    """Algorithmic bytes of one forward launch: each lookup reads its row
+    (D_t * elem_size; for an 8-bit row-wise row its D_t codes and 8 bytes of
+    scale and bias, not the padding) and its index (+ a 4-byte weight when
+    weighted); each bag reads one offset and writes D_t outputs."""
     B = spec.B
     per_table_lookups = offsets_host[np.arange(1, spec.T + 1) * B] - offsets_host[np.arange(spec.T) * B]
     dims = spec.dims.astype(np.int64)
-    rows = int((per_table_lookups * spec.row_elems).sum()) * spec.elem_size
+    read = dims + 8 if spec.dtype == "u8" else dims
+    rows = int((per_table_lookups * read).sum()) * spec.elem_size
     n = int(offsets_host[-1])
     idx = index_bytes * n + (4 * n if spec.weighted else 0)
     bags = index_bytes * (spec.T * B + 1) + out_bytes * B * int(dims.sum())

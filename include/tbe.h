@@ -56,8 +56,9 @@ extern "C" {
  * BF16.  TBE_U8_ROWWISE is an 8-bit row-wise quantised table (the paper names
  * quantised operations among early-stage ranking's kernels: Introduction,
  * "Model Diversity Across Ranking Stages"): a row of D_t values is stored as
- * D_t unsigned 8-bit codes followed by an fp32 scale and an fp32 bias, D_t + 8
- * bytes, and value d is scale * code[d] + bias (one fp32 fma).
+ * D_t unsigned 8-bit codes, an fp32 scale, an fp32 bias and 8 bytes of
+ * padding, D_t + 16 bytes (so rows stay 16-byte aligned), and value d is
+ * scale * code[d] + bias (one fp32 fma).
  */
 enum tbe_dtype { TBE_F32 = 0, TBE_F16 = 1, TBE_BF16 = 2, TBE_U8_ROWWISE = 3 };
 
@@ -103,13 +104,12 @@ typedef struct tbe_desc {
     int64_t batch_size;           /* B >= 0                                       */
     const int64_t *rows;          /* host [T]: R_t >= 1                           */
     const int32_t *dims;          /* host [T]: D_t >= 1, D_t*elem_size % 16 == 0
-                                     (TBE_U8_ROWWISE: D_t % 8 == 0)               */
+                                     (elem_size 1 for TBE_U8_ROWWISE)             */
     const int64_t *table_offsets; /* host [T]: element offset of table t in the
                                      flat tables buffer (row-major R_t x D_t,
                                      16-byte aligned; TBE_U8_ROWWISE: byte
-                                     offset of R_t rows of D_t + 8 bytes, 8-byte
-                                     aligned); NULL = tables packed in order
-                                     with no gaps                                */
+                                     offset of R_t rows of D_t + 16 bytes);
+                                     NULL = tables packed in order, no gaps      */
     int64_t table_elems;          /* elements (TBE_U8_ROWWISE: bytes) in the flat
                                      tables buffer; every table must lie inside  */
     int32_t bounds_check;         /* 1 = check indices and offsets on the GPU,

@@ -15,9 +15,10 @@
 // Variants: indices and offsets are int64 or int32 (a template parameter);
 // mean pooling multiplies a finished bag by fl32(1/L) as it is written; the
 // output is stored as fp32, or rounded to nearest even to fp16 / bf16; 8-bit
-// row-wise tables are read as 8-byte vectors of codes (a lane group of D/8
-// lanes per row), and every lane also loads its row's fp32 scale and bias
-// (the 8 bytes after the codes) into the same ring slot.
+// row-wise tables are read as 16-byte vectors of codes (a lane group of D/16
+// lanes per row; rows of D + 16 bytes keep every vector aligned), and every
+// lane also loads its row's fp32 scale and bias (the 8 bytes after the codes)
+// into the same ring slot.
 //
 // The work is bound by memory latency and bandwidth (HBM and the L2 /
 // Infinity Cache that serve hot rows): about one fma per element read, far
@@ -31,6 +32,7 @@ namespace {
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = 64 * kWavesPerBlock;
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
@@ -43,7 +45,7 @@ template <>
 struct Elem<TBE_F32> {
     static constexpr int kPerVec = 4;
     using Vec = uint4;
-    __device__ static inline void fma(float *acc, const uint4 v, float w, float2) {
+    __device__ static inline void fma(float *acc, const uint4 v, float w, f2) {
         acc[0] = __builtin_fmaf(w, __uint_as_float(v.x), acc[0]);
         acc[1] = __builtin_fmaf(w, __uint_as_float(v.y), acc[1]);
         acc[2] = __builtin_fmaf(w, __uint_as_float(v.z), acc[2]);
@@ -62,7 +64,7 @@ template <>
 struct Elem<TBE_F16> {
     static constexpr int kPerVec = 8;
     using Vec = uint4;
-    __device__ static inline void fma(float *acc, const uint4 v, float w, float2) {
+    __device__ static inline void fma(float *acc, const uint4 v, float w, f2) {
         const uint32_t q[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -77,7 +79,7 @@ template <>
 struct Elem<TBE_BF16> {
     static constexpr int kPerVec = 8;
     using Vec = uint4;
-    __device__ static inline void fma(float *acc, const uint4 v, float w, float2) {
+    __device__ static inline void fma(float *acc, const uint4 v, float w, f2) {
         const uint32_t q[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -90,12 +92,12 @@ struct Elem<TBE_BF16> {
 // 8-bit row-wise: value = scale * code + bias (one fma), then acc += w * value.
 template <>
 struct Elem<TBE_U8_ROWWISE> {
-    static constexpr int kPerVec = 8;
-    using Vec = uint2;
-    __device__ static inline void fma(float *acc, const uint2 v, float w, float2 sb) {
-        const uint32_t q[2] = {v.x, v.y};
+    static constexpr int kPerVec = 16;
+    using Vec = uint4;
+    __device__ static inline void fma(float *acc, const uint4 v, float w, f2 sb) {
+        const uint32_t q[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < 4; ++i) {
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
                 const float code = static_cast<float>((q[i] >> (8 * b)) & 0xffu);
@@ -160,7 +162,8 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
     constexpr bool kQuant = DT == TBE_U8_ROWWISE;
     constexpr int VB = sizeof(VT);  // bytes per load vector
     constexpr int U = LPR < 8 ? LPR : 8;  // row loads in flight per lane group
-    constexpr int NB = kBagsPerGroup;
+    constexpr int NB = kQuant ? kBagsPerGroup / 2 : kBagsPerGroup;  // bags_per_group(DT)
+    static_assert(NB == 4 || NB == 2, "end_of below");
     constexpr uint32_t kSkip = 0xffffffffu;
     const int g = lane / LPR, v = lane % LPR;
     const int nbs = nbags_unit - g * NB < 0 ? 0 : (nbags_unit - g * NB > NB ? NB : nbags_unit - g * NB);
@@ -199,6 +202,7 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
         const int32_t o = __shfl_xor(span, mask);
         span = o > span ? o : span;
     }
+    static_assert(64 * NB * E::kPerVec <= 64 * kBagsPerGroup * 8, "finished bags fit the wave's LDS stage");
     float *my_stage = stage + (static_cast<int>(g) * NB * LPR + v) * E::kPerVec;  // + bag * LPR * kPerVec
 
     for (int c0 = 0; c0 < m.nvec; c0 += LPR) {  // one pass unless rows exceed 1 KiB
@@ -238,8 +242,8 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
 
         VT ring[U];
         float ring_w[WEIGHTED ? U : 1];
-        float2 ring_sb[kQuant ? U : 1];
-        auto issue = [&](int src_lane, bool from_next, VT &dst, float &dw, float2 &dsb) {
+        f2 ring_sb[kQuant ? U : 1];
+        auto issue = [&](int src_lane, bool from_next, VT &dst, float &dw, f2 &dsb) {
             const int src = g * LPR + src_lane;
             const uint32_t r = from_next ? __shfl(nxt_r, src) : __shfl(cur_r, src);
             const bool ok = r != kSkip && vact;
@@ -248,7 +252,7 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
             if constexpr (kQuant) {
                 // the row's scale and bias follow its D codes
                 const char *sba = ok ? table + static_cast<uint64_t>(r) * row_bytes + m.dim : zerop;
-                dsb = *reinterpret_cast<const float2 *>(sba);
+                dsb = *reinterpret_cast<const f2 *>(sba);
             }
             if constexpr (WEIGHTED) {
                 const float w = from_next ? __shfl(nxt_w, src) : __shfl(cur_w, src);
@@ -263,8 +267,9 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
 #pragma unroll
         for (int i = 0; i < E::kPerVec; ++i) acc[i] = 0.0f;
         int bag = 0;
-        auto end_of = [&](int i) {
-            return i == 0 ? bnd[1] : i == 1 ? bnd[2] : i == 2 ? bnd[3] : bnd[4];
+        auto end_of = [&](int i) {  // bnd[i + 1], by selects (no indexed register array)
+            if constexpr (NB == 4) return i == 0 ? bnd[1] : i == 1 ? bnd[2] : i == 2 ? bnd[3] : bnd[4];
+            else return i == 0 ? bnd[1] : bnd[2];
         };
         int32_t bag_end = bnd[1];
         while (bag + 1 < nbs && bag_end == 0) bag_end = end_of(++bag);
@@ -276,7 +281,7 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
                 for (int sl = 0; sl < U; ++sl) {
                     const int32_t rp = base + s0 + sl;
                     E::fma(acc, ring[sl], WEIGHTED ? ring_w[WEIGHTED ? sl : 0] : 1.0f,
-                           kQuant ? ring_sb[kQuant ? sl : 0] : float2{0.f, 0.f});
+                           kQuant ? ring_sb[kQuant ? sl : 0] : f2{0.f, 0.f});
                     if (rp < Q && rp + 1 == bag_end) {
                         float *st = my_stage + bag * LPR * E::kPerVec;
 #pragma unroll

@@ -42,11 +42,11 @@ int32_t validate_desc(const tbe_desc *d) {
         const int64_t R = d->rows[t];
         const int32_t D = d->dims[t];
         if (R < 1 || D < 1) return TBE_ERR_SHAPE;
-        if (u8 ? D % 8 != 0 : (static_cast<int64_t>(D) * es) % 16 != 0) return TBE_ERR_ALIGN;
+        if ((static_cast<int64_t>(D) * es) % 16 != 0) return TBE_ERR_ALIGN;
         if (R > (int64_t(1) << 40) || D > (1 << 20)) return TBE_ERR_SHAPE;
-        const int64_t row_elems = u8 ? D + 8 : D;
+        const int64_t row_elems = u8 ? D + 16 : D;
         const int64_t off = d->table_offsets ? d->table_offsets[t] : packed;
-        if (off < 0 || (u8 ? off % 8 != 0 : (off * es) % 16 != 0)) return TBE_ERR_ALIGN;
+        if (off < 0 || (off * es) % 16 != 0) return TBE_ERR_ALIGN;
         if (off > d->table_elems || R * row_elems > d->table_elems - off) return TBE_ERR_SHAPE;
         packed += R * row_elems;
         total_dim += D;
@@ -114,19 +114,19 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
         m.dim = D;
         m.dim_off = static_cast<int32_t>(dim_off);
         const bool u8 = p.dtype == TBE_U8_ROWWISE;
-        m.nvec = u8 ? D / 8 : static_cast<int32_t>(static_cast<int64_t>(D) * es / 16);
-        m.row_bytes = u8 ? D + 8 : D * es;
+        m.nvec = static_cast<int32_t>(static_cast<int64_t>(D) * es / 16);
+        m.row_bytes = u8 ? D + 16 : D * es;
         int l = 0;
         while ((1 << l) < m.nvec && l < 6) ++l;
         m.lpr_log2 = l;
         l = 0;
         while ((1 << l) < D / 4 && l < 6) ++l;
         m.glpr_log2 = l;
-        m.unit_bags = tbe::kBagsPerGroup * (64 >> m.lpr_log2);
+        m.unit_bags = tbe::bags_per_group(p.dtype) * (64 >> m.lpr_log2);
         m.unit_base = p.fwd_units;
         p.fwd_units += (p.B + m.unit_bags - 1) / m.unit_bags;
         m.pad = 0;
-        packed += R * (u8 ? D + 8 : D);
+        packed += R * (u8 ? D + 16 : D);
         dim_off += D;
         row_base += R;
         if (D > p.max_dim) p.max_dim = D;

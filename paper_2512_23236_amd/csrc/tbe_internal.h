@@ -16,8 +16,8 @@ struct TableMeta {
     int64_t row_base;     // first global row id: sum of R_t' for t' < t
     int32_t dim;          // D_t
     int32_t dim_off;      // first output column: sum of D_t' for t' < t
-    int32_t nvec;         // load vectors per table row: D_t * elem_size / 16 (8-bit
-                          // row-wise tables: D_t / 8 vectors of 8 code bytes)
+    int32_t nvec;         // 16-byte load vectors per table row: D_t * elem_size / 16
+                          // (8-bit row-wise: the D_t codes, without scale and bias)
     int32_t lpr_log2;     // log2 of lanes per row: smallest power of two >= min(nvec, 64)
     int32_t glpr_log2;    // the same for an fp32 row of D_t (gradient rows): min(D_t / 4, 64)
     int32_t unit_bags;    // forward: bags per wave work unit (bags per lane group x groups per wave)
@@ -90,8 +90,11 @@ __device__ inline int64_t xcd_remap(int64_t w, int64_t nwg, int num_xcd) {
 constexpr int kNumXcd = 8;
 
 // Forward work decomposition: each lane group of a wave streams through
-// kBagsPerGroup consecutive bags of one table.
+// kBagsPerGroup consecutive bags of one table (half as many for 8-bit row-wise
+// tables, whose lanes hold twice the columns, so finished bags take the same
+// LDS).
 constexpr int kBagsPerGroup = 4;
+inline int bags_per_group(int dtype) { return dtype == TBE_U8_ROWWISE ? kBagsPerGroup / 2 : kBagsPerGroup; }
 
 // Zeros that a lane with no row to read loads instead (one wave's 16 bytes per
 // lane), so every row load in the forward stream is issued unconditionally.

@@ -20,7 +20,7 @@ ABI_VERSION = 2
 
 F32, F16, BF16, U8_ROWWISE = 0, 1, 2, 3
 # table storage type -> tbe_dtype; torch.uint8 tables are 8-bit row-wise (rows of
-# D codes followed by an fp32 scale and bias)
+# D codes, an fp32 scale and bias, 8 padding bytes)
 DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16, torch.uint8: U8_ROWWISE}
 OUT_DTYPE_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 POOLING_CODE = {"sum": 0, "mean": 1}
@@ -135,7 +135,7 @@ class Plan:
         self.bounds_check = bool(bounds_check)
         self.table_offsets = None if table_offsets is None else np.ascontiguousarray(table_offsets, dtype=np.int64)
         if table_elems is None:
-            extra = 8 if dtype == torch.uint8 else 0
+            extra = 16 if dtype == torch.uint8 else 0
             table_elems = int((self.rows * (self.dims.astype(np.int64) + extra)).sum())
         self.table_elems = int(table_elems)
         if dtype not in DTYPE_CODE or out_dtype not in OUT_DTYPE_CODE or index_dtype not in INDEX_TYPE_CODE:

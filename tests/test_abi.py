@@ -39,7 +39,7 @@ def _desc(rows=(100, 50), dims=(64, 128), dtype=tbe.F16, B=4, offs=None, elems=N
     d = np.ascontiguousarray(dims, np.int32)
     o = None if offs is None else np.ascontiguousarray(offs, np.int64)
     if elems is None:
-        extra = 8 if dtype == tbe.U8_ROWWISE else 0
+        extra = 16 if dtype == tbe.U8_ROWWISE else 0
         elems = int((r * (d.astype(np.int64) + extra)).sum())
     desc = tbe._Desc(len(r) if T is None else T, dtype, B, r.ctypes.data, d.ctypes.data,
                      None if o is None else o.ctypes.data, elems, check, pooling, index_type, out_dtype)
@@ -69,9 +69,9 @@ def _create(desc):
     (dict(index_type=2), -3),                   # unknown index type
     (dict(out_dtype=3), -3),                    # 8-bit row-wise is a table format only
     (dict(out_dtype=-1), -3),
-    (dict(dtype=tbe.U8_ROWWISE, dims=(64, 12)), -4),          # 8-bit rows need D % 8 == 0
-    (dict(dtype=tbe.U8_ROWWISE, offs=(0, 7204)), -4),         # 8-bit table offsets are 8-byte aligned
-    (dict(dtype=tbe.U8_ROWWISE, offs=(0, 7200), elems=7200 + 50 * 136 - 1), -2),  # last row past the end
+    (dict(dtype=tbe.U8_ROWWISE, dims=(64, 24)), -4),          # 8-bit rows need D % 16 == 0
+    (dict(dtype=tbe.U8_ROWWISE, offs=(0, 8008)), -4),         # 8-bit table offsets are 16-byte aligned
+    (dict(dtype=tbe.U8_ROWWISE, offs=(0, 8000), elems=8000 + 50 * 144 - 1), -2),  # last row past the end
 ])
 def test_plan_create_rejects_bad_descriptors(kwargs, code):
     rc, h = _create(_desc(**kwargs))

@@ -97,8 +97,9 @@ def test_reduced_precision_output(dtype, out_dt):
 
 @pytest.mark.parametrize("weighted", [False, True])
 def test_u8_rowwise_dims(weighted):
-    """8-bit rows from one 8-byte vector to more than one wave of vectors."""
-    dims = [8, 24, 64, 128, 96, 256, 520, 1024]
+    """8-bit rows from one 16-byte vector of codes to more than one wave of
+    vectors (1040 codes: 65 vectors); rows of D + 8 bytes start 8-byte aligned."""
+    dims = [16, 48, 64, 128, 96, 256, 528, 1040]
     spec = small(T=len(dims), B=41, dtype="u8", dims=np.array(dims, np.int32), weighted=weighted,
                  name=f"u8-dims-{'w' if weighted else 'u'}")
     d = inputs(spec)
