@@ -231,6 +231,8 @@ typedef struct tbe_optimizer {
  *                       (row-wise Adagrad's per-row sum, updated in place);
  *                       may be NULL for SGD
  *   grad_idx, grad_row_offsets, grad_rows   device, as tbe_backward writes them
+ *                       (grad_rows 16-byte aligned); ids outside the plan's
+ *                       rows are skipped
  *   num_unique          device int64 scalar U, as tbe_backward writes it
  *   max_unique          host upper bound on U (at most this many rows are
  *                       updated), e.g. the backward's num_indices

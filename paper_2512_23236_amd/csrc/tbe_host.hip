@@ -205,7 +205,7 @@ int32_t tbe_apply_gradient(const tbe_plan *plan, void *tables, const tbe_optimiz
     if (opt->kind == TBE_OPT_ROWWISE_ADAGRAD && !state) return TBE_ERR_NULL;
     if (!aligned16(tables) || (reinterpret_cast<uintptr_t>(grad_idx) & 7u) ||
         (reinterpret_cast<uintptr_t>(grad_row_offsets) & 7u) || (reinterpret_cast<uintptr_t>(num_unique) & 7u) ||
-        (reinterpret_cast<uintptr_t>(grad_rows) & 3u) || (reinterpret_cast<uintptr_t>(state) & 3u))
+        !aligned16(grad_rows) || (reinterpret_cast<uintptr_t>(state) & 3u))
         return TBE_ERR_ALIGN;
     const hipError_t e = tbe::launch_apply_gradient(*p, tables, opt->kind, opt->learning_rate, opt->eps, state,
                                                     grad_idx, grad_row_offsets, grad_rows, num_unique, max_unique,

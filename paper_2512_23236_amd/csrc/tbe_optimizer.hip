@@ -5,12 +5,17 @@
 //   SGD:               W[r] <- W[r] - lr * g
 //   row-wise Adagrad:  s[r] <- s[r] + mean_d g_d^2;  W[r] <- W[r] - lr * g / (sqrt(s[r]) + eps)
 //
-// One wave per listed row (a fixed grid of waves strides over the rows, so
-// the launch does not depend on the row count the backward found): every
-// row, and its state, has exactly one writer, so the step is race-free and
-// bitwise reproducible.  Arithmetic is fp32: the mean of squares is a
-// per-lane sum in column order followed by a fixed xor tree, and each new
-// element is one fma rounded to the table format (round to nearest even).
+// Each wave takes a contiguous run of the listed rows, 64 at a time: one
+// coalesced load brings 64 row ids and gradient offsets, a wave ballot finds
+// how many consecutive ones belong to the current table, and lane groups of
+// LPR = D_t / 4 lanes (at most 64) update G = 64 / LPR rows at once, two rows
+// per group in flight, each lane moving 4 columns (a 16-byte gradient vector
+// and 4 table elements).  Every row, and its state, has exactly one writer, so
+// the step is race-free and bitwise reproducible.  Arithmetic is fp32: the
+// mean of squares is a per-lane chain over its 4 columns then a fixed xor tree
+// across the group, and each new element is one fma rounded to the table
+// format (round to nearest even).  Row ids outside the plan's rows are
+// skipped.
 
 #include "tbe_internal.h"
 
@@ -18,36 +23,57 @@ namespace tbe {
 namespace {
 
 constexpr int kOptWaves = 4;
-constexpr unsigned kOptGroups = 4096;  // 16384 waves stride over the rows
+constexpr unsigned kOptGroups = 4096;  // 16384 waves share the rows
+constexpr int kInFlight = 2;           // rows per lane group in flight
 
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+
+// Four consecutive table elements as fp32, and back (round to nearest even).
 template <int DT>
-struct Cell;
+struct Quad;
 
 template <>
-struct Cell<TBE_F32> {
-    __device__ static inline float load(const char *p) { return *reinterpret_cast<const float *>(p); }
-    __device__ static inline void store(char *p, float v) { *reinterpret_cast<float *>(p) = v; }
+struct Quad<TBE_F32> {
+    __device__ static inline f4 load(const char *p) { return *reinterpret_cast<const f4 *>(p); }
+    __device__ static inline void store(char *p, f4 v) { *reinterpret_cast<f4 *>(p) = v; }
 };
 
 template <>
-struct Cell<TBE_F16> {
-    __device__ static inline float load(const char *p) {
-        return static_cast<float>(*reinterpret_cast<const _Float16 *>(p));
+struct Quad<TBE_F16> {
+    __device__ static inline float lo(uint32_t x) {
+        return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(x & 0xffffu)));
     }
-    // the conversion rounds to nearest even
-    __device__ static inline void store(char *p, float v) { *reinterpret_cast<_Float16 *>(p) = static_cast<_Float16>(v); }
+    __device__ static inline float hi(uint32_t x) {
+        return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(x >> 16)));
+    }
+    __device__ static inline uint32_t bits(float x) {
+        return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(x)));  // nearest even
+    }
+    __device__ static inline f4 load(const char *p) {
+        const u2 w = *reinterpret_cast<const u2 *>(p);
+        return f4{lo(w.x), hi(w.x), lo(w.y), hi(w.y)};
+    }
+    __device__ static inline void store(char *p, f4 v) {
+        *reinterpret_cast<u2 *>(p) = u2{bits(v.x) | (bits(v.y) << 16), bits(v.z) | (bits(v.w) << 16)};
+    }
 };
 
 template <>
-struct Cell<TBE_BF16> {
-    __device__ static inline float load(const char *p) {
-        return __uint_as_float(static_cast<uint32_t>(*reinterpret_cast<const uint16_t *>(p)) << 16);
-    }
+struct Quad<TBE_BF16> {
     // keep the upper half of the fp32 word, rounded to nearest even (NaN stays NaN)
-    __device__ static inline void store(char *p, float v) {
-        const uint32_t u = __float_as_uint(v);
+    __device__ static inline uint32_t bits(float x) {
+        const uint32_t u = __float_as_uint(x);
         const uint32_t r = (u & 0x7fffffffu) > 0x7f800000u ? (u | 0x00400000u) : u + 0x7fffu + ((u >> 16) & 1u);
-        *reinterpret_cast<uint16_t *>(p) = static_cast<uint16_t>(r >> 16);
+        return r >> 16;
+    }
+    __device__ static inline f4 load(const char *p) {
+        const u2 w = *reinterpret_cast<const u2 *>(p);
+        return f4{__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u), __uint_as_float(w.y << 16),
+                  __uint_as_float(w.y & 0xffff0000u)};
+    }
+    __device__ static inline void store(char *p, f4 v) {
+        *reinterpret_cast<u2 *>(p) = u2{bits(v.x) | (bits(v.y) << 16), bits(v.z) | (bits(v.w) << 16)};
     }
 };
 
@@ -60,37 +86,128 @@ __device__ inline int table_of_row(const TableMeta *__restrict__ meta, int T, in
     return lo;
 }
 
+__device__ inline int64_t lane_i64(int64_t x, int src) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), src);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(static_cast<uint64_t>(x) >> 32), src);
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Sum over the lane group (lanes sharing lane >> log2(LPR)), fixed xor order.
+__device__ inline float group_sum(float x, int lpr) {
+    for (int off = lpr >> 1; off > 0; off >>= 1) x += __shfl_xor(x, off);
+    return x;
+}
+
+__device__ inline float sumsq4(f4 g) {
+    float s = g.x * g.x;
+    s = __builtin_fmaf(g.y, g.y, s);
+    s = __builtin_fmaf(g.z, g.z, s);
+    return __builtin_fmaf(g.w, g.w, s);
+}
+
+__device__ inline f4 update4(f4 w, f4 g, float step) {
+    return f4{__builtin_fmaf(-step, g.x, w.x), __builtin_fmaf(-step, g.y, w.y), __builtin_fmaf(-step, g.z, w.z),
+              __builtin_fmaf(-step, g.w, w.w)};
+}
+
 template <int DT, bool kAdagrad>
 __global__ __launch_bounds__(64 * kOptWaves) void apply_kernel(
-    const TableMeta *__restrict__ meta, int T, char *__restrict__ tables, float *__restrict__ state,
-    const int64_t *__restrict__ grad_idx, const int64_t *__restrict__ grad_row_offsets,
+    const TableMeta *__restrict__ meta, int T, int64_t total_rows, char *__restrict__ tables,
+    float *__restrict__ state, const int64_t *__restrict__ grad_idx, const int64_t *__restrict__ grad_row_offsets,
     const float *__restrict__ grad_rows, const int64_t *__restrict__ num_unique, int64_t max_unique, float lr,
     float eps) {
+    using Q = Quad<DT>;
     constexpr int ES = DT == TBE_F32 ? 4 : 2;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t U = *num_unique < max_unique ? *num_unique : max_unique;
-    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kOptWaves;
-    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kOptWaves + wave; u < U; u += nwaves) {
-        const int64_t g = grad_idx[u];
-        const int t = table_of_row(meta, T, g);
-        const TableMeta m = meta[t];
-        const int64_t r = g - m.row_base;
-        const int D = m.dim;
-        const float *gr = grad_rows + grad_row_offsets[u];
-        char *row = tables + (m.elem_offset + r * D) * ES;
-        float step = lr;
-        if constexpr (kAdagrad) {
-            float sq = 0.f;
-            for (int c = lane; c < D; c += 64) sq = __builtin_fmaf(gr[c], gr[c], sq);
-            for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
-            const float s = state[g] + sq / static_cast<float>(D);
-            if (lane == 0) state[g] = s;
-            step = lr / (sqrtf(s) + eps);
-        }
-        for (int c = lane; c < D; c += 64) {
-            const float w = Cell<DT>::load(row + c * ES);
-            Cell<DT>::store(row + c * ES, __builtin_fmaf(-step, gr[c], w));
+    const int64_t nw = static_cast<int64_t>(gridDim.x) * kOptWaves;
+    const int64_t w = static_cast<int64_t>(blockIdx.x) * kOptWaves + wave;
+    const int64_t batches = (U + 63) / 64;
+    const int64_t per = (batches + nw - 1) / nw;
+    const int64_t b_end = (w + 1) * per < batches ? (w + 1) * per : batches;
+    int t = 0;
+    int64_t t_lo = 1, t_hi = 0;  // global row ids [t_lo, t_hi) belong to table t (empty: none cached)
+    for (int64_t bb = w * per; bb < b_end; ++bb) {
+        const int64_t base = bb * 64;
+        const int n = U - base < 64 ? static_cast<int>(U - base) : 64;
+        const int64_t my_g = lane < n ? grad_idx[base + lane] : -1;
+        const int64_t my_o = lane < n ? grad_row_offsets[base + lane] : 0;
+        int i = 0;
+        while (i < n) {
+            const int64_t g0 = lane_i64(my_g, i);
+            if (g0 < 0 || g0 >= total_rows) {  // not a row of the plan: skipped
+                ++i;
+                continue;
+            }
+            if (g0 < t_lo || g0 >= t_hi) {
+                t = table_of_row(meta, T, g0);
+                t_lo = meta[t].row_base;
+                t_hi = t_lo + meta[t].rows;
+            }
+            // rows i .. e-1 of the batch lie in table t
+            const uint64_t out = __ballot(lane >= i && (lane >= n || my_g < t_lo || my_g >= t_hi));
+            const int e = out ? static_cast<int>(__builtin_ctzll(out)) : 64;
+            const TableMeta m = meta[t];
+            const int lpr_log2 = m.glpr_log2;
+            const int LPR = 1 << lpr_log2, G = 64 >> lpr_log2;
+            const int grp = lane >> lpr_log2, v = lane & (LPR - 1);
+            const int nq = m.dim >> 2;  // 4-column quads per row
+            const float fd = static_cast<float>(m.dim);
+            char *tab = tables + m.elem_offset * ES;
+            if (nq <= LPR) {
+                // one quad per lane: kInFlight rows per lane group at once
+                for (int s = i; s < e; s += kInFlight * G) {
+                    int64_t g[kInFlight], o[kInFlight];
+                    bool has[kInFlight], act[kInFlight];
+                    f4 gr[kInFlight], wv[kInFlight];
+                    char *p[kInFlight];
+#pragma unroll
+                    for (int k = 0; k < kInFlight; ++k) {
+                        const int r = s + k * G + grp;
+                        has[k] = r < e;
+                        act[k] = has[k] && v < nq;
+                        g[k] = __shfl(my_g, r & 63);
+                        o[k] = __shfl(my_o, r & 63);
+                        p[k] = tab + ((g[k] - t_lo) * m.dim + v * 4) * ES;
+                        const f4 z = f4{0.f, 0.f, 0.f, 0.f};
+                        gr[k] = act[k] ? *reinterpret_cast<const f4 *>(grad_rows + o[k] + v * 4) : z;
+                        wv[k] = act[k] ? Q::load(p[k]) : z;
+                    }
+#pragma unroll
+                    for (int k = 0; k < kInFlight; ++k) {
+                        float step = lr;
+                        if constexpr (kAdagrad) {
+                            const float sq = group_sum(sumsq4(gr[k]), LPR);
+                            const float sk = (has[k] ? state[g[k]] : 0.f) + sq / fd;
+                            if (has[k] && v == 0) state[g[k]] = sk;
+                            step = lr / (sqrtf(sk) + eps);
+                        }
+                        if (act[k]) Q::store(p[k], update4(wv[k], gr[k], step));
+                    }
+                }
+            } else {
+                // wide rows (more quads than 64 lanes): one row at a time, in passes
+                for (int r = i; r < e; ++r) {
+                    const int64_t g = lane_i64(my_g, r), o = lane_i64(my_o, r);
+                    char *row = tab + (g - t_lo) * m.dim * ES;
+                    float step = lr;
+                    if constexpr (kAdagrad) {
+                        float sq = 0.f;
+                        for (int q = v; q < nq; q += 64)
+                            sq += sumsq4(*reinterpret_cast<const f4 *>(grad_rows + o + q * 4));
+                        sq = group_sum(sq, 64);
+                        const float sr = state[g] + sq / fd;
+                        if (v == 0) state[g] = sr;
+                        step = lr / (sqrtf(sr) + eps);
+                    }
+                    for (int q = v; q < nq; q += 64) {
+                        const f4 gq = *reinterpret_cast<const f4 *>(grad_rows + o + q * 4);
+                        Q::store(row + q * 4 * ES, update4(Q::load(row + q * 4 * ES), gq, step));
+                    }
+                }
+            }
+            i = e;
         }
     }
 }
@@ -101,12 +218,12 @@ hipError_t launch_apply_gradient(const Plan &p, void *tables, int32_t kind, floa
                                  const int64_t *grad_idx, const int64_t *grad_row_offsets, const float *grad_rows,
                                  const int64_t *num_unique, int64_t max_unique, hipStream_t stream) {
     if (max_unique == 0) return hipSuccess;
-    const int64_t want = (max_unique + kOptWaves - 1) / kOptWaves;
+    const int64_t want = (max_unique + 64 * kOptWaves - 1) / (64 * kOptWaves);  // a 64-row batch per wave
     const dim3 grid(static_cast<unsigned>(want < kOptGroups ? want : kOptGroups)), block(64 * kOptWaves);
     char *tb = static_cast<char *>(tables);
 #define TBE_LAUNCH(DT, A)                                                                                     \
-    hipLaunchKernelGGL((apply_kernel<DT, A>), grid, block, 0, stream, p.meta_dev, p.T, tb, state, grad_idx,   \
-                       grad_row_offsets, grad_rows, num_unique, max_unique, lr, eps)
+    hipLaunchKernelGGL((apply_kernel<DT, A>), grid, block, 0, stream, p.meta_dev, p.T, p.total_rows, tb, state,  \
+                       grad_idx, grad_row_offsets, grad_rows, num_unique, max_unique, lr, eps)
     const bool ada = kind == TBE_OPT_ROWWISE_ADAGRAD;
     switch (p.dtype) {
         case TBE_F32: if (ada) TBE_LAUNCH(TBE_F32, true); else TBE_LAUNCH(TBE_F32, false); break;

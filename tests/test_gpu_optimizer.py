@@ -136,3 +136,29 @@ def test_after_backward():
         changed[rb[t]:rb[t + 1]] = np.any(after[t] != before[t], axis=1)
     assert int(status.item()) == 0
     assert not changed[np.setdiff1d(np.arange(rb[-1]), gidx)].any()  # only listed rows move
+
+
+def test_ids_outside_the_plan_are_skipped():
+    """Ids past the plan's rows change nothing; the valid ids around them are
+    updated as usual."""
+    spec = workloads.small_config(4, seed=26, T=3, B=4)
+    d = workloads.gen_all(spec, device())
+    plan = plan_for(spec)
+    rng = np.random.default_rng(6)
+    gidx, gro, rows = sparse_grad(rng, spec, 150)
+    total = int(spec.rows.sum())
+    bad = gidx.copy()
+    bad[-3:] = total + np.arange(3)  # still ascending
+    g = tbe.SparseGrad(torch.as_tensor(rows, device=device()), torch.as_tensor(bad, device=device()),
+                       torch.zeros(151, dtype=torch.int64, device=device()), torch.as_tensor(gro, device=device()),
+                       torch.tensor([150], dtype=torch.int64, device=device()))
+    ref_g = tbe.SparseGrad(torch.as_tensor(rows, device=device()), torch.as_tensor(gidx[:-3], device=device()),
+                           torch.zeros(148, dtype=torch.int64, device=device()),
+                           torch.as_tensor(gro[:-3], device=device()),
+                           torch.tensor([147], dtype=torch.int64, device=device()))
+    a, b = d["tables"].clone(), d["tables"].clone()
+    tbe.apply_gradient(plan, a, g, tbe.SGD, 0.1)
+    tbe.apply_gradient(plan, b, ref_g, tbe.SGD, 0.1)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    assert not torch.equal(a, d["tables"])
