@@ -310,7 +310,18 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__
 #pragma unroll
     for (int r = 0; r < kItems; ++r) {
         const int64_t pos = wbase + r * 64 + lane;
-        if (pos < ti.p_hi) atomicAdd(&cnt[wave][digit_of(k[r], shift, mask)], 1u);
+        const bool valid = pos < ti.p_hi;
+        const uint32_t d = digit_of(k[r], shift, mask);
+        // a round whose keys all share one digit (common in the high passes,
+        // where small tables' keys are all 0) adds once instead of 64 times
+        // to one LDS word
+        const uint32_t d0 = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(d)));
+        const uint64_t vm = __ballot(valid);
+        if (__ballot(valid && d == d0) == vm) {
+            if (lane == 0 && vm) atomicAdd(&cnt[wave][d0], static_cast<uint32_t>(__popcll(vm)));
+        } else if (valid) {
+            atomicAdd(&cnt[wave][d], 1u);
+        }
     }
     __syncthreads();
     uint32_t c = 0;
@@ -420,7 +431,12 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
         const int64_t pos = wbase + r * 64 + lane;
         const bool valid = pos < ti.p_hi;
         const uint32_t d = digit_of(key[r], shift, mask);
-        const uint64_t peers = match_digit(d, valid, nbits);
+        // one digit for the whole round: every valid lane is a peer
+        const uint32_t d0 = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(d)));
+        const uint64_t vm = __ballot(valid);
+        uint64_t peers;
+        if (__ballot(valid && d == d0) == vm) peers = valid ? vm : 0ull;
+        else peers = match_digit(d, valid, nbits);
         const uint32_t before = static_cast<uint32_t>(__popcll(peers & lanemask_lt()));
         uint32_t base = 0;
         if (valid) base = cnt[wave][d];
