@@ -18,8 +18,8 @@
 //             minor, so scanned counts are final positions), and a stable
 //             scatter that ranks keys with wave ballots and stages the tile
 //             in LDS so global writes run in digit order.
-//   segments  per tile: segment starts (key change) and kept lookups; one
-//             scan over tiles; then grad_idx / seg_offsets /
+//   segments  per tile: segment starts (key change) per block and tile and
+//             kept lookups; one scan over tiles; then grad_idx / seg_offsets /
 //             grad_row_offsets are written for every segment start.
 //   reduce    sorted positions are cut into fixed blocks of kBlk; a wave
 //             walks one block in order, accumulating fp32 rows of
@@ -527,7 +527,8 @@ __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t *__r
                                                              const TableMeta *__restrict__ meta,
                                                              const Range *__restrict__ ranges, int T,
                                                              const Ctl *__restrict__ ctl,
-                                                             TileSeg *__restrict__ tseg) {
+                                                             TileSeg *__restrict__ tseg,
+                                                             uint32_t *__restrict__ blk_starts) {
     __shared__ uint32_t wsum[2][kWaves];
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->abort) return;
@@ -537,13 +538,20 @@ __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t *__r
     const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
     TileKeys tk;
     load_tile_keys(keys, ti, wbase, tk);
-    uint32_t ns = 0, nk = 0;
+    uint32_t ns = 0, nk = 0, nb = 0;
 #pragma unroll
     for (int r = 0; r < kItems; ++r) {
         const RoundFlags f = round_flags(tk, ti, wbase, r);
         ns += static_cast<uint32_t>(__popcll(f.start));
         nk += static_cast<uint32_t>(__popcll(f.kept));
+        // segment starts per block of kBlk positions (two rounds per block)
+        nb += static_cast<uint32_t>(__popcll(f.start));
+        if (r & 1) {
+            if (lane == 0) blk_starts[tile * kBlksPerTile + wave * kBlksPerWave + (r >> 1)] = nb;
+            nb = 0;
+        }
     }
+    static_assert(kItems == 2 * kBlksPerWave, "two rounds of 64 positions per block");
     if (lane == 0) {
         wsum[0][wave] = ns;
         wsum[1][wave] = nk;
@@ -568,19 +576,31 @@ __global__ __launch_bounds__(kThreads) void seg_scan_kernel(TileSeg *__restrict_
     __shared__ uint64_t lds[kWaves];
     if (ctl->abort) return;
     const int64_t n = ctl->total_tiles;
-    uint64_t cs = 0, ck = 0, cd = 0;
-    for (int64_t base = 0; base < n; base += kThreads) {
-        const int64_t i = base + threadIdx.x;
-        TileSeg v{0, 0, 0, 0};
-        if (i < n) v = tseg[i];
-        uint64_t ts, tk, td;
-        const uint64_t es = block_excl_scan<uint64_t>(v.starts, lds, &ts);
-        const uint64_t ek = block_excl_scan<uint64_t>(v.kept, lds, &tk);
-        const uint64_t ed = block_excl_scan<uint64_t>(v.dimsum, lds, &td);
-        if (i < n) tseg[i] = TileSeg{cs + es, ck + ek, cd + ed, 0};
-        cs += ts;
-        ck += tk;
-        cd += td;
+    // thread i scans the contiguous run [i0, i1) of tiles: its sums first
+    // (independent loads, several in flight), one block scan of the runs'
+    // sums, then the run again with its exclusive prefixes
+    const int64_t per = (n + kThreads - 1) / kThreads;
+    const int64_t i0 = static_cast<int64_t>(threadIdx.x) * per < n ? static_cast<int64_t>(threadIdx.x) * per : n;
+    const int64_t i1 = i0 + per < n ? i0 + per : n;
+    uint64_t rs = 0, rk = 0, rd = 0;
+#pragma unroll 8
+    for (int64_t i = i0; i < i1; ++i) {
+        const TileSeg v = tseg[i];
+        rs += v.starts;
+        rk += v.kept;
+        rd += v.dimsum;
+    }
+    uint64_t cs, ck, cd;
+    uint64_t es = block_excl_scan<uint64_t>(rs, lds, &cs);
+    uint64_t ek = block_excl_scan<uint64_t>(rk, lds, &ck);
+    uint64_t ed = block_excl_scan<uint64_t>(rd, lds, &cd);
+#pragma unroll 8
+    for (int64_t i = i0; i < i1; ++i) {
+        const TileSeg v = tseg[i];
+        tseg[i] = TileSeg{es, ek, ed, 0};
+        es += v.starts;
+        ek += v.kept;
+        ed += v.dimsum;
     }
     if (threadIdx.x == 0) {
         *num_unique = static_cast<int64_t>(cs);
@@ -907,52 +927,33 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     }
 }
 
-// Per-tile facts of the reduce, computed once for all column slices: segment
-// starts per block, which block edges lie inside a long segment (one with
-// more than kBlk lookups), and the head / tail pieces of every block (read by
-// the combine kernel).
-__global__ __launch_bounds__(kThreads) void edges_kernel(const uint32_t *__restrict__ keys,
-                                                         const int64_t *__restrict__ seg_offsets,
-                                                         const Range *__restrict__ ranges, int T, Ctl *ctl,
-                                                         const TileSeg *__restrict__ tseg,
-                                                         TileEdges *__restrict__ edges,
-                                                         int32_t *__restrict__ head_seg,
-                                                         int32_t *__restrict__ tail_seg,
-                                                         int64_t *__restrict__ tail_list) {
-    __shared__ uint32_t blk_cnt[kBlksPerTile];
+// Per-tile facts of the reduce, computed once for all column slices by one
+// wave per tile (lane e for block edge e): segment starts before each block
+// (from the per-block counts of the segment-count kernel), which block edges
+// lie inside a long segment (one with more than kBlk lookups), and the head /
+// tail pieces of every block (read by the combine kernel).
+__global__ __launch_bounds__(64) void edges_kernel(const uint32_t *__restrict__ keys,
+                                                   const uint32_t *__restrict__ blk_starts,
+                                                   const int64_t *__restrict__ seg_offsets,
+                                                   const Range *__restrict__ ranges, int T, Ctl *ctl,
+                                                   const TileSeg *__restrict__ tseg,
+                                                   TileEdges *__restrict__ edges, int32_t *__restrict__ head_seg,
+                                                   int32_t *__restrict__ tail_seg,
+                                                   int64_t *__restrict__ tail_list) {
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->skip_rows || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
     const TileSeg pre = tseg[tile];
     const int tid = threadIdx.x;
-    // segment starts per block of kBlk positions: wave w, round r covers
-    // positions of block w * kBlksPerWave + r / 2 (two rounds per block)
     {
-        const int lane = tid & 63, wave = tid >> 6;
-        const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
-        TileKeys tk;
-        load_tile_keys(keys, ti, wbase, tk);
-        uint32_t c = 0;
-#pragma unroll
-        for (int r = 0; r < kItems; ++r) {
-            const RoundFlags f = round_flags(tk, ti, wbase, r);
-            c += static_cast<uint32_t>(__popcll(f.start));
-            if ((r & 1) && lane == 0) {
-                blk_cnt[wave * kBlksPerWave + (r >> 1)] = c;
-                c = 0;
-            }
-        }
-        static_assert(kItems == 2 * kBlksPerWave, "two rounds of 64 positions per block");
-    }
-    __syncthreads();
-    if (tid < 64) {
         // lane e: block edge e at position p_lo + e * kBlk (e = kBlksPerTile is
         // the tile's end).  The edge lies inside a segment when the keys on
         // both sides match; that segment is long when it has more than kBlk
         // lookups.
         const int e = tid;
-        const uint32_t cnt = e < kBlksPerTile ? blk_cnt[e] : 0u;
+        // segment starts in block e, counted by the segment-count kernel
+        const uint32_t cnt = e < kBlksPerTile ? blk_starts[tile * kBlksPerTile + e] : 0u;
         const uint32_t incl = wave_incl_scan(cnt);
         const uint32_t before = incl - cnt;  // starts in blocks < e
         const int64_t pos = ti.p_lo + static_cast<int64_t>(e) * kBlk;
@@ -1128,7 +1129,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
 // ------------------------------------------------------------- workspace
 
 struct Layout {
-    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, edges, head, tail, tails, partials, total;
+    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, edges, blk_starts, head, tail, tails, partials,
+        total;
     int64_t max_tiles, max_blocks, max_works, hist_chunks;
 };
 
@@ -1157,6 +1159,7 @@ Layout layout(const Plan &p, int64_t N) {
     L.sums = take(sizeof(uint32_t) * (L.hist_chunks + 1));
     L.tseg = take(sizeof(TileSeg) * L.max_tiles);
     L.edges = take(sizeof(TileEdges) * L.max_tiles);
+    L.blk_starts = take(sizeof(uint32_t) * L.max_blocks);
     L.head = take(sizeof(int32_t) * L.max_blocks);
     L.tail = take(sizeof(int32_t) * L.max_blocks);
     L.tails = take(sizeof(int64_t) * L.max_blocks);
@@ -1178,6 +1181,7 @@ hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT
     uint32_t *sums = reinterpret_cast<uint32_t *>(ws + L.sums);
     TileSeg *tseg = reinterpret_cast<TileSeg *>(ws + L.tseg);
     TileEdges *edges = reinterpret_cast<TileEdges *>(ws + L.edges);
+    uint32_t *blk_starts = reinterpret_cast<uint32_t *>(ws + L.blk_starts);
     int32_t *head = reinterpret_cast<int32_t *>(ws + L.head);
     int32_t *tail = reinterpret_cast<int32_t *>(ws + L.tail);
     int64_t *tails = reinterpret_cast<int64_t *>(ws + L.tails);
@@ -1228,13 +1232,14 @@ hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT
         cur ^= 1;
     }
     if ((me = mark(TBE_PHASE_SEGMENTS)) != hipSuccess) return me;
-    hipLaunchKernelGGL(seg_count_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg);
+    hipLaunchKernelGGL(seg_count_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
+                       blk_starts);
     hipLaunchKernelGGL(seg_scan_kernel, dim3(1), blk, 0, stream, tseg, ctl, num_unique, seg_offsets,
                        grad_row_offsets, capacity, status);
     hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
                        grad_idx, seg_offsets, grad_row_offsets);
-    hipLaunchKernelGGL(edges_kernel, tiles, blk, 0, stream, keys[cur], seg_offsets, ranges, T, ctl, tseg, edges, head,
-                       tail, tails);
+    hipLaunchKernelGGL(edges_kernel, tiles, dim3(64), 0, stream, keys[cur], blk_starts, seg_offsets, ranges, T, ctl,
+                       tseg, edges, head, tail, tails);
     if ((me = mark(TBE_PHASE_REDUCE)) != hipSuccess) return me;
     hipLaunchKernelGGL(reduce_kernel<V>, dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream, keys[cur],
                        vals[cur], grad_out, p.meta_dev, ranges, T, ctl, tseg, edges, p.total_dim, p.B * p.total_dim,
