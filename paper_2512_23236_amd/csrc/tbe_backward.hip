@@ -50,7 +50,7 @@ constexpr int kRadixBits = 8;
 constexpr int kBuckets = 1 << kRadixBits;
 constexpr uint32_t kSentinel = 0xffffffffu;
 constexpr int kPairLevels = 12;               // pairwise-sum depth in combine
-constexpr int kCombineGroups = 2048;          // combine grid (waves loop over the tail list)
+constexpr int kCombineGroups = 2048;          // combine grid (waves loop over runs of 64 blocks)
 constexpr int kKeyBags = 256;                 // bags per keys workgroup
 constexpr int kCombineBatch = 8;              // piece rows loaded at once in combine
 
@@ -60,7 +60,7 @@ struct Ctl {
     int32_t skip_rows;   // grad_rows too small: write no gradient row
     int64_t total_tiles;
     int64_t total_works;  // reduce work items: (table, column slice, tile)
-    uint64_t n_tails;     // blocks holding the first piece of a long segment
+    uint64_t spare;
     int64_t pad[4];
 };
 
@@ -209,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const IT *__restrict__ 
         ctl->skip_rows = 0;
         ctl->total_tiles = bad ? 0 : carry;
         ctl->total_works = bad ? 0 : wcarry;
-        ctl->n_tails = 0;
+        ctl->spare = 0;
         if (bad) atomicOr(status, TBE_STATUS_OFFSETS);
     }
 }
@@ -938,8 +938,7 @@ __global__ __launch_bounds__(64) void edges_kernel(const uint32_t *__restrict__ 
                                                    const Range *__restrict__ ranges, int T, Ctl *ctl,
                                                    const TileSeg *__restrict__ tseg,
                                                    TileEdges *__restrict__ edges, int32_t *__restrict__ head_seg,
-                                                   int32_t *__restrict__ tail_seg,
-                                                   int64_t *__restrict__ tail_list) {
+                                                   int32_t *__restrict__ tail_seg) {
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->skip_rows || ctl->abort) return;
     TileInfo ti;
@@ -976,13 +975,6 @@ __global__ __launch_bounds__(64) void edges_kernel(const uint32_t *__restrict__ 
             head_seg[gq] = head ? static_cast<int32_t>(u) : -1;
             tail_seg[gq] = tail ? static_cast<int32_t>(u_next) : -1;
         }
-        // append this tile's tail blocks to the combine kernel's work list
-        // (list order is free: every entry is summed and written on its own)
-        const uint64_t tmask = __ballot(tail);
-        uint64_t base = 0;
-        if (e == 0 && tmask) base = atomicAdd(&ctl->n_tails, static_cast<uint64_t>(__popcll(tmask)));
-        base = __shfl(base, 0);
-        if (tail) tail_list[base + __popcll(tmask & lanemask_lt())] = gq;
     }
 }
 
@@ -1037,14 +1029,13 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
 // Sums the pieces of every segment that crosses a block edge, in a fixed
 // pairwise order (binary-counter summation over the pieces: the tail piece of
 // the block where the segment begins, then the head pieces of the blocks that
-// follow), and writes its gradient row once.  One wave per entry of the tail
-// list, which holds the block of each such segment's tail piece.
+// follow), and writes its gradient row once.  A wave takes a run of 64 blocks
+// and handles the segments whose tail piece lies in one of them.
 __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restrict__ ranges, int T,
                                                            const TableMeta *__restrict__ meta,
                                                            const Ctl *__restrict__ ctl,
                                                            const int32_t *__restrict__ head_seg,
                                                            const int32_t *__restrict__ tail_seg,
-                                                           const int64_t *__restrict__ tail_list,
                                                            const float *__restrict__ partials, int max_dim,
                                                            const int64_t *__restrict__ grad_row_offsets,
                                                            float *__restrict__ grad_rows) {
@@ -1052,76 +1043,81 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (ctl->skip_rows || ctl->abort) return;
     const int64_t nblk = ctl->total_tiles * kBlksPerTile;
-    const int64_t ntail = static_cast<int64_t>(ctl->n_tails);
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kWaves + wave; i < ntail;
-         i += static_cast<int64_t>(gridDim.x) * kWaves) {
-        const int64_t q = tail_list[i];
-        const int32_t u = tail_seg[q];
-        const int t = find_table(ranges, T, q / kBlksPerTile);
-        const int nvec = meta[t].dim / 4;
-        float *out = grad_rows + grad_row_offsets[u];
-        // pieces: the tail of block q, then the heads of blocks q+1 .. q+nh
-        int64_t nh = 0;
-        for (;;) {
-            const int64_t qq = q + 1 + nh + lane;
-            const bool same = qq < nblk && head_seg[qq] == u;
-            const uint64_t run = ~__ballot(same);  // first lane that is not a head of u
-            const int c = run ? __ffsll(static_cast<long long>(run)) - 1 : 64;
-            nh += c;
-            if (c < 64) break;
-        }
-        const int64_t npieces = nh + 1;
-        for (int c0 = 0; c0 < nvec; c0 += 64) {
-            const int cv = c0 + lane;
-            const bool act = cv < nvec;
-            float4 st[kPairLevels];
-            float4 top = make_float4(0.f, 0.f, 0.f, 0.f);
-            bool top_used = false;
-            uint32_t n = 0;
-            // piece p lives in partial slot 2q+1 (p = 0) or 2(q+p) (p > 0)
-            auto slot_of = [&](int64_t pc) { return pc == 0 ? 2 * q + 1 : 2 * (q + pc); };
-            for (int64_t p0 = 0; p0 < npieces; p0 += kCombineBatch) {
-                float4 xs[kCombineBatch];
+    // waves take runs of 64 blocks and sum the segments whose tail piece lies
+    // in one of them (tail_seg >= 0), lowest block first
+    for (int64_t b0 = (static_cast<int64_t>(blockIdx.x) * kWaves + wave) * 64; b0 < nblk;
+         b0 += static_cast<int64_t>(gridDim.x) * kWaves * 64) {
+        uint64_t todo = __ballot(b0 + lane < nblk && tail_seg[b0 + lane] >= 0);
+        while (todo) {
+            const int64_t q = b0 + __builtin_ctzll(todo);
+            todo &= todo - 1;
+            const int32_t u = tail_seg[q];
+            const int t = find_table(ranges, T, q / kBlksPerTile);
+            const int nvec = meta[t].dim / 4;
+            float *out = grad_rows + grad_row_offsets[u];
+            // pieces: the tail of block q, then the heads of blocks q+1 .. q+nh
+            int64_t nh = 0;
+            for (;;) {
+                const int64_t qq = q + 1 + nh + lane;
+                const bool same = qq < nblk && head_seg[qq] == u;
+                const uint64_t run = ~__ballot(same);  // first lane that is not a head of u
+                const int c = run ? __ffsll(static_cast<long long>(run)) - 1 : 64;
+                nh += c;
+                if (c < 64) break;
+            }
+            const int64_t npieces = nh + 1;
+            for (int c0 = 0; c0 < nvec; c0 += 64) {
+                const int cv = c0 + lane;
+                const bool act = cv < nvec;
+                float4 st[kPairLevels];
+                float4 top = make_float4(0.f, 0.f, 0.f, 0.f);
+                bool top_used = false;
+                uint32_t n = 0;
+                // piece p lives in partial slot 2q+1 (p = 0) or 2(q+p) (p > 0)
+                auto slot_of = [&](int64_t pc) { return pc == 0 ? 2 * q + 1 : 2 * (q + pc); };
+                for (int64_t p0 = 0; p0 < npieces; p0 += kCombineBatch) {
+                    float4 xs[kCombineBatch];
 #pragma unroll
-                for (int r = 0; r < kCombineBatch; ++r) {
-                    const int64_t pc = p0 + r < npieces ? p0 + r : npieces - 1;  // clamped, unconditional
-                    xs[r] = act ? *reinterpret_cast<const float4 *>(partials + slot_of(pc) * max_dim + cv * 4)
-                                : make_float4(0.f, 0.f, 0.f, 0.f);
-                }
+                    for (int r = 0; r < kCombineBatch; ++r) {
+                        const int64_t pc = p0 + r < npieces ? p0 + r : npieces - 1;  // clamped, unconditional
+                        xs[r] = act ? *reinterpret_cast<const float4 *>(partials + slot_of(pc) * max_dim + cv * 4)
+                                    : make_float4(0.f, 0.f, 0.f, 0.f);
+                    }
 #pragma unroll
-                for (int r = 0; r < kCombineBatch; ++r) {
-                    if (p0 + r >= npieces) break;
-                    float4 x = xs[r];
-                    bool done = false;
+                    for (int r = 0; r < kCombineBatch; ++r) {
+                        if (p0 + r >= npieces) break;
+                        float4 x = xs[r];
+                        bool done = false;
 #pragma unroll
-                    for (int l = 0; l < kPairLevels; ++l) {
-                        if (!done) {
-                            if ((n >> l) & 1u) {
-                                x = make_float4(st[l].x + x.x, st[l].y + x.y, st[l].z + x.z, st[l].w + x.w);
-                            } else {
-                                st[l] = x;
-                                done = true;
+                        for (int l = 0; l < kPairLevels; ++l) {
+                            if (!done) {
+                                if ((n >> l) & 1u) {
+                                    x = make_float4(st[l].x + x.x, st[l].y + x.y, st[l].z + x.z, st[l].w + x.w);
+                                } else {
+                                    st[l] = x;
+                                    done = true;
+                                }
                             }
                         }
+                        if (!done) {
+                            top = top_used ? make_float4(top.x + x.x, top.y + x.y, top.z + x.z, top.w + x.w) : x;
+                            top_used = true;
+                        }
+                        ++n;
                     }
-                    if (!done) {
-                        top = top_used ? make_float4(top.x + x.x, top.y + x.y, top.z + x.z, top.w + x.w) : x;
-                        top_used = true;
-                    }
-                    ++n;
                 }
-            }
-            float4 sum = top;
-            bool have = top_used;
+                float4 sum = top;
+                bool have = top_used;
 #pragma unroll
-            for (int l = kPairLevels - 1; l >= 0; --l) {
-                if ((n >> l) & 1u) {
-                    sum = have ? make_float4(sum.x + st[l].x, sum.y + st[l].y, sum.z + st[l].z, sum.w + st[l].w)
-                               : st[l];
-                    have = true;
+                for (int l = kPairLevels - 1; l >= 0; --l) {
+                    if ((n >> l) & 1u) {
+                        sum = have ? make_float4(sum.x + st[l].x, sum.y + st[l].y, sum.z + st[l].z, sum.w + st[l].w)
+                                   : st[l];
+                        have = true;
+                    }
                 }
+                if (act) store4(out + cv * 4, sum);
             }
-            if (act) store4(out + cv * 4, sum);
         }
     }
 }
@@ -1129,8 +1125,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
 // ------------------------------------------------------------- workspace
 
 struct Layout {
-    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, edges, blk_starts, head, tail, tails, partials,
-        total;
+    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, edges, blk_starts, head, tail, partials, total;
     int64_t max_tiles, max_blocks, max_works, hist_chunks;
 };
 
@@ -1162,7 +1157,6 @@ Layout layout(const Plan &p, int64_t N) {
     L.blk_starts = take(sizeof(uint32_t) * L.max_blocks);
     L.head = take(sizeof(int32_t) * L.max_blocks);
     L.tail = take(sizeof(int32_t) * L.max_blocks);
-    L.tails = take(sizeof(int64_t) * L.max_blocks);
     L.partials = take(sizeof(float) * 2 * L.max_blocks * static_cast<size_t>(p.max_dim));
     L.total = o;
     return L;
@@ -1184,7 +1178,6 @@ hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT
     uint32_t *blk_starts = reinterpret_cast<uint32_t *>(ws + L.blk_starts);
     int32_t *head = reinterpret_cast<int32_t *>(ws + L.head);
     int32_t *tail = reinterpret_cast<int32_t *>(ws + L.tail);
-    int64_t *tails = reinterpret_cast<int64_t *>(ws + L.tails);
     float *partials = reinterpret_cast<float *>(ws + L.partials);
     const int check = p.bounds_check;
     const int T = p.T;
@@ -1239,17 +1232,18 @@ hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT
     hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
                        grad_idx, seg_offsets, grad_row_offsets);
     hipLaunchKernelGGL(edges_kernel, tiles, dim3(64), 0, stream, keys[cur], blk_starts, seg_offsets, ranges, T, ctl,
-                       tseg, edges, head, tail, tails);
+                       tseg, edges, head, tail);
     if ((me = mark(TBE_PHASE_REDUCE)) != hipSuccess) return me;
     hipLaunchKernelGGL(reduce_kernel<V>, dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream, keys[cur],
                        vals[cur], grad_out, p.meta_dev, ranges, T, ctl, tseg, edges, p.total_dim, p.B * p.total_dim,
                        grad_rows, partials, p.max_dim, static_cast<const float *>(p.zero_page));
     if ((me = mark(TBE_PHASE_COMBINE)) != hipSuccess) return me;
-    // the tail list is short (one entry per segment longer than a block)
-    const int64_t combine_groups = (L.max_blocks + kWaves - 1) / kWaves < kCombineGroups
-                                       ? (L.max_blocks + kWaves - 1) / kWaves : kCombineGroups;
+    // one wave per run of 64 blocks, at most kCombineGroups workgroups
+    const int64_t runs = (L.max_blocks + 63) / 64;
+    const int64_t combine_groups = (runs + kWaves - 1) / kWaves < kCombineGroups ? (runs + kWaves - 1) / kWaves
+                                                                                 : kCombineGroups;
     hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>(combine_groups)), blk, 0, stream, ranges, T,
-                       p.meta_dev, ctl, head, tail, tails, partials, p.max_dim, grad_row_offsets, grad_rows);
+                       p.meta_dev, ctl, head, tail, partials, p.max_dim, grad_row_offsets, grad_rows);
     const hipError_t e = hipGetLastError();
     return e != hipSuccess ? e : mark(TBE_NUM_PHASES);
 }
