@@ -232,6 +232,8 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
                                                         uint32_t *__restrict__ keys, V *__restrict__ vals,
                                                         int32_t *status) {
     __shared__ int64_t off[kKeyBags + 1];
+    __shared__ int64_t bag_rows[kKeyBags];  // R_t of each bag's table
+    __shared__ uint32_t bag_b[kKeyBags];    // batch row of each bag
     __shared__ int bad;
     const int tid = threadIdx.x;
     const int64_t k0 = static_cast<int64_t>(blockIdx.x) * kKeyBags;
@@ -239,6 +241,12 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
     const int nk = nbags - k0 < kKeyBags ? static_cast<int>(nbags - k0) : kKeyBags;
     if (tid == 0) bad = 0;
     for (int i = tid; i <= nk; i += kThreads) off[i] = static_cast<int64_t>(offsets[k0 + i]);
+    // table and batch row once per bag, not per lookup
+    for (int i = tid; i < nk; i += kThreads) {
+        const int64_t t = (k0 + i) / B;
+        bag_b[i] = static_cast<uint32_t>(k0 + i - t * B);
+        bag_rows[i] = meta[t].rows;
+    }
     __syncthreads();
     if (check) {
         // each bag lies inside its table's range, in order
@@ -264,11 +272,10 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
             const int mid = (lo + hi) >> 1;
             if (off[mid] <= j) lo = mid; else hi = mid;
         }
-        const int64_t k = k0 + lo;
-        const int64_t t = k / B, b = k - t * B;
+        const uint32_t b = bag_b[lo];
         const int64_t idx = static_cast<int64_t>(__builtin_nontemporal_load(indices + j));
         uint32_t key = static_cast<uint32_t>(idx);
-        if (check && (idx < 0 || idx >= meta[t].rows)) {
+        if (check && (idx < 0 || idx >= bag_rows[lo])) {
             key = kSentinel;
             atomicOr(status, TBE_STATUS_INDEX_OOB);
         }
