@@ -7,17 +7,18 @@
 // Pipeline (all on the caller's stream, no host synchronisation):
 //   setup     per-table lookup ranges [offsets[tB], offsets[(t+1)B]) and the
 //             tiling of each range into tiles of kTile positions.
-//   keys      one wave per bag writes key_j = idx_j (32-bit, local to the
-//             table) and val_j = b(j) (plus the weight when weighted).  A
+//   keys      one workgroup per run of bags writes key_j = idx_j (32-bit,
+//             local to the table) and val_j = b(j) (plus the weight).  A
 //             table's lookups already occupy exactly the positions its rows
 //             take in the global order, so sorting every table's range by
 //             its local key yields the global stable sort.
 //   radix     stable LSD radix sort of each range, 8-bit digits, over the
-//             bits of the largest table: per pass a tile histogram, one
-//             device-wide exclusive scan (table-major, digit-major, tile-
-//             minor, so scanned counts are final positions), and a stable
-//             scatter that ranks keys with wave ballots and stages the tile
-//             in LDS so global writes run in digit order.
+//             bits of the largest table: per pass a tile histogram (one
+//             contiguous row per tile), a per-table scan of every digit's
+//             column over the table's tiles, and a stable scatter that
+//             ranks keys with wave ballots, derives its digits' final
+//             positions from the table's digit totals and its tile's row,
+//             and stages the tile in LDS so global writes run in digit order.
 //   segments  per tile: segment starts (key change) per block and tile and
 //             kept lookups; one scan over tiles; then grad_idx / seg_offsets /
 //             grad_row_offsets are written for every segment start.
@@ -334,77 +335,42 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__
     uint32_t c = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) c += cnt[w][tid];
-    // layout: table-major, digit-major, tile-minor
-    const int64_t base = ranges[ti.t].tile_base * kBuckets;
-    hist[base + static_cast<int64_t>(tid) * ti.ntiles + ti.local] = c;
+    // layout: tile-major (one contiguous row of kBuckets counts per tile)
+    hist[tile * kBuckets + tid] = c;
 }
 
-// Exclusive scan over `count` u32 values in place: chunk sums, a one-block
-// scan of the sums, then each chunk rescanned with its offset.
-constexpr int kScanChunk = kThreads * kItems;
+// Per table, per digit: the exclusive prefix of the digit's counts over the
+// table's tiles (in place), and the digit's total over the table.  One
+// workgroup per table, one thread per digit; a wave's loads cover 64
+// consecutive digits of one tile row (coalesced), several tiles in flight.
+constexpr int kColAhead = 8;
 
-__device__ inline int64_t hist_count(const Ctl *ctl) { return ctl->total_tiles * kBuckets; }
-
-__global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const uint32_t *__restrict__ data,
-                                                               uint32_t *__restrict__ sums,
-                                                               const Ctl *__restrict__ ctl) {
-    __shared__ uint32_t lds[kWaves];
-    const int64_t count = hist_count(ctl);
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanChunk;
-    if (base >= count) return;
-    uint32_t s = 0;
-    for (int i = threadIdx.x; i < kScanChunk; i += kThreads)
-        if (base + i < count) s += data[base + i];
-    uint32_t tot;
-    block_excl_scan<uint32_t>(s, lds, &tot);
-    if (threadIdx.x == 0) sums[blockIdx.x] = tot;
-}
-
-__global__ __launch_bounds__(kThreads) void scan_top_kernel(uint32_t *__restrict__ sums,
+__global__ __launch_bounds__(kThreads) void col_scan_kernel(uint32_t *__restrict__ hist,
+                                                            uint32_t *__restrict__ totals,
+                                                            const Range *__restrict__ ranges,
                                                             const Ctl *__restrict__ ctl) {
-    __shared__ uint32_t lds[kWaves];
-    const int64_t n = (hist_count(ctl) + kScanChunk - 1) / kScanChunk;
-    uint32_t carry = 0;
-    for (int64_t base = 0; base < n; base += kThreads) {
-        const int64_t i = base + threadIdx.x;
-        const uint32_t v = i < n ? sums[i] : 0u;
-        uint32_t tot;
-        const uint32_t ex = block_excl_scan<uint32_t>(v, lds, &tot);
-        if (i < n) sums[i] = carry + ex;
-        carry += tot;
-    }
-}
-
-__global__ __launch_bounds__(kThreads) void scan_down_kernel(uint32_t *__restrict__ data,
-                                                             const uint32_t *__restrict__ sums,
-                                                             const Ctl *__restrict__ ctl) {
-    __shared__ uint32_t lds[kWaves];
-    const int64_t count = hist_count(ctl);
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanChunk;
-    if (base >= count) return;
-    // blocked: thread i owns items [i*kItems, (i+1)*kItems) of the chunk
-    uint32_t v[kItems];
-    uint32_t s = 0;
-    const int64_t my = base + static_cast<int64_t>(threadIdx.x) * kItems;
+    if (ctl->abort) return;
+    const int t = blockIdx.x, d = threadIdx.x;
+    const int64_t t0 = ranges[t].tile_base, t1 = ranges[t + 1].tile_base;
+    uint32_t run = 0;
+    for (int64_t c = t0; c < t1; c += kColAhead) {
+        uint32_t h[kColAhead];
 #pragma unroll
-    for (int q = 0; q < kItems; ++q) {
-        v[q] = my + q < count ? data[my + q] : 0u;
-        s += v[q];
-    }
-    uint32_t tot;
-    uint32_t run = sums[blockIdx.x] + block_excl_scan<uint32_t>(s, lds, &tot);
+        for (int r = 0; r < kColAhead; ++r) h[r] = c + r < t1 ? hist[(c + r) * kBuckets + d] : 0u;
 #pragma unroll
-    for (int q = 0; q < kItems; ++q) {
-        if (my + q < count) data[my + q] = run;
-        run += v[q];
+        for (int r = 0; r < kColAhead; ++r) {
+            if (c + r < t1) hist[(c + r) * kBuckets + d] = run;
+            run += h[r];
+        }
     }
+    totals[static_cast<int64_t>(t) * kBuckets + d] = run;
 }
 
 template <typename V>
 __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     const uint32_t *__restrict__ keys_in, const V *__restrict__ vals_in, uint32_t *__restrict__ keys_out,
-    V *__restrict__ vals_out, const uint32_t *__restrict__ scanned, const Range *__restrict__ ranges, int T,
-    const Ctl *__restrict__ ctl, int shift, int nbits) {
+    V *__restrict__ vals_out, const uint32_t *__restrict__ prefix, const uint32_t *__restrict__ totals,
+    const Range *__restrict__ ranges, int T, const Ctl *__restrict__ ctl, int shift, int nbits) {
     __shared__ uint32_t cnt[kWaves][kBuckets];  // per-wave digit counts, then wave offsets
     __shared__ uint32_t tstart[kBuckets];       // first tile-local slot of each digit
     __shared__ uint32_t goff[kBuckets];         // first global slot of each digit for this tile
@@ -466,7 +432,11 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
         }
         uint32_t tot;
         tstart[d] = block_excl_scan<uint32_t>(run, lds, &tot);
-        goff[d] = scanned[ranges[ti.t].tile_base * kBuckets + static_cast<int64_t>(d) * ti.ntiles + ti.local];
+        // first global slot of digit d for this tile: the table's first
+        // position, the table's keys of smaller digits, then this digit's keys
+        // in the table's earlier tiles
+        const uint32_t below = block_excl_scan<uint32_t>(totals[static_cast<int64_t>(ti.t) * kBuckets + d], lds, &tot);
+        goff[d] = static_cast<uint32_t>(ranges[ti.t].start) + below + prefix[tile * kBuckets + d];
     }
     __syncthreads();
 #pragma unroll
@@ -1132,8 +1102,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
 // ------------------------------------------------------------- workspace
 
 struct Layout {
-    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, sums, tseg, edges, blk_starts, head, tail, partials, total;
-    int64_t max_tiles, max_blocks, max_works, hist_chunks;
+    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, totals, tseg, edges, blk_starts, head, tail, partials, total;
+    int64_t max_tiles, max_blocks, max_works;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1144,7 +1114,6 @@ Layout layout(const Plan &p, int64_t N) {
     L.max_tiles = (N + kTile - 1) / kTile + p.T;
     L.max_blocks = L.max_tiles * kBlksPerTile;
     L.max_works = L.max_tiles * ((p.max_dim + kSliceCols - 1) / kSliceCols);
-    L.hist_chunks = (L.max_tiles * kBuckets + kScanChunk - 1) / kScanChunk;
     size_t o = 0;
     auto take = [&](size_t bytes) {
         const size_t at = o;
@@ -1158,7 +1127,7 @@ Layout layout(const Plan &p, int64_t N) {
     L.vals0 = take(vb * N);
     L.vals1 = take(vb * N);
     L.hist = take(sizeof(uint32_t) * L.max_tiles * kBuckets);
-    L.sums = take(sizeof(uint32_t) * (L.hist_chunks + 1));
+    L.totals = take(sizeof(uint32_t) * kBuckets * p.T);
     L.tseg = take(sizeof(TileSeg) * L.max_tiles);
     L.edges = take(sizeof(TileEdges) * L.max_tiles);
     L.blk_starts = take(sizeof(uint32_t) * L.max_blocks);
@@ -1179,7 +1148,7 @@ hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT
     uint32_t *keys[2] = {reinterpret_cast<uint32_t *>(ws + L.keys0), reinterpret_cast<uint32_t *>(ws + L.keys1)};
     V *vals[2] = {reinterpret_cast<V *>(ws + L.vals0), reinterpret_cast<V *>(ws + L.vals1)};
     uint32_t *hist = reinterpret_cast<uint32_t *>(ws + L.hist);
-    uint32_t *sums = reinterpret_cast<uint32_t *>(ws + L.sums);
+    uint32_t *totals = reinterpret_cast<uint32_t *>(ws + L.totals);
     TileSeg *tseg = reinterpret_cast<TileSeg *>(ws + L.tseg);
     TileEdges *edges = reinterpret_cast<TileEdges *>(ws + L.edges);
     uint32_t *blk_starts = reinterpret_cast<uint32_t *>(ws + L.blk_starts);
@@ -1222,13 +1191,10 @@ hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT
     for (int shift = 0; shift < bits; shift += kRadixBits) {
         const int nb = bits - shift < kRadixBits ? bits - shift : kRadixBits;
         hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, keys[cur], ranges, T, ctl, shift, nb, hist);
-        hipLaunchKernelGGL(scan_reduce_kernel, dim3(static_cast<unsigned>(L.hist_chunks)), blk, 0, stream, hist,
-                           sums, ctl);
-        hipLaunchKernelGGL(scan_top_kernel, dim3(1), blk, 0, stream, sums, ctl);
-        hipLaunchKernelGGL(scan_down_kernel, dim3(static_cast<unsigned>(L.hist_chunks)), blk, 0, stream, hist,
-                           sums, ctl);
+        hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), blk, 0, stream, hist, totals, ranges,
+                           ctl);
         hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, blk, 0, stream, keys[cur], vals[cur], keys[cur ^ 1],
-                           vals[cur ^ 1], hist, ranges, T, ctl, shift, nb);
+                           vals[cur ^ 1], hist, totals, ranges, T, ctl, shift, nb);
         cur ^= 1;
     }
     if ((me = mark(TBE_PHASE_SEGMENTS)) != hipSuccess) return me;
