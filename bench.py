@@ -60,20 +60,21 @@ def forward_bytes(spec, offsets_host: np.ndarray, index_bytes: int = 8, out_byte
     return rows + idx + bags
 
 
-def backward_bytes(spec, N: int, U: int, grad_floats: int, index_bytes: int = 8) -> int:
-    """Compulsory bytes of one backward: indices and offsets read, the fp32
-    output gradient read once, int64 row ids, segment offsets and row offsets
+def backward_bytes(spec, N: int, U: int, grad_floats: int, index_bytes: int = 8, grad_out_bytes: int = 4) -> int:
+    """Compulsory bytes of one backward: indices and offsets read, the output
+    gradient read once, int64 row ids, segment offsets and row offsets
     written, and the fp32 gradient rows written."""
-    return (index_bytes * N + index_bytes * (spec.T * spec.B + 1) + 4 * spec.B * spec.total_dim
+    return (index_bytes * N + index_bytes * (spec.T * spec.B + 1) + grad_out_bytes * spec.B * spec.total_dim
             + 3 * 8 * (U + 1) + 4 * grad_floats)
 
 
-def reduce_bytes(spec, N: int, grad_floats: int, carries_weight: bool) -> int:
+def reduce_bytes(spec, N: int, grad_floats: int, carries_weight: bool, grad_out_bytes: int = 4) -> int:
     """Algorithmic bytes of one segmented-reduce launch: each sorted lookup's
     key and batch row (4 + 4 bytes, + 4 for its weight: the per-sample weight,
-    or 1/L under mean pooling), the fp32 output gradient read once, and the
-    fp32 gradient rows written."""
-    return (8 + (4 if carries_weight else 0)) * N + 4 * spec.B * spec.total_dim + 4 * grad_floats
+    or 1/L under mean pooling), the output gradient read once, and the fp32
+    gradient rows written."""
+    return ((8 + (4 if carries_weight else 0)) * N + grad_out_bytes * spec.B * spec.total_dim
+            + 4 * grad_floats)
 
 
 # Counter-derived HBM traffic per launch, with the hash of the kernel source it
@@ -313,7 +314,7 @@ def variant_text(args, spec) -> str:
     if args.index_type != "i64":
         parts.append("int32 indices and offsets")
     if args.out_dtype != "f32":
-        parts.append(f"{args.out_dtype} output")
+        parts.append(f"{args.out_dtype} output" + (" and grad_out" if spec.grad else ""))
     return ("; " + ", ".join(parts)) if parts else ""
 
 
@@ -382,6 +383,8 @@ def main():
                     pooling=args.pooling, index_dtype=index_dtype, out_dtype=out_dtype)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     out = torch.empty((spec.B, plan.total_dim), dtype=out_dtype, device=dev)
+    if spec.grad and out_dtype != torch.float32:
+        d["grad_out"] = d["grad_out"].to(out_dtype)  # the gradient of out has out's type
     training = spec.grad
     grads = None
     if training:
@@ -463,7 +466,8 @@ def main():
         bwd_avg = float(np.mean(bwd_ms))
         U = grads.num_unique()
         gro_total = int(grads.grad_row_offsets[U].item())
-        bbytes = backward_bytes(spec, N, U, gro_total, ib)
+        gob = 4 if args.out_dtype == "f32" else 2
+        bbytes = backward_bytes(spec, N, U, gro_total, ib, gob)
         res["backward"] = {"ms": bwd_avg, "ms_p10": float(np.percentile(bwd_ms, 10)),
                            "ms_p90": float(np.percentile(bwd_ms, 90)), "lookups_per_s": N / (bwd_avg * 1e-3),
                            "unique_rows": U, "compulsory_bytes": bbytes,
@@ -471,7 +475,7 @@ def main():
                            "frac_of_hbm_peak": bbytes / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
                            "phases_ms": {name: float(np.mean(t)) for name, t in zip(tbe.PHASES, phase_ms)}}
         red_ms = float(np.mean(phase_ms[tbe.PHASES.index("reduce")]))
-        rbytes = reduce_bytes(spec, N, gro_total, spec.weighted or args.pooling == "mean")
+        rbytes = reduce_bytes(spec, N, gro_total, spec.weighted or args.pooling == "mean", gob)
         red_gbs = rbytes / (red_ms * 1e-3) / 1e9
         roof["reduce_kernel"] = {"bound": "hbm", "kernel": "reduce_kernel", "ms": red_ms, "achieved": red_gbs,
                                  "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": red_gbs / HBM_PEAK_GBS,

@@ -117,8 +117,10 @@ typedef struct tbe_desc {
     int32_t pooling;              /* enum tbe_pooling (0: sum)                    */
     int32_t index_type;           /* enum tbe_index_type of indices and offsets
                                      (0: int64)                                  */
-    int32_t out_dtype;            /* enum tbe_dtype of the forward output: F32,
-                                     F16 or BF16 (0: fp32); rounded to nearest
+    int32_t out_dtype;            /* enum tbe_dtype of the forward output and of
+                                     its gradient (grad_out of tbe_backward and
+                                     tbe_weight_grad): F32, F16 or BF16 (0:
+                                     fp32); the output is rounded to nearest
                                      even from the fp32 result                   */
 } tbe_desc;
 
@@ -176,7 +178,8 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const void *indice
  * each weight, so for lookup j of bag (t, b)
  *     grad_weights[j] = sum_{d < D_t} grad_out[b, dim_off[t] + d] * W_t[idx_j, d].
  *   tables, indices, offsets, num_indices   as in tbe_forward
- *   grad_out            device fp32 [B x total_dim] row-major, 16-byte aligned
+ *   grad_out            device [B x total_dim] of the plan's out_dtype,
+ *                       row-major, 16-byte aligned
  *   grad_weights        device fp32 [num_indices]; every entry of every bag is
  *                       written (0 for a lookup whose index fails the bounds
  *                       check, which also sets TBE_STATUS_INDEX_OOB)
@@ -187,7 +190,7 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const void *indice
  * order (per lane in column order, then a fixed tree across lanes), so results
  * are bitwise reproducible.
  */
-int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out, const void *indices,
+int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const void *grad_out, const void *indices,
                         const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                         void *stream);
 
@@ -250,8 +253,9 @@ int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, 
 
 /*
  * Sparse gradient of the tables.
- *   grad_out            device fp32 [B x total_dim], the gradient of `out`
- *                       (fp32 whatever the plan's out_dtype)
+ *   grad_out            device [B x total_dim] of the plan's out_dtype, the
+ *                       gradient of `out` (16-bit values are widened exactly;
+ *                       all sums are fp32)
  *   indices, offsets, num_indices, per_sample_weights   as in tbe_forward; with
  *                       mean pooling each lookup of a bag of L lookups carries
  *                       the weight fl32(1/L)
@@ -275,7 +279,7 @@ int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, 
  * Every gradient row has a single writer and a fixed summation order, so the
  * result is bitwise reproducible.
  */
-int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const void *indices,
+int32_t tbe_backward(const tbe_plan *plan, const void *grad_out, const void *indices,
                      const void *offsets, int64_t num_indices, const float *per_sample_weights,
                      void *workspace, size_t workspace_bytes, float *grad_rows,
                      int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
@@ -301,7 +305,7 @@ enum tbe_backward_phase {
  * this tbe_backward.  A failed record returns TBE_ERR_HIP.
  * For callers that time the parts of the backward (profilers, benchmarks).
  */
-int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const void *indices,
+int32_t tbe_backward_timed(const tbe_plan *plan, const void *grad_out, const void *indices,
                            const void *offsets, int64_t num_indices, const float *per_sample_weights,
                            void *workspace, size_t workspace_bytes, float *grad_rows,
                            int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,

@@ -716,6 +716,13 @@ __device__ inline void store_cols(uint64_t base, uint32_t off, const float (&s)[
     }
 }
 
+// A 16-bit grad_out element (fp16 or bf16) widened to fp32 (exact).
+template <int GT>
+__device__ inline float widen16(uint32_t h) {
+    if constexpr (GT == TBE_F16) return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h)));
+    else return __uint_as_float((h & 0xffffu) << 16);
+}
+
 __device__ inline uint32_t rl(uint32_t x, int l) {
     return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x), l));
 }
@@ -755,9 +762,9 @@ constexpr int kBufferWord3 = 0x00020000;
 // moves its position's values into scalar registers, so addressing and the
 // flush test are uniform.  A ring of kRing row loads stays in flight;
 // positions the wave does not own read the zero page with weight 0.
-template <typename V, bool kWide>
+template <typename V, bool kWide, int GT>
 __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
-                                   const float *__restrict__ grad_out, const TableMeta &m, const TileInfo &ti,
+                                   const void *__restrict__ grad_out, const TableMeta &m, const TileInfo &ti,
                                    const TileSeg &pre, const TileEdges &te, int64_t total_dim,
                                    int64_t gout_elems, float *__restrict__ grad_rows,
                                    float *__restrict__ partials, int max_dim, int64_t tile, int c0,
@@ -781,14 +788,16 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     const uint32_t u_r0 = static_cast<uint32_t>(pre.starts) + te.starts[q0];
     const int64_t part0 = 2 * (tile * kBlksPerTile) * max_dim;
 
+    constexpr int GES = GT == TBE_F32 ? 4 : 2;  // bytes per grad_out element
     const int col = c0 + lane;
     const bool vact = col < m.dim;
-    const uint32_t voff = vact ? static_cast<uint32_t>(lane * 4) : 0u;  // bytes
-    const float *const gbase = grad_out + m.dim_off + c0;
+    const uint32_t voff = vact ? static_cast<uint32_t>(lane * GES) : 0u;  // bytes into a grad_out row
+    const uint32_t doff = static_cast<uint32_t>(lane * 4);                // bytes into an fp32 gradient row
+    const char *const gbase = static_cast<const char *>(grad_out) + (m.dim_off + c0) * GES;
     // grad_out below 2 GiB: rows are 32-bit byte offsets from gbase into a
     // buffer resource; a step whose position is not owned reads through a
     // resource of length 0, which returns zeros without a memory access
-    const uint32_t gbytes = static_cast<uint32_t>((gout_elems - (m.dim_off + c0)) * 4);
+    const uint32_t gbytes = static_cast<uint32_t>((gout_elems - (m.dim_off + c0)) * GES);
     float *const row_base = grad_rows + static_cast<int64_t>(pre.dimsum) + c0;
     float *const part_base = partials + part0 + c0;
     struct Raw {
@@ -841,10 +850,10 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
         float wl;
         val_split<V>(r.val, b, wl);
         if constexpr (kWide) {
-            const float *row = gbase + static_cast<int64_t>(b) * total_dim;
-            o.addr = reinterpret_cast<uint64_t>(own ? row : zero_page);
+            const char *row = gbase + static_cast<int64_t>(b) * total_dim * GES;
+            o.addr = reinterpret_cast<uint64_t>(own ? row : reinterpret_cast<const char *>(zero_page));
         } else {
-            o.addr = static_cast<uint32_t>(b) * static_cast<uint32_t>(total_dim * 4);
+            o.addr = static_cast<uint32_t>(b) * static_cast<uint32_t>(total_dim * GES);
         }
         o.dst = reinterpret_cast<uint64_t>(dst);
         o.w = own ? wl : 0.f;
@@ -862,15 +871,25 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     // one gradient column of the row slice of step j of a chunk
     auto fetch = [&](const Cooked &ck, int j, float (&d)[1]) {
         if constexpr (kWide) {
-            load_cols<1>(rl64(ck.addr, j), voff, d);
+            if constexpr (GT == TBE_F32) {
+                load_cols<1>(rl64(ck.addr, j), voff, d);
+            } else {
+                uint32_t off = voff;
+                asm volatile("" : "+v"(off));
+                const gptr<char> p = reinterpret_cast<gptr<char>>(rl64(ck.addr, j)) + off;
+                d[0] = widen16<GT>(*reinterpret_cast<gptr<uint16_t>>(p));
+            }
         } else {
             const int n = ((ck.pmask >> j) & 1ull) ? static_cast<int>(gbytes) : 0;
             const __amdgpu_buffer_rsrc_t rs =
-                __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(gbase), 0, n, kBufferWord3);
+                __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(gbase), 0, n, kBufferWord3);
             // lanes past the row slice read its first column (voff), so every
             // address stays inside grad_out
-            d[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                rs, static_cast<int>(voff), static_cast<int>(rl(static_cast<uint32_t>(ck.addr), j)), 0));
+            const int soff = static_cast<int>(rl(static_cast<uint32_t>(ck.addr), j));
+            if constexpr (GT == TBE_F32)
+                d[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<int>(voff), soff, 0));
+            else
+                d[0] = widen16<GT>(__builtin_amdgcn_raw_buffer_load_b16(rs, static_cast<int>(voff), soff, 0));
         }
     };
     float ring[U][1];
@@ -886,7 +905,7 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
             acc[0] = __builtin_fmaf(w, ring[s][0], acc[0]);
             if ((cur.fmask >> j) & 1ull) {
                 const uint64_t dst = rl64(cur.dst, j);
-                if (vact) store_cols<1>(dst, voff, acc);
+                if (vact) store_cols<1>(dst, doff, acc);
                 acc[0] = 0.f;
             }
             const int a = j + U;
@@ -968,10 +987,10 @@ __device__ inline int find_work_table(const Range *__restrict__ r, int T, int64_
 // One workgroup per work item (table, column slice, tile), slice-major within
 // a table, numbered so that each XCD takes a contiguous run of work items:
 // the waves of one XCD then share one table slice of grad_out in their L2.
-template <typename V>
+template <typename V, int GT>
 __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__restrict__ keys,
                                                           const V *__restrict__ vals,
-                                                          const float *__restrict__ grad_out,
+                                                          const void *__restrict__ grad_out,
                                                           const TableMeta *__restrict__ meta,
                                                           const Range *__restrict__ ranges, int T,
                                                           const Ctl *__restrict__ ctl,
@@ -995,12 +1014,13 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
     const TableMeta m = meta[t];
     const TileSeg pre = tseg[tile];
     const TileEdges te = edges[tile];
-    if (gout_elems * 4 < kBufferLimit)
-        reduce_wave<V, false>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
-                              max_dim, tile, slice * kSliceCols, zero_page);
+    constexpr int GES = GT == TBE_F32 ? 4 : 2;
+    if (gout_elems * GES < kBufferLimit)
+        reduce_wave<V, false, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
+                                  max_dim, tile, slice * kSliceCols, zero_page);
     else
-        reduce_wave<V, true>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
-                             max_dim, tile, slice * kSliceCols, zero_page);
+        reduce_wave<V, true, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
+                                 max_dim, tile, slice * kSliceCols, zero_page);
 }
 
 // Sums the pieces of every segment that crosses a block edge, in a fixed
@@ -1139,7 +1159,7 @@ Layout layout(const Plan &p, int64_t N) {
 }
 
 template <typename V, typename IT>
-hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT *offsets,
+hipError_t run(const Plan &p, const void *grad_out, const IT *indices, const IT *offsets,
                int64_t N, const float *weights, char *ws, const Layout &L, float *grad_rows, int64_t capacity,
                int64_t *grad_idx, int64_t *seg_offsets, int64_t *grad_row_offsets, int64_t *num_unique,
                int32_t *status, hipStream_t stream, void *const *phase_events) {
@@ -1207,9 +1227,15 @@ hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT
     hipLaunchKernelGGL(edges_kernel, tiles, dim3(64), 0, stream, keys[cur], blk_starts, seg_offsets, ranges, T, ctl,
                        tseg, edges, head, tail);
     if ((me = mark(TBE_PHASE_REDUCE)) != hipSuccess) return me;
-    hipLaunchKernelGGL(reduce_kernel<V>, dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream, keys[cur],
-                       vals[cur], grad_out, p.meta_dev, ranges, T, ctl, tseg, edges, p.total_dim, p.B * p.total_dim,
-                       grad_rows, partials, p.max_dim, static_cast<const float *>(p.zero_page));
+#define TBE_REDUCE(GT)                                                                                        \
+    hipLaunchKernelGGL((reduce_kernel<V, GT>), dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream, keys[cur], \
+                       vals[cur], grad_out, p.meta_dev, ranges, T, ctl, tseg, edges, p.total_dim, p.B * p.total_dim,  \
+                       grad_rows, partials, p.max_dim, static_cast<const float *>(p.zero_page))
+    // grad_out has the forward output's element type
+    if (p.out_dtype == TBE_F16) TBE_REDUCE(TBE_F16);
+    else if (p.out_dtype == TBE_BF16) TBE_REDUCE(TBE_BF16);
+    else TBE_REDUCE(TBE_F32);
+#undef TBE_REDUCE
     if ((me = mark(TBE_PHASE_COMBINE)) != hipSuccess) return me;
     // one wave per run of 64 blocks, at most kCombineGroups workgroups
     const int64_t runs = (L.max_blocks + 63) / 64;
@@ -1225,7 +1251,7 @@ hipError_t run(const Plan &p, const float *grad_out, const IT *indices, const IT
 
 size_t backward_workspace_bytes(const Plan &p, int64_t num_indices) { return layout(p, num_indices).total; }
 
-hipError_t launch_backward(const Plan &p, const float *grad_out, const void *indices, const void *offsets,
+hipError_t launch_backward(const Plan &p, const void *grad_out, const void *indices, const void *offsets,
                            int64_t num_indices, const float *weights, void *workspace, size_t workspace_bytes,
                            float *grad_rows, int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                            int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, hipStream_t stream,

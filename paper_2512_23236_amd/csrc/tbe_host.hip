@@ -226,7 +226,7 @@ int32_t tbe_map_ids(const int64_t *values, int64_t num_values, const int64_t *ma
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
 }
 
-int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const float *grad_out, const void *indices,
+int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const void *grad_out, const void *indices,
                         const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                         void *stream) {
     const tbe::Plan *p = plan_of(plan);
@@ -255,7 +255,7 @@ int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, 
     return TBE_OK;
 }
 
-int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const void *indices,
+int32_t tbe_backward(const tbe_plan *plan, const void *grad_out, const void *indices,
                      const void *offsets, int64_t num_indices, const float *per_sample_weights,
                      void *workspace, size_t workspace_bytes, float *grad_rows,
                      int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
@@ -265,7 +265,7 @@ int32_t tbe_backward(const tbe_plan *plan, const float *grad_out, const void *in
                               grad_row_offsets, num_unique, status, stream, nullptr);
 }
 
-int32_t tbe_backward_timed(const tbe_plan *plan, const float *grad_out, const void *indices,
+int32_t tbe_backward_timed(const tbe_plan *plan, const void *grad_out, const void *indices,
                            const void *offsets, int64_t num_indices, const float *per_sample_weights,
                            void *workspace, size_t workspace_bytes, float *grad_rows,
                            int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,

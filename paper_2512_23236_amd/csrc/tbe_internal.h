@@ -64,13 +64,13 @@ hipError_t launch_map_ids(const int64_t *values, int64_t n, const int64_t *mappi
                           hipStream_t stream);
 
 // Gradient with respect to the per-sample weights.
-hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const void *indices,
+hipError_t launch_weight_grad(const Plan &p, const void *tables, const void *grad_out, const void *indices,
                               const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                               hipStream_t stream);
 
 // Backward: workspace size and the full sort + segmented-reduce pipeline.
 size_t backward_workspace_bytes(const Plan &p, int64_t num_indices);
-hipError_t launch_backward(const Plan &p, const float *grad_out, const void *indices,
+hipError_t launch_backward(const Plan &p, const void *grad_out, const void *indices,
                            const void *offsets, int64_t num_indices, const float *weights,
                            void *workspace, size_t workspace_bytes, float *grad_rows,
                            int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,

@@ -58,10 +58,22 @@ struct Wide<TBE_BF16> {
     }
 };
 
-template <int DT, typename IT>
+// grad_out element e as fp32 (fp16 / bf16 widened exactly).
+template <int GT>
+__device__ inline float grad_elem(const void *__restrict__ g, int64_t e) {
+    if constexpr (GT == TBE_F32) {
+        return static_cast<const float *>(g)[e];
+    } else {
+        const uint16_t h = static_cast<const uint16_t *>(g)[e];
+        if constexpr (GT == TBE_F16) return static_cast<float>(__builtin_bit_cast(_Float16, h));
+        else return __uint_as_float(static_cast<uint32_t>(h) << 16);
+    }
+}
+
+template <int DT, typename IT, int GT>
 __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
     const TableMeta *__restrict__ meta, const char *__restrict__ tables, const IT *__restrict__ indices,
-    const IT *__restrict__ offsets, const float *__restrict__ grad_out, float *__restrict__ grad_w,
+    const IT *__restrict__ offsets, const void *__restrict__ grad_out, float *__restrict__ grad_w,
     int32_t *status, int64_t B, int64_t nbags, int64_t N, int64_t total_dim, int check,
     const char *__restrict__ zero_page) {
     constexpr int KV = Wide<DT>::kPerVec;
@@ -87,13 +99,13 @@ __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
     const int g = lane >> lpr_log2, v = lane & (LPR - 1);
     const int64_t row_bytes = static_cast<int64_t>(m.nvec) * 16;
     const char *tab = tables + m.elem_offset * ES;
-    const float *grow = grad_out + b * total_dim + m.dim_off;
+    const int64_t grow = b * total_dim + m.dim_off;  // first grad_out element of the bag's slice
     bool oob = false;
     for (int c0 = 0; c0 < m.nvec; c0 += LPR) {  // chunks of 64 vectors (one chunk unless D is large)
         const bool vact = c0 + v < m.nvec;
         float gc[KV];
 #pragma unroll
-        for (int i = 0; i < KV; ++i) gc[i] = vact ? grow[(c0 + v) * KV + i] : 0.f;
+        for (int i = 0; i < KV; ++i) gc[i] = vact ? grad_elem<GT>(grad_out, grow + (c0 + v) * KV + i) : 0.f;
         for (int64_t base = s; base < e; base += 64) {
             const int cnt = e - base < 64 ? static_cast<int>(e - base) : 64;
             const int64_t my_idx = lane < cnt ? static_cast<int64_t>(indices[base + lane]) : 0;
@@ -131,7 +143,7 @@ __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
 
 }  // namespace
 
-hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *grad_out, const void *indices,
+hipError_t launch_weight_grad(const Plan &p, const void *tables, const void *grad_out, const void *indices,
                               const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                               hipStream_t stream) {
     const int64_t nbags = static_cast<int64_t>(p.T) * p.B;
@@ -139,10 +151,16 @@ hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *gr
     const dim3 grid(static_cast<unsigned>((nbags + kWgWaves - 1) / kWgWaves)), block(64 * kWgWaves);
     const char *tb = static_cast<const char *>(tables);
     const char *zp = static_cast<const char *>(p.zero_page);
-#define TBE_LAUNCH_IT(DT, IT)                                                                                 \
-    hipLaunchKernelGGL((weight_grad_kernel<DT, IT>), grid, block, 0, stream, p.meta_dev, tb,                   \
+#define TBE_LAUNCH_G(DT, IT, GT)                                                                              \
+    hipLaunchKernelGGL((weight_grad_kernel<DT, IT, GT>), grid, block, 0, stream, p.meta_dev, tb,               \
                        static_cast<const IT *>(indices), static_cast<const IT *>(offsets), grad_out, grad_weights, \
                        status, p.B, nbags, num_indices, p.total_dim, p.bounds_check, zp)
+#define TBE_LAUNCH_IT(DT, IT)                                                                                 \
+    do {                                                                                                      \
+        if (p.out_dtype == TBE_F16) TBE_LAUNCH_G(DT, IT, TBE_F16);                                            \
+        else if (p.out_dtype == TBE_BF16) TBE_LAUNCH_G(DT, IT, TBE_BF16);                                     \
+        else TBE_LAUNCH_G(DT, IT, TBE_F32);                                                                   \
+    } while (0)
 #define TBE_LAUNCH(DT)                                                                                        \
     do {                                                                                                      \
         if (p.index_type == TBE_INDEX_I32) TBE_LAUNCH_IT(DT, int32_t); else TBE_LAUNCH_IT(DT, int64_t);       \
@@ -154,6 +172,7 @@ hipError_t launch_weight_grad(const Plan &p, const void *tables, const float *gr
     }
 #undef TBE_LAUNCH
 #undef TBE_LAUNCH_IT
+#undef TBE_LAUNCH_G
     return hipGetLastError();
 }
 

@@ -249,10 +249,11 @@ def map_ids(values: torch.Tensor, mapping: torch.Tensor, out: Optional[torch.Ten
 def weight_grad(plan: Plan, tables: torch.Tensor, grad_out: torch.Tensor, indices: torch.Tensor,
                 offsets: torch.Tensor, out: Optional[torch.Tensor] = None,
                 status: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Gradient with respect to the per-sample weights: fp32 [N] (queued on the current stream)."""
+    """Gradient with respect to the per-sample weights: fp32 [N] (queued on the current stream).
+    grad_out has the plan's out_dtype."""
     N = indices.numel()
     _dev_tensor(tables, plan.dtype, "tables", plan)
-    _dev_tensor(grad_out, torch.float32, "grad_out", plan)
+    _dev_tensor(grad_out, plan.out_dtype, "grad_out", plan)
     _dev_tensor(indices, plan.index_dtype, "indices", plan)
     _dev_tensor(offsets, plan.index_dtype, "offsets", plan)
     if grad_out.numel() != plan.B * plan.total_dim:
@@ -308,7 +309,7 @@ def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets:
     phase_events: NUM_PHASES + 1 events recorded at the phase boundaries of
     the backward (tbe_backward_timed); event i .. i+1 brackets phase i."""
     N = indices.numel()
-    _dev_tensor(grad_out, torch.float32, "grad_out", plan)
+    _dev_tensor(grad_out, plan.out_dtype, "grad_out", plan)  # the gradient of out has out's type
     _dev_tensor(indices, plan.index_dtype, "indices", plan)
     _dev_tensor(offsets, plan.index_dtype, "offsets", plan)
     if grad_out.numel() != plan.B * plan.total_dim:

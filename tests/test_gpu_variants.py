@@ -162,7 +162,7 @@ def test_full_size_cfg3_variants_sampled():
 # ------------------------------------------------------------------ backward
 
 
-def backward(spec, d, **kw):
+def backward(spec, d, **kw):  # kw: make_plan options
     plan = make_plan(spec, **kw)
     st = torch.zeros(1, dtype=torch.int32, device=device())
     g = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], d.get("weights"), status=st)
@@ -206,6 +206,30 @@ def test_int32_backward_equals_int64(k):
     check_backward(spec, d32, b, "sum")
 
 
+@pytest.mark.parametrize("gdt", ["f16", "bf16"])
+@pytest.mark.parametrize("weighted", [False, True])
+def test_reduced_precision_grad_out(gdt, weighted):
+    """With a 16-bit output the gradient of the output is 16-bit too; its
+    values widen exactly, so the oracle gets them as fp32."""
+    spec = small(k=4 if weighted else 5, seed=7, T=4, B=300, grad=True, name=f"grad-{gdt}")
+    d = inputs(spec)
+    d["grad_out"] = d["grad_out"].to(OUT_TORCH[gdt])
+    g = backward(spec, d, out=gdt)
+    check_backward(spec, dict(d, grad_out=d["grad_out"].float()), g, "sum")
+
+
+def test_reduced_precision_grad_out_past_2gib():
+    """16-bit grad_out of more than 2 GiB (rows addressed with 64-bit pointers
+    instead of 32-bit buffer offsets): one-hot bags over two wide tables."""
+    base = workloads.small_config(2, seed=17, T=2, B=440000)
+    spec = dataclasses.replace(base, dims=np.array([1536, 1024], np.int32), grad=True, name="grad-bf16-wide")
+    assert spec.B * int(spec.dims.sum()) * 2 >= 2 ** 31
+    d = inputs(spec)
+    d["grad_out"] = d["grad_out"].to(torch.bfloat16)
+    g = backward(spec, d, out="bf16")
+    check_backward(spec, dict(d, grad_out=d["grad_out"].float()), g, "sum")
+
+
 def test_backward_with_u8_tables():
     """The gradient never reads the tables: an 8-bit row-wise plan gives the
     same sparse gradient as an fp16 plan of the same shapes."""
@@ -218,6 +242,21 @@ def test_backward_with_u8_tables():
 
 
 # ------------------------------------------------------------------ weight gradient
+
+
+@pytest.mark.parametrize("gdt", ["f16", "bf16"])
+def test_weight_grad_reduced_precision_grad_out(gdt):
+    spec = small(k=4, seed=9, T=3, B=120, grad=True, name=f"wgrad-{gdt}")
+    d = inputs(spec)
+    g16 = d["grad_out"].to(OUT_TORCH[gdt])
+    st = torch.zeros(1, dtype=torch.int32, device=device())
+    gw = tbe.weight_grad(make_plan(spec, out=gdt), d["tables"], g16, d["indices"], d["offsets"], status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    ref, ab = oracle.weight_grad(spec.rows, spec.dims, spec.dtype, raw_tables(spec, d["tables"].cpu()),
+                                 d["indices"].cpu().numpy(), d["offsets"].cpu().numpy(), spec.B,
+                                 g16.float().cpu().numpy())
+    assert oracle.summation_error(gw.cpu().numpy(), ref, ab).max() <= RTOL[spec.dtype]
 
 
 def test_int32_weight_grad_equals_int64():
