@@ -327,6 +327,9 @@ def main():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--flushed-steps", type=int, default=5,
+                    help="extra steps, each after writing 1 GiB to evict L2 and the Infinity Cache, reported "
+                         "as the secondary (cold-cache) timing; 0 skips them")
     ap.add_argument("--op", default="step", choices=["step", "weight_grad", "map_ids", "sgd", "adagrad"],
                     help="step: forward (+ backward for cfg5), the default; weight_grad: the per-sample-weight "
                          "gradient alone (use --config 4); map_ids: the MapId preprocessing step at the "
@@ -485,6 +488,24 @@ def main():
     dominant = max(roof.values(), key=lambda r: r["ms"])
     res["roofline"] = dominant
     res["roofline_forward"] = roof["forward_kernel"]
+    if args.flushed_steps > 0:
+        # secondary timing: every step starts with cold caches (1 GiB written
+        # first, outside the timed events)
+        junk = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        fl = []
+        for i in range(args.flushed_steps):
+            junk.fill_(float(i))
+            ev = tuple(torch.cuda.Event(enable_timing=True) for _ in range(nev))
+            step(ev)
+            torch.cuda.synchronize()
+            fl.append((ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[-1]) if training else 0.0))
+        del junk
+        fw = [x[0] for x in fl]
+        res["flushed"] = {"steps": args.flushed_steps, "forward_ms": float(np.median(fw)),
+                          "forward_frac_of_hbm_peak": fbytes / (float(np.median(fw)) * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        if training:
+            res["flushed"]["backward_ms"] = float(np.median([x[1] for x in fl]))
+            res["flushed"]["step_ms"] = float(np.median([x[0] + x[1] for x in fl]))
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())}")
     if not args.no_cpu_baseline:
