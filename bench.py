@@ -346,8 +346,8 @@ def main():
                     help="only copy a device buffer of this size 3 times (calibrates the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU table-wise "
-              "sharding is a design, not part of this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the table-wise sharding over "
+              "several GPUs exists as a design, not as code", file=sys.stderr)
         sys.exit(2)
 
     dev = torch.device("cuda", 0)

@@ -103,6 +103,20 @@ def lib():
     return _load()
 
 
+STATUS_NAMES = {STATUS_INDEX_OOB: "index out of range", STATUS_OFFSETS: "malformed offsets",
+                STATUS_CAPACITY: "grad_rows capacity too small"}
+
+
+def check_status(status: torch.Tensor) -> None:
+    """Waits for the status word's stream work and raises if the device set
+    any TBE_STATUS_* bit (an out-of-range index, malformed offsets, too small
+    a gradient capacity)."""
+    bits = int(status.item())  # synchronises with the work that wrote it
+    if bits:
+        names = [n for b, n in STATUS_NAMES.items() if bits & b]
+        raise RuntimeError(f"device status {bits}: " + ", ".join(names))
+
+
 def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
