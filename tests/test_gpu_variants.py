@@ -128,6 +128,8 @@ def test_mean_counts_dropped_lookups():
     out = tbe.forward(plan, d["tables"], bad, d["offsets"], status=st)
     torch.cuda.synchronize()
     assert int(st.item()) == tbe.STATUS_INDEX_OOB
+    with pytest.raises(RuntimeError, match="index out of range"):
+        tbe.check_status(st)
     tab = raw_tables(spec, d["tables"].cpu())[t]
     ref, ab = oracle.forward([int(spec.rows[t])], [int(spec.dims[t])], "f32", [tab],
                              d["indices"][s + 1:e].cpu().numpy(), [0, e - s - 1], 1)
@@ -299,3 +301,22 @@ def test_unsupported_combinations_rejected():
         tbe.apply_gradient(make_plan(u8spec), u8, g, tbe.SGD, 0.1)
     assert e.value.code == -8
     torch.cuda.synchronize()
+
+
+def test_unchecked_plans_match_checked():
+    """On valid inputs a plan without bounds checking (status may be NULL)
+    gives the same bits as a checking plan: forward and backward, with the
+    variants combined."""
+    spec = small(k=5, seed=10, T=4, B=250, dtype="u8", name="unchecked")
+    d = inputs(spec, "i32")
+    outs, grads = [], []
+    for check in (True, False):
+        plan = make_plan(spec, pooling="mean", index="i32", out="bf16", bounds_check=check)
+        st = torch.zeros(1, dtype=torch.int32, device=device()) if check else None
+        outs.append(tbe.forward(plan, d["tables"], d["indices"], d["offsets"], status=st))
+        gplan = make_plan(spec, pooling="mean", index="i32", bounds_check=check)
+        grads.append(tbe.backward(gplan, d["grad_out"], d["indices"], d["offsets"], status=st))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+    for x, y in zip(grads[0].trimmed(), grads[1].trimmed()):
+        assert torch.equal(x, y)
