@@ -61,8 +61,7 @@ struct Ctl {
     int32_t skip_rows;   // grad_rows too small: write no gradient row
     int64_t total_tiles;
     int64_t total_works;  // reduce work items: (table, column slice, tile)
-    uint64_t spare;
-    int64_t pad[4];
+    int64_t pad[5];
 };
 
 // Per-table lookup range in the sorted order, its first tile and its first
@@ -210,7 +209,6 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const IT *__restrict__ 
         ctl->skip_rows = 0;
         ctl->total_tiles = bad ? 0 : carry;
         ctl->total_works = bad ? 0 : wcarry;
-        ctl->spare = 0;
         if (bad) atomicOr(status, TBE_STATUS_OFFSETS);
     }
 }
