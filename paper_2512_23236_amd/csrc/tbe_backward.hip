@@ -45,7 +45,10 @@ constexpr int kTile = kThreads * kItems;      // positions per tile
 constexpr int kBlk = 128;                     // positions per reduce block
 constexpr int kBlksPerTile = kTile / kBlk;    // 32
 constexpr int kBlksPerWave = kBlksPerTile / kWaves;  // one wave's contiguous range in the reduce
-constexpr int kSliceCols = 64;                // gradient columns per reduce work item (one per lane)
+// Gradient columns per reduce work item: 256 bytes of a grad_out row, so 64
+// fp32 columns (one per lane) or 128 fp16 / bf16 columns (two per lane).
+constexpr int kSliceBytes = 256;
+__host__ __device__ constexpr int slice_cols(int grad_dtype) { return kSliceBytes / (grad_dtype == TBE_F32 ? 4 : 2); }
 static_assert(kBlk == 128 && kBlksPerTile <= 62, "reduce block indexing");
 constexpr int kRadixBits = 8;
 constexpr int kBuckets = 1 << kRadixBits;
@@ -165,7 +168,7 @@ __device__ inline uint64_t match_digit(uint32_t d, bool valid, int nbits) {
 // ------------------------------------------------------------------ setup
 
 template <typename IT>
-__global__ __launch_bounds__(kThreads) void setup_kernel(const IT *__restrict__ offsets,
+__global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__restrict__ offsets,
                                                          const TableMeta *__restrict__ meta, int T, int64_t B,
                                                          int64_t N, int check, Ctl *ctl, Range *ranges,
                                                          int32_t *status, int64_t *num_unique,
@@ -193,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(const IT *__restrict__ 
                 s = e = 0;
             }
             nt = (e - s + kTile - 1) / kTile;
-            nw = nt * ((meta[t].dim + kSliceCols - 1) / kSliceCols);
+            nw = nt * ((meta[t].dim + scols - 1) / scols);
         }
         int64_t tot, wtot;
         const int64_t ex = block_excl_scan<int64_t>(nt, lds, &tot);
@@ -745,14 +748,14 @@ struct TileEdges {
 };
 static_assert(sizeof(TileEdges) % 16 == 0, "TileEdges layout");
 
-constexpr int kRing = 64;  // row loads in flight per reduce wave
+constexpr int kRing = 64;  // row loads in flight per reduce wave (one column per lane; half with two)
 // Buffer resources: byte offsets below kBufferLimit; word 3 of an untyped
 // 32-bit-element resource.
 constexpr int64_t kBufferLimit = int64_t(1) << 31;
 constexpr int kBufferWord3 = 0x00020000;
 
 // One wave walks one contiguous range of positions (kBlksPerWave blocks) in
-// order for one slice of kSliceCols gradient columns, one position per step
+// order for one slice of slice_cols(GT) gradient columns, one position per step
 // with the whole wave on that position's slice (one column per lane).
 // Per-position metadata (row address, destination address, weight, flush
 // flag) is prepared by one lane per position, 64 positions at a time, one
@@ -767,7 +770,8 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
                                    int64_t gout_elems, float *__restrict__ grad_rows,
                                    float *__restrict__ partials, int max_dim, int64_t tile, int c0,
                                    const float *__restrict__ zero_page) {
-    constexpr int U = kRing;
+    constexpr int NC = GT == TBE_F32 ? 1 : 2;  // columns per lane: a 256-byte slice of a grad_out row
+    constexpr int U = kRing / NC;              // same registers for the ring either way
     constexpr bool kWeighted = sizeof(V) == 8;
     const int lane = threadIdx.x & 63;
     const int wave = static_cast<int>(uni(threadIdx.x >> 6));
@@ -787,10 +791,10 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     const int64_t part0 = 2 * (tile * kBlksPerTile) * max_dim;
 
     constexpr int GES = GT == TBE_F32 ? 4 : 2;  // bytes per grad_out element
-    const int col = c0 + lane;
+    const int col = c0 + NC * lane;  // this lane's first column (row widths are even)
     const bool vact = col < m.dim;
-    const uint32_t voff = vact ? static_cast<uint32_t>(lane * GES) : 0u;  // bytes into a grad_out row
-    const uint32_t doff = static_cast<uint32_t>(lane * 4);                // bytes into an fp32 gradient row
+    const uint32_t voff = vact ? static_cast<uint32_t>(lane * NC * GES) : 0u;  // bytes into a grad_out row
+    const uint32_t doff = static_cast<uint32_t>(lane * NC * 4);                // bytes into an fp32 gradient row
     const char *const gbase = static_cast<const char *>(grad_out) + (m.dim_off + c0) * GES;
     // grad_out below 2 GiB: rows are 32-bit byte offsets from gbase into a
     // buffer resource; a step whose position is not owned reads through a
@@ -866,8 +870,9 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     cook(r0 + 64, far, nxt);
     load_raw(r0 + 128, far);
 
-    // one gradient column of the row slice of step j of a chunk
-    auto fetch = [&](const Cooked &ck, int j, float (&d)[1]) {
+    // this lane's NC gradient columns of the row slice of step j of a chunk
+    // (fp32: one column; fp16 / bf16: two, from one 32-bit load)
+    auto fetch = [&](const Cooked &ck, int j, float (&d)[NC]) {
         if constexpr (kWide) {
             if constexpr (GT == TBE_F32) {
                 load_cols<1>(rl64(ck.addr, j), voff, d);
@@ -875,36 +880,45 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
                 uint32_t off = voff;
                 asm volatile("" : "+v"(off));
                 const gptr<char> p = reinterpret_cast<gptr<char>>(rl64(ck.addr, j)) + off;
-                d[0] = widen16<GT>(*reinterpret_cast<gptr<uint16_t>>(p));
+                const uint32_t h = *reinterpret_cast<gptr<uint32_t>>(p);
+                d[0] = widen16<GT>(h & 0xffffu);
+                d[1] = widen16<GT>(h >> 16);
             }
         } else {
             const int n = ((ck.pmask >> j) & 1ull) ? static_cast<int>(gbytes) : 0;
             const __amdgpu_buffer_rsrc_t rs =
                 __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(gbase), 0, n, kBufferWord3);
-            // lanes past the row slice read its first column (voff), so every
+            // lanes past the row slice read its first columns (voff), so every
             // address stays inside grad_out
             const int soff = static_cast<int>(rl(static_cast<uint32_t>(ck.addr), j));
-            if constexpr (GT == TBE_F32)
-                d[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<int>(voff), soff, 0));
-            else
-                d[0] = widen16<GT>(__builtin_amdgcn_raw_buffer_load_b16(rs, static_cast<int>(voff), soff, 0));
+            const uint32_t h = __builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<int>(voff), soff, 0);
+            if constexpr (GT == TBE_F32) {
+                d[0] = __uint_as_float(h);
+            } else {
+                d[0] = widen16<GT>(h & 0xffffu);
+                d[1] = widen16<GT>(h >> 16);
+            }
         }
     };
-    float ring[U][1];
+    float ring[U][NC];
 #pragma unroll
     for (int s = 0; s < U; ++s) fetch(cur, s, ring[s]);
 
-    float acc[1] = {0.f};
+    float acc[NC];
+#pragma unroll
+    for (int q = 0; q < NC; ++q) acc[q] = 0.f;
     for (int64_t c = r0;; c += 64) {
 #pragma unroll
         for (int j = 0; j < 64; ++j) {
             const int s = j % U;
             const float w = kWeighted ? __int_as_float(static_cast<int>(rl(__float_as_uint(cur.w), j))) : 1.0f;
-            acc[0] = __builtin_fmaf(w, ring[s][0], acc[0]);
+#pragma unroll
+            for (int q = 0; q < NC; ++q) acc[q] = __builtin_fmaf(w, ring[s][q], acc[q]);
             if ((cur.fmask >> j) & 1ull) {
                 const uint64_t dst = rl64(cur.dst, j);
-                if (vact) store_cols<1>(dst, doff, acc);
-                acc[0] = 0.f;
+                if (vact) store_cols<NC>(dst, doff, acc);
+#pragma unroll
+                for (int q = 0; q < NC; ++q) acc[q] = 0.f;
             }
             const int a = j + U;
             if (a < 64) fetch(cur, a, ring[s]);
@@ -1015,10 +1029,10 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
     constexpr int GES = GT == TBE_F32 ? 4 : 2;
     if (gout_elems * GES < kBufferLimit)
         reduce_wave<V, false, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
-                                  max_dim, tile, slice * kSliceCols, zero_page);
+                                  max_dim, tile, slice * slice_cols(GT), zero_page);
     else
         reduce_wave<V, true, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
-                                 max_dim, tile, slice * kSliceCols, zero_page);
+                                 max_dim, tile, slice * slice_cols(GT), zero_page);
 }
 
 // Sums the pieces of every segment that crosses a block edge, in a fixed
@@ -1131,7 +1145,7 @@ Layout layout(const Plan &p, int64_t N) {
     const size_t vb = 8;  // room for weighted values; unweighted calls use half
     L.max_tiles = (N + kTile - 1) / kTile + p.T;
     L.max_blocks = L.max_tiles * kBlksPerTile;
-    L.max_works = L.max_tiles * ((p.max_dim + kSliceCols - 1) / kSliceCols);
+    L.max_works = L.max_tiles * ((p.max_dim + slice_cols(p.out_dtype) - 1) / slice_cols(p.out_dtype));
     size_t o = 0;
     auto take = [&](size_t bytes) {
         const size_t at = o;
@@ -1188,7 +1202,8 @@ hipError_t run(const Plan &p, const void *grad_out, const IT *indices, const IT 
     hipError_t me = mark(TBE_PHASE_KEYS);
     if (me != hipSuccess) return me;
 
-    hipLaunchKernelGGL(setup_kernel<IT>, dim3(1), dim3(kThreads), 0, stream, offsets, p.meta_dev, T, p.B, N, check, ctl,
+    hipLaunchKernelGGL(setup_kernel<IT>, dim3(1), dim3(kThreads), 0, stream, slice_cols(p.out_dtype), offsets,
+                       p.meta_dev, T, p.B, N, check, ctl,
                        ranges, status, num_unique, seg_offsets, grad_row_offsets);
     if (N == 0 || nbags == 0) {
         const hipError_t e = hipGetLastError();
