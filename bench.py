@@ -114,10 +114,12 @@ def measured_traffic(kernel: str, workload: str):
         return None
 
 
-def cpu_baseline(spec, d, target_s: float, pooling: str = "sum"):
+def cpu_baseline(spec, d, target_s: float, pooling: str = "sum", training: bool = False):
     """The CPU oracle on a bounded sample: the first b_s bags of every table,
     their rows copied into compact host tables; b_s is sized so the oracle
-    runs for roughly target_s seconds."""
+    runs for roughly target_s seconds.  With training, the sample's backward
+    (sort and segments, then the gradient rows against grad_out's first b_s
+    rows) is timed with its forward, as the GPU step does both."""
     import oracle
 
     off = d["offsets"].cpu().numpy()
@@ -146,8 +148,12 @@ def cpu_baseline(spec, d, target_s: float, pooling: str = "sum"):
 
     def run(bs):
         tabs, rows, indices, offsets, w = sample(bs)
+        g = d["grad_out"][:bs].float().cpu().numpy() if training else None
         t0 = time.perf_counter()
         oracle.forward(rows, spec.dims, spec.dtype, tabs, indices, offsets, bs, w, pooling=pooling)
+        if training:
+            seg = oracle.backward_segments(rows, spec.dims, indices, offsets, bs)
+            oracle.backward_rows(rows, spec.dims, offsets, bs, g, seg, w, pooling=pooling)
         return time.perf_counter() - t0, indices.size
 
     bs = max(1, min(spec.B, 64))
@@ -156,8 +162,10 @@ def cpu_baseline(spec, d, target_s: float, pooling: str = "sum"):
         bs = min(spec.B, int(bs * max(2.0, min(16.0, target_s / max(dt, 1e-3) * 0.8))))
         dt, n = run(bs)
     return {"value": n / dt, "unit": "lookups/s", "cores": threads, "kind": "oracle",
-            "sample": f"forward over the first {bs} bags of each of the {spec.T} tables "
-                      f"({n} lookups, {dt:.1f} s, binary64, OpenMP over bags)"}
+            "sample": (f"forward + backward (sort single-threaded; forward and gradient rows OpenMP) "
+                       if training else "forward (OpenMP over bags) ")
+                      + f"over the first {bs} bags of each of the {spec.T} tables ({n} lookups, {dt:.1f} s, "
+                        f"binary64)"}
 
 
 def weight_grad_bytes(spec, offsets_host: np.ndarray) -> int:
@@ -510,7 +518,7 @@ def main():
         raise RuntimeError(f"device status {int(status.item())}")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
-        res["cpu_baseline"] = cpu_baseline(spec, d, args.cpu_seconds, args.pooling)
+        res["cpu_baseline"] = cpu_baseline(spec, d, args.cpu_seconds, args.pooling, training)
     print(json.dumps(res), flush=True)
 
 

@@ -50,7 +50,6 @@ constexpr int kBlksPerWave = kBlksPerTile / kWaves;  // one wave's contiguous ra
 constexpr int kSliceBytes = 256;
 __host__ __device__ constexpr int slice_cols(int grad_dtype) { return kSliceBytes / (grad_dtype == TBE_F32 ? 4 : 2); }
 static_assert(kBlk == 128 && kBlksPerTile <= 62, "reduce block indexing");
-constexpr int kRadixBits = 8;
 constexpr int kBuckets = 1 << kRadixBits;
 constexpr uint32_t kSentinel = 0xffffffffu;
 constexpr int kPairLevels = 12;               // pairwise-sum depth in combine
@@ -223,7 +222,9 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__
 // order, 256 at a time (coalesced loads and stores), and find each lookup's
 // bag by binary search over the staged offsets.  With 64-bit values the
 // weight rides along: the per-sample weight, or fl32(1/L) under mean pooling
-// (L = the bag's lookup count, read from the staged offsets).
+// (L = the bag's lookup count, read from the staged offsets).  A table's keys
+// go to the buffer from which its own sort_passes radix passes end in buffer
+// passes & 1, where every table's sorted keys then lie.
 template <typename V, typename IT>
 __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restrict__ meta,
                                                         const IT *__restrict__ indices,
@@ -231,11 +232,13 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
                                                         const float *__restrict__ weights, int mean,
                                                         const Range *__restrict__ ranges, int64_t B,
                                                         int64_t nbags, int check, Ctl *ctl,
-                                                        uint32_t *__restrict__ keys, V *__restrict__ vals,
+                                                        uint32_t *__restrict__ keys0, uint32_t *__restrict__ keys1,
+                                                        V *__restrict__ vals0, V *__restrict__ vals1, int passes,
                                                         int32_t *status) {
     __shared__ int64_t off[kKeyBags + 1];
     __shared__ int64_t bag_rows[kKeyBags];  // R_t of each bag's table
     __shared__ uint32_t bag_b[kKeyBags];    // batch row of each bag
+    __shared__ uint8_t bag_buf[kKeyBags];   // buffer the bag's table starts its sort in
     __shared__ int bad;
     const int tid = threadIdx.x;
     const int64_t k0 = static_cast<int64_t>(blockIdx.x) * kKeyBags;
@@ -248,6 +251,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         const int64_t t = (k0 + i) / B;
         bag_b[i] = static_cast<uint32_t>(k0 + i - t * B);
         bag_rows[i] = meta[t].rows;
+        bag_buf[i] = static_cast<uint8_t>((passes - meta[t].sort_passes) & 1);
     }
     __syncthreads();
     if (check) {
@@ -281,6 +285,9 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
             key = kSentinel;
             atomicOr(status, TBE_STATUS_INDEX_OOB);
         }
+        const bool second = bag_buf[lo] != 0;
+        uint32_t *const keys = second ? keys1 : keys0;
+        V *const vals = second ? vals1 : vals0;
         keys[j] = key;
         if constexpr (sizeof(V) == 8) {
             const float w = mean ? 1.0f / static_cast<float>(off[lo + 1] - off[lo]) : weights[j];
@@ -293,10 +300,19 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
 
 // ------------------------------------------------------------ radix sort
 
-__global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__restrict__ keys,
+// Pass `pass` of `passes` reads table t's keys from buffer
+// (pass + passes - sort_passes_t) & 1; a table whose keys are already sorted
+// (pass >= sort_passes_t) takes no part.
+__device__ inline int sort_src(const TableMeta &m, int pass, int passes) {
+    return pass < m.sort_passes ? (pass + passes - m.sort_passes) & 1 : -1;
+}
+
+__global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__restrict__ keys0,
+                                                              const uint32_t *__restrict__ keys1,
+                                                              const TableMeta *__restrict__ meta,
                                                               const Range *__restrict__ ranges, int T,
-                                                              const Ctl *__restrict__ ctl, int shift, int nbits,
-                                                              uint32_t *__restrict__ hist) {
+                                                              const Ctl *__restrict__ ctl, int pass, int passes,
+                                                              int shift, int nbits, uint32_t *__restrict__ hist) {
     // counts only (order does not matter here): one LDS histogram per wave,
     // plain atomic increments, summed at the end
     __shared__ uint32_t cnt[kWaves][kBuckets];
@@ -304,6 +320,9 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__
     if (tile >= ctl->total_tiles || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
+    const int src = sort_src(meta[ti.t], pass, passes);
+    if (src < 0) return;
+    const uint32_t *__restrict__ keys = src ? keys1 : keys0;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) cnt[w][tid] = 0;
@@ -348,10 +367,12 @@ constexpr int kColAhead = 8;
 
 __global__ __launch_bounds__(kThreads) void col_scan_kernel(uint32_t *__restrict__ hist,
                                                             uint32_t *__restrict__ totals,
+                                                            const TableMeta *__restrict__ meta,
                                                             const Range *__restrict__ ranges,
-                                                            const Ctl *__restrict__ ctl) {
+                                                            const Ctl *__restrict__ ctl, int pass) {
     if (ctl->abort) return;
     const int t = blockIdx.x, d = threadIdx.x;
+    if (pass >= meta[t].sort_passes) return;
     const int64_t t0 = ranges[t].tile_base, t1 = ranges[t + 1].tile_base;
     uint32_t run = 0;
     for (int64_t c = t0; c < t1; c += kColAhead) {
@@ -369,9 +390,10 @@ __global__ __launch_bounds__(kThreads) void col_scan_kernel(uint32_t *__restrict
 
 template <typename V>
 __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
-    const uint32_t *__restrict__ keys_in, const V *__restrict__ vals_in, uint32_t *__restrict__ keys_out,
-    V *__restrict__ vals_out, const uint32_t *__restrict__ prefix, const uint32_t *__restrict__ totals,
-    const Range *__restrict__ ranges, int T, const Ctl *__restrict__ ctl, int shift, int nbits) {
+    uint32_t *__restrict__ keys0, uint32_t *__restrict__ keys1, V *__restrict__ vals0, V *__restrict__ vals1,
+    const uint32_t *__restrict__ prefix, const uint32_t *__restrict__ totals, const TableMeta *__restrict__ meta,
+    const Range *__restrict__ ranges, int T, const Ctl *__restrict__ ctl, int pass, int passes, int shift,
+    int nbits) {
     __shared__ uint32_t cnt[kWaves][kBuckets];  // per-wave digit counts, then wave offsets
     __shared__ uint32_t tstart[kBuckets];       // first tile-local slot of each digit
     __shared__ uint32_t goff[kBuckets];         // first global slot of each digit for this tile
@@ -383,6 +405,12 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     if (tile >= ctl->total_tiles || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
+    const int src = sort_src(meta[ti.t], pass, passes);
+    if (src < 0) return;
+    const uint32_t *__restrict__ keys_in = src ? keys1 : keys0;
+    const V *__restrict__ vals_in = src ? vals1 : vals0;
+    uint32_t *__restrict__ keys_out = src ? keys0 : keys1;
+    V *__restrict__ vals_out = src ? vals0 : vals1;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint32_t mask = (1u << nbits) - 1u;
 #pragma unroll
@@ -1210,26 +1238,28 @@ hipError_t run(const Plan &p, const void *grad_out, const IT *indices, const IT 
         return e != hipSuccess ? e : mark(TBE_NUM_PHASES);
     }
     const int mean = p.pooling == TBE_POOL_MEAN;
-    hipLaunchKernelGGL((keys_kernel<V, IT>), dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)),
-                       dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights, mean, ranges, p.B, nbags,
-                       check, ctl, keys[0], vals[0], status);
-    // bits: every valid local key, and the drop key's low bits above them
+    // bits: every valid local key of the largest table, and the drop key's
+    // low bits above them; a smaller table stops after its own sort_passes
     int64_t max_rows = 1;
     for (int t = 0; t < T; ++t) max_rows = p.meta_host[t].rows > max_rows ? p.meta_host[t].rows : max_rows;
-    int bits = 1;
-    while (bits < 32 && (int64_t(1) << bits) <= max_rows) ++bits;
+    const int bits = key_bits_for(max_rows);
+    const int passes = (bits + kRadixBits - 1) / kRadixBits;
+    hipLaunchKernelGGL((keys_kernel<V, IT>), dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)),
+                       dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights, mean, ranges, p.B, nbags,
+                       check, ctl, keys[0], keys[1], vals[0], vals[1], passes, status);
     const dim3 tiles(static_cast<unsigned>(L.max_tiles)), blk(kThreads);
     if ((me = mark(TBE_PHASE_SORT)) != hipSuccess) return me;
-    int cur = 0;
-    for (int shift = 0; shift < bits; shift += kRadixBits) {
+    for (int pass = 0; pass < passes; ++pass) {
+        const int shift = pass * kRadixBits;
         const int nb = bits - shift < kRadixBits ? bits - shift : kRadixBits;
-        hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, keys[cur], ranges, T, ctl, shift, nb, hist);
-        hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), blk, 0, stream, hist, totals, ranges,
-                           ctl);
-        hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, blk, 0, stream, keys[cur], vals[cur], keys[cur ^ 1],
-                           vals[cur ^ 1], hist, totals, ranges, T, ctl, shift, nb);
-        cur ^= 1;
+        hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, keys[0], keys[1], p.meta_dev, ranges, T, ctl,
+                           pass, passes, shift, nb, hist);
+        hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), blk, 0, stream, hist, totals, p.meta_dev,
+                           ranges, ctl, pass);
+        hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, blk, 0, stream, keys[0], keys[1], vals[0], vals[1], hist,
+                           totals, p.meta_dev, ranges, T, ctl, pass, passes, shift, nb);
     }
+    const int cur = passes & 1;  // every table's sorted keys and values
     if ((me = mark(TBE_PHASE_SEGMENTS)) != hipSuccess) return me;
     hipLaunchKernelGGL(seg_count_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
                        blk_starts);

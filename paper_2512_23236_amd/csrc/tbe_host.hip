@@ -125,7 +125,7 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
         m.unit_bags = tbe::bags_per_group(p.dtype) * (64 >> m.lpr_log2);
         m.unit_base = p.fwd_units;
         p.fwd_units += (p.B + m.unit_bags - 1) / m.unit_bags;
-        m.pad = 0;
+        m.sort_passes = tbe::sort_passes_for(R);
         packed += R * (u8 ? D + 16 : D);
         dim_off += D;
         row_base += R;

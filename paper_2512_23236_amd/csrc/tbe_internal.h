@@ -23,7 +23,8 @@ struct TableMeta {
     int32_t unit_bags;    // forward: bags per wave work unit (bags per lane group x groups per wave)
     int64_t unit_base;    // forward: work units of all tables before t
     int32_t row_bytes;    // bytes per stored row (8-bit row-wise: D_t codes + scale + bias)
-    int32_t pad;
+    int32_t sort_passes;  // backward: radix passes that sort the table's local keys (digits of
+                          // kRadixBits over the bits of R_t, the drop key's low bits above them)
 };
 static_assert(sizeof(TableMeta) == 64, "TableMeta layout");
 
@@ -88,6 +89,17 @@ __device__ inline int64_t xcd_remap(int64_t w, int64_t nwg, int num_xcd) {
 }
 
 constexpr int kNumXcd = 8;
+
+// Backward radix sort: bits per digit, and the passes that order local keys
+// below `rows` (the smallest bit count b with 2^b > rows, so every valid key
+// stays below the drop key's low b bits, in digits of kRadixBits).
+constexpr int kRadixBits = 8;
+inline int key_bits_for(int64_t rows) {
+    int b = 1;
+    while (b < 32 && (int64_t(1) << b) <= rows) ++b;
+    return b;
+}
+inline int sort_passes_for(int64_t rows) { return (key_bits_for(rows) + kRadixBits - 1) / kRadixBits; }
 
 // Forward work decomposition: each lane group of a wave streams through
 // kBagsPerGroup consecutive bags of one table (half as many for 8-bit row-wise

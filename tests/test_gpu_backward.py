@@ -142,6 +142,16 @@ def test_all_tables_one_row():
     check(spec)
 
 
+@pytest.mark.parametrize("k", [5, 4])
+def test_mixed_sort_passes(k):
+    # tables sorted in 1, 2 and 3 radix passes of 8 bits in one call (each
+    # table stops after the passes its row count needs), at the pass-count
+    # boundaries; k = 4 carries weights (64-bit sort values)
+    rows = np.array([3, 255, 256, 65535, 65536, 300000], np.int64)
+    base = workloads.small_config(k, seed=11, T=len(rows), B=700)
+    check(dataclasses.replace(base, rows=rows, name=f"bwd-passes-{k}"))
+
+
 def test_deterministic_repeat():
     spec = workloads.small_config(4, seed=8, T=3, B=400)
     d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
