@@ -55,6 +55,7 @@ constexpr uint32_t kSentinel = 0xffffffffu;
 constexpr int kPairLevels = 12;               // pairwise-sum depth in combine
 constexpr int kCombineGroups = 2048;          // combine grid (waves loop over runs of 64 blocks)
 constexpr int kKeyBags = 256;                 // bags per keys workgroup
+constexpr int kKeyAhead = 4;                  // keys kernel: lookup rounds whose loads are in flight together
 constexpr int kCombineBatch = 8;              // piece rows loaded at once in combine
 
 // Device control block at the start of the workspace.
@@ -272,28 +273,43 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         }
     }
     const int64_t first = off[0], last = off[nk];
-    for (int64_t j = first + tid; j < last; j += kThreads) {
-        int lo = 0, hi = nk;  // off[lo] <= j < off[hi]
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (off[mid] <= j) lo = mid; else hi = mid;
+    // kKeyAhead rounds of the run's lookups at a time: their index (and
+    // weight) loads are all issued before the first is used
+    for (int64_t j0 = first + tid; j0 < last; j0 += static_cast<int64_t>(kThreads) * kKeyAhead) {
+        int64_t ids[kKeyAhead];
+        float wts[kKeyAhead];
+#pragma unroll
+        for (int r = 0; r < kKeyAhead; ++r) {
+            const int64_t j = j0 + static_cast<int64_t>(r) * kThreads;
+            ids[r] = j < last ? static_cast<int64_t>(__builtin_nontemporal_load(indices + j)) : 0;
+            if constexpr (sizeof(V) == 8) wts[r] = (!mean && j < last) ? weights[j] : 0.f;
         }
-        const uint32_t b = bag_b[lo];
-        const int64_t idx = static_cast<int64_t>(__builtin_nontemporal_load(indices + j));
-        uint32_t key = static_cast<uint32_t>(idx);
-        if (check && (idx < 0 || idx >= bag_rows[lo])) {
-            key = kSentinel;
-            atomicOr(status, TBE_STATUS_INDEX_OOB);
-        }
-        const bool second = bag_buf[lo] != 0;
-        uint32_t *const keys = second ? keys1 : keys0;
-        V *const vals = second ? vals1 : vals0;
-        keys[j] = key;
-        if constexpr (sizeof(V) == 8) {
-            const float w = mean ? 1.0f / static_cast<float>(off[lo + 1] - off[lo]) : weights[j];
-            vals[j] = static_cast<uint64_t>(b) | (static_cast<uint64_t>(__float_as_uint(w)) << 32);
-        } else {
-            vals[j] = static_cast<uint32_t>(b);
+#pragma unroll
+        for (int r = 0; r < kKeyAhead; ++r) {
+            const int64_t j = j0 + static_cast<int64_t>(r) * kThreads;
+            if (j >= last) break;
+            int lo = 0, hi = nk;  // off[lo] <= j < off[hi]
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (off[mid] <= j) lo = mid; else hi = mid;
+            }
+            const uint32_t b = bag_b[lo];
+            const int64_t idx = ids[r];
+            uint32_t key = static_cast<uint32_t>(idx);
+            if (check && (idx < 0 || idx >= bag_rows[lo])) {
+                key = kSentinel;
+                atomicOr(status, TBE_STATUS_INDEX_OOB);
+            }
+            const bool second = bag_buf[lo] != 0;
+            uint32_t *const keys = second ? keys1 : keys0;
+            V *const vals = second ? vals1 : vals0;
+            keys[j] = key;
+            if constexpr (sizeof(V) == 8) {
+                const float w = mean ? 1.0f / static_cast<float>(off[lo + 1] - off[lo]) : wts[r];
+                vals[j] = static_cast<uint64_t>(b) | (static_cast<uint64_t>(__float_as_uint(w)) << 32);
+            } else {
+                vals[j] = static_cast<uint32_t>(b);
+            }
         }
     }
 }
