@@ -356,16 +356,14 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__
         const int64_t pos = wbase + r * 64 + lane;
         const bool valid = pos < ti.p_hi;
         const uint32_t d = digit_of(k[r], shift, mask);
-        // a round whose keys all share one digit (common in the high passes,
-        // where small tables' keys are all 0) adds once instead of 64 times
-        // to one LDS word
+        // the lanes holding lane 0's digit add once, through lane 0, instead
+        // of one atomic each to one LDS word: a round whose keys share a digit
+        // (small tables' high digits are all 0; after the first pass a hot
+        // row fills most of its low-byte group) costs one add
         const uint32_t d0 = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(d)));
-        const uint64_t vm = __ballot(valid);
-        if (__ballot(valid && d == d0) == vm) {
-            if (lane == 0 && vm) atomicAdd(&cnt[wave][d0], static_cast<uint32_t>(__popcll(vm)));
-        } else if (valid) {
-            atomicAdd(&cnt[wave][d], 1u);
-        }
+        const uint64_t same = __ballot(valid && d == d0);
+        if (lane == 0 && same) atomicAdd(&cnt[wave][d0], static_cast<uint32_t>(__popcll(same)));
+        if (valid && d != d0) atomicAdd(&cnt[wave][d], 1u);
     }
     __syncthreads();
     uint32_t c = 0;
