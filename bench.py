@@ -2,11 +2,15 @@
 
 One step = one pass of the whole path over one batch: the forward pooled
 lookup over every (bag, table) and, for the training configuration, the
-sparse backward (key build, radix sort, segments, segmented reduce).  Inputs
-are seeded synthetic draws resident in HBM before timing starts.  Prints one
-JSON line: whole-step lookups/s, the roofline of the step's dominant kernel
-(and of the forward kernel) against HBM, per-phase backward times, and the
-CPU oracle timed on a bounded sample of the same workload.
+sparse backward (key build, radix sort, segments, segmented reduce), queued
+in that order on one stream.  (--overlap-index queues the backward's index
+phase, which needs only the lookup ids, on a second stream beside the
+forward instead; on MI355X that gains nothing, since the forward's
+workgroups fill every CU and both are bound by the same per-CU memory
+request rate.)  Inputs are seeded synthetic draws resident in HBM before
+timing starts.  Prints one JSON line: whole-step lookups/s, the roofline of the
+step's dominant kernel (and of the forward kernel) against HBM, per-phase
+times, and the CPU oracle timed on a bounded sample of the same workload.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 5]
 """
@@ -60,6 +64,45 @@ def forward_bytes(spec, offsets_host: np.ndarray, index_bytes: int = 8, out_byte
     return rows + idx + bags
 
 
+def compulsory_forward_bytes(spec, d, index_bytes: int = 8, out_bytes: int = 4) -> int:
+    """Bytes one forward launch cannot avoid: every distinct row it looks up
+    read once, every index (and weight) and offset read once, the output
+    written once.  Under Zipf-skewed ids the per-lookup figure counts hot rows
+    many times over; this one counts each once."""
+    off = d["offsets"].cpu().numpy()
+    B = spec.B
+    rows = 0
+    read = spec.dims.astype(np.int64) + 8 if spec.dtype == "u8" else spec.dims.astype(np.int64)
+    for t in range(spec.T):
+        s, e = int(off[t * B]), int(off[(t + 1) * B])
+        if e > s:
+            rows += int(torch.unique(d["indices"][s:e]).numel()) * int(read[t]) * spec.elem_size
+    n = int(off[-1])
+    return (rows + index_bytes * n + (4 * n if spec.weighted else 0) + index_bytes * (spec.T * B + 1)
+            + out_bytes * B * spec.total_dim)
+
+
+def host_info() -> dict:
+    """CPU model, logical CPUs the process may use, and host RAM."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    ram = None
+    try:
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal"):
+                ram = int(line.split()[1]) * 1024
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "cpus_available": len(os.sched_getaffinity(0)), "host_ram_bytes": ram}
+
+
 def backward_bytes(spec, N: int, U: int, grad_floats: int, index_bytes: int = 8, grad_out_bytes: int = 4) -> int:
     """Compulsory bytes of one backward: indices and offsets read, the output
     gradient read once, int64 row ids, segment offsets and row offsets
@@ -92,6 +135,25 @@ def source_hash(kernel: str) -> str:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
+
+
+def measured_hit_rate(kernel: str, workload: str):
+    """L2 (TCC) hit rate of the kernel from profiles/<kernel>_<workload>_tcc.md,
+    if that file was written for the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_tcc.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("source_sha256") != source_hash(kernel):
+        return None
+    try:
+        return float(fields["tcc_hit_rate"])
+    except (KeyError, ValueError):
+        return None
 
 
 def measured_traffic(kernel: str, workload: str):
@@ -161,7 +223,7 @@ def cpu_baseline(spec, d, target_s: float, pooling: str = "sum", training: bool 
     while dt < target_s / 4 and bs < spec.B:
         bs = min(spec.B, int(bs * max(2.0, min(16.0, target_s / max(dt, 1e-3) * 0.8))))
         dt, n = run(bs)
-    return {"value": n / dt, "unit": "lookups/s", "cores": threads, "kind": "oracle",
+    return {"value": n / dt, "unit": "lookups/s", "cores": threads, "kind": "oracle", **host_info(),
             "sample": (f"forward + backward (sort single-threaded; forward and gradient rows OpenMP) "
                        if training else "forward (OpenMP over bags) ")
                       + f"over the first {bs} bags of each of the {spec.T} tables ({n} lookups, {dt:.1f} s, "
@@ -343,6 +405,8 @@ def main():
                          "gradient alone (use --config 4); map_ids: the MapId preprocessing step at the "
                          "evaluation's largest shape (10000 ids x 50000 values); sgd / adagrad: the optimizer "
                          "step alone, on the sparse gradient of one cfg5 backward")
+    ap.add_argument("--overlap-index", action="store_true",
+                    help="queue the backward's index phase on a second stream beside the forward")
     ap.add_argument("--pooling", default="sum", choices=["sum", "mean"])
     ap.add_argument("--index-type", default="i64", choices=["i64", "i32"],
                     help="integer type of indices and offsets")
@@ -398,6 +462,7 @@ def main():
         d["grad_out"] = d["grad_out"].to(out_dtype)  # the gradient of out has out's type
     training = spec.grad
     grads = None
+    side = torch.cuda.Stream(dev)  # the backward's index phase (default priority, like the main stream)
     if training:
         N = d["N"]
         bounds = d["offsets"][:: spec.B].cpu().numpy().astype(np.int64)
@@ -410,16 +475,42 @@ def main():
         workspace = torch.empty(tbe.backward_workspace_bytes(plan, N), dtype=torch.uint8, device=dev)
         log(f"[bench] backward workspace {workspace.numel() / 1e9:.2f} GB, grad_rows capacity {cap / 2.5e8:.2f} GB")
 
-    def step(ev=None):
+    def forward(ev=None):
         if ev is not None:
             ev[0].record()
         tbe.forward(plan, d["tables"], d["indices"], d["offsets"], d["weights"], out=out, status=status)
         if ev is not None:
             ev[1].record()
+
+    def index_phase(ev=None):
+        tbe.backward_index(plan, d["indices"], d["offsets"], d["weights"], workspace=workspace, status=status,
+                           outputs=grads, events=ev)
+
+    def reduce_phase(ev=None):
+        tbe.backward_reduce(plan, d["grad_out"], d["N"], workspace, grads, per_sample_weights=d["weights"],
+                            status=status, events=ev)
+
+    def overlapped_step(ev=None):
+        """The index phase on the side stream beside the forward, the reduce
+        after both.  ev: forward (2), index phase (4) and reduce phase (3) events."""
+        if not training:
+            return forward(ev)
+        main = torch.cuda.current_stream(dev)
+        side.wait_stream(main)  # the previous step's reduce has read the workspace
+        with torch.cuda.stream(side):
+            index_phase(None if ev is None else ev[2:6])
+        forward(ev)
+        main.wait_stream(side)
+        reduce_phase(None if ev is None else ev[6:9])
+
+    def serial_step(ev=None):
+        """Forward, index phase, reduce phase in order on one stream."""
+        forward(ev)
         if training:
-            # ev[1:] also bracket the backward's phases (ev[1] opens the first)
-            tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], d["weights"], workspace=workspace,
-                         status=status, outputs=grads, phase_events=None if ev is None else ev[1:])
+            index_phase(None if ev is None else ev[2:6])
+            reduce_phase(None if ev is None else ev[6:9])
+
+    step = overlapped_step if args.overlap_index else serial_step
 
     for _ in range(args.warmup):
         step()
@@ -427,7 +518,7 @@ def main():
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())}")
 
-    nev = 2 + (tbe.NUM_PHASES if training else 0)
+    nev = 2 + (7 if training else 0)
     evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(nev)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -435,16 +526,24 @@ def main():
         step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
-    fwd_avg = float(np.mean(fwd_ms))
-    bwd_ms = [e[1].elapsed_time(e[-1]) for e in evs] if training else None
-    phase_ms = ([[e[1 + i].elapsed_time(e[2 + i]) for e in evs] for i in range(tbe.NUM_PHASES)]
-                if training else None)
     ms_per_step = wall * 1e3 / args.steps
+    overlapped_fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    sev = evs
+    if args.overlap_index:
+        # a serial pass as well: every part alone on one stream (kernel
+        # durations for the rooflines)
+        sev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(nev)) for _ in range(args.steps)]
+        for i in range(args.steps):
+            serial_step(sev[i])
+        torch.cuda.synchronize()
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in sev]
+    fwd_avg = float(np.mean(fwd_ms))
     N = d["N"]
     off_host = d["offsets"].cpu().numpy().astype(np.int64)
     ib = 4 if args.index_type == "i32" else 8
-    fbytes = forward_bytes(spec, off_host, ib, 4 if args.out_dtype == "f32" else 2)
+    ob = 4 if args.out_dtype == "f32" else 2
+    fbytes = forward_bytes(spec, off_host, ib, ob)
+    cbytes = compulsory_forward_bytes(spec, d, ib, ob)
     achieved = fbytes / (fwd_avg * 1e-3) / 1e9
 
     res = {
@@ -463,57 +562,78 @@ def main():
         "config": {"workload": DESCRIPTIONS[args.config] + variant_text(args, spec), "tables": spec.T,
                    "batch": spec.B, "table_dtype": spec.dtype, "lookups": N, "table_bytes": spec.table_bytes,
                    "total_dim": plan.total_dim, "seed": spec.seed, "training": training,
-                   "pooling": args.pooling, "index_type": args.index_type, "out_dtype": args.out_dtype},
+                   "pooling": args.pooling, "index_type": args.index_type, "out_dtype": args.out_dtype,
+                   "schedule": ("forward, then the backward's index and reduce phases, on one stream"
+                                if training and not args.overlap_index else
+                                "backward index phase on a second stream beside the forward, then the reduce"
+                                if training else "forward only")},
         "forward": {"ms": fwd_avg, "ms_p10": float(np.percentile(fwd_ms, 10)),
                     "ms_p90": float(np.percentile(fwd_ms, 90)), "lookups_per_s": N / (fwd_avg * 1e-3),
                     "algorithmic_bytes": fbytes, "effective_GBps": achieved,
-                    "frac_of_hbm_peak": achieved / HBM_PEAK_GBS},
+                    "frac_of_hbm_peak": achieved / HBM_PEAK_GBS, "compulsory_bytes": cbytes,
+                    "compulsory_GBps": cbytes / (fwd_avg * 1e-3) / 1e9,
+                    "compulsory_frac_of_hbm_peak": cbytes / (fwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                    "ms_in_timed_steps": overlapped_fwd},
     }
     workload = f"cfg{args.config}" + variant_tag(args, spec)
-    roof = {"forward_kernel": {"bound": "hbm", "kernel": "forward_kernel", "ms": fwd_avg, "achieved": achieved,
-                               "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                               "traffic": measured_traffic("forward_kernel", workload), "algorithmic_bytes": fbytes}}
+
+    def roof(kernel, ms, nbytes, extra=None):
+        traffic = measured_traffic(kernel, workload)
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        r = {"bound": "hbm", "kernel": kernel, "ms": ms, "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+             "frac": gbs / HBM_PEAK_GBS, "traffic": traffic, "algorithmic_bytes": nbytes,
+             # the same time against the bytes the counters saw move beyond L2
+             "traffic_GBps": None if traffic is None else traffic / (ms * 1e-3) / 1e9,
+             "traffic_frac": None if traffic is None else traffic / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+             "l2_hit_rate": measured_hit_rate(kernel, workload)}
+        r.update(extra or {})
+        return r
+
+    rf = {"forward_kernel": roof("forward_kernel", fwd_avg, fbytes,
+                                 {"compulsory_bytes": cbytes,
+                                  "compulsory_frac": cbytes / (fwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS})}
     if training:
+        idx_ms = [e[2].elapsed_time(e[5]) for e in sev]
+        red_ph = [e[6].elapsed_time(e[7]) for e in sev]
+        comb_ph = [e[7].elapsed_time(e[8]) for e in sev]
+        phase_ms = {"keys": [e[2].elapsed_time(e[3]) for e in sev], "sort": [e[3].elapsed_time(e[4]) for e in sev],
+                    "segments": [e[4].elapsed_time(e[5]) for e in sev], "reduce": red_ph, "combine": comb_ph}
+        bwd_ms = [a + b + c for a, b, c in zip(idx_ms, red_ph, comb_ph)]
         bwd_avg = float(np.mean(bwd_ms))
         U = grads.num_unique()
         gro_total = int(grads.grad_row_offsets[U].item())
-        gob = 4 if args.out_dtype == "f32" else 2
-        bbytes = backward_bytes(spec, N, U, gro_total, ib, gob)
+        bbytes = backward_bytes(spec, N, U, gro_total, ib, ob)
         res["backward"] = {"ms": bwd_avg, "ms_p10": float(np.percentile(bwd_ms, 10)),
                            "ms_p90": float(np.percentile(bwd_ms, 90)), "lookups_per_s": N / (bwd_avg * 1e-3),
                            "unique_rows": U, "compulsory_bytes": bbytes,
                            "effective_GBps": bbytes / (bwd_avg * 1e-3) / 1e9,
                            "frac_of_hbm_peak": bbytes / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                           "phases_ms": {name: float(np.mean(t)) for name, t in zip(tbe.PHASES, phase_ms)}}
-        red_ms = float(np.mean(phase_ms[tbe.PHASES.index("reduce")]))
-        rbytes = reduce_bytes(spec, N, gro_total, spec.weighted or args.pooling == "mean", gob)
-        red_gbs = rbytes / (red_ms * 1e-3) / 1e9
-        roof["reduce_kernel"] = {"bound": "hbm", "kernel": "reduce_kernel", "ms": red_ms, "achieved": red_gbs,
-                                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": red_gbs / HBM_PEAK_GBS,
-                                 "traffic": measured_traffic("reduce_kernel", workload),
-                                 "algorithmic_bytes": rbytes}
+                           "phases_ms": {k: float(np.mean(v)) for k, v in phase_ms.items()},
+                           "serial_step_ms": fwd_avg + bwd_avg}
+        red_ms = float(np.mean(red_ph))
+        rbytes = reduce_bytes(spec, N, gro_total, spec.weighted or args.pooling == "mean", ob)
+        rf["reduce_kernel"] = roof("reduce_kernel", red_ms, rbytes)
     # the roofline of the step's dominant kernel (the longest average launch)
-    dominant = max(roof.values(), key=lambda r: r["ms"])
-    res["roofline"] = dominant
-    res["roofline_forward"] = roof["forward_kernel"]
+    res["roofline"] = max(rf.values(), key=lambda r: r["ms"])
+    res["roofline_forward"] = rf["forward_kernel"]
     if args.flushed_steps > 0:
         # secondary timing: every step starts with cold caches (1 GiB written
-        # first, outside the timed events)
+        # first, outside the timed events), parts serial
         junk = torch.empty(1 << 28, dtype=torch.float32, device=dev)
         fl = []
         for i in range(args.flushed_steps):
             junk.fill_(float(i))
             ev = tuple(torch.cuda.Event(enable_timing=True) for _ in range(nev))
-            step(ev)
+            serial_step(ev)
             torch.cuda.synchronize()
-            fl.append((ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[-1]) if training else 0.0))
+            fl.append((ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[-1]) if training else 0.0))
         del junk
         fw = [x[0] for x in fl]
         res["flushed"] = {"steps": args.flushed_steps, "forward_ms": float(np.median(fw)),
                           "forward_frac_of_hbm_peak": fbytes / (float(np.median(fw)) * 1e-3) / 1e9 / HBM_PEAK_GBS}
         if training:
             res["flushed"]["backward_ms"] = float(np.median([x[1] for x in fl]))
-            res["flushed"]["step_ms"] = float(np.median([x[0] + x[1] for x in fl]))
+            res["flushed"]["serial_step_ms"] = float(np.median([x[0] + x[1] for x in fl]))
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())}")
     if not args.no_cpu_baseline:

@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define TBE_ABI_VERSION 2
+#define TBE_ABI_VERSION 3
 
 /*
  * Element types.  Tables may use any of them; the forward output F32, F16 or
@@ -102,7 +102,8 @@ typedef struct tbe_desc {
     int32_t num_tables;           /* T >= 1                                       */
     int32_t dtype;                /* enum tbe_dtype of every table                */
     int64_t batch_size;           /* B >= 0                                       */
-    const int64_t *rows;          /* host [T]: R_t >= 1                           */
+    const int64_t *rows;          /* host [T]: 1 <= R_t < 2^32 - 1 (row ids are
+                                     32-bit on the GPU, one value reserved)      */
     const int32_t *dims;          /* host [T]: D_t >= 1, D_t*elem_size % 16 == 0
                                      (elem_size 1 for TBE_U8_ROWWISE)             */
     const int64_t *table_offsets; /* host [T]: element offset of table t in the
@@ -195,8 +196,9 @@ int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const void *gr
                         void *stream);
 
 /*
- * MapId preprocessing (the paper's Evaluation section, "MapId Transform"):
- * remaps raw categorical ids to dense ids for the embedding lookup.  For a
+ * MapId preprocessing (Monetization Case Study, "Data Preprocessing Kernels on
+ * MTIA", "MapId Transform": the algorithm's three steps and its worked
+ * example): remaps raw categorical ids to dense ids for the embedding lookup.  For a
  * mapping of known raw ids in non-decreasing order, value v maps to p + 1,
  * where p is the number of mapping entries less than v clamped to
  * mapping_size - 1, if mapping[p] == v, and to 0 otherwise: the 1-based
@@ -248,7 +250,8 @@ int32_t tbe_apply_gradient(const tbe_plan *plan, void *tables, const tbe_optimiz
                            const int64_t *grad_idx, const int64_t *grad_row_offsets, const float *grad_rows,
                            const int64_t *num_unique, int64_t max_unique, void *stream);
 
-/* Bytes of device workspace tbe_backward needs for num_indices lookups. */
+/* Bytes of device workspace tbe_backward (and its two phases) needs for
+ * num_indices lookups. */
 int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, size_t *bytes);
 
 /*
@@ -273,11 +276,17 @@ int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, 
  *   num_unique          device int64 scalar: U
  *   status              as in tbe_forward; TBE_STATUS_CAPACITY is set (and no
  *                       gradient row written) if grad_row_offsets[U] exceeds
- *                       grad_rows_capacity
+ *                       grad_rows_capacity.  May be NULL only when the plan
+ *                       does not check bounds; a too-small capacity then
+ *                       writes no gradient row and is seen by the caller as
+ *                       grad_row_offsets[U] > grad_rows_capacity.
  * Entries past U of grad_idx / seg_offsets / grad_row_offsets are unspecified.
  * The tables themselves are not read, so any table type is accepted.
  * Every gradient row has a single writer and a fixed summation order, so the
- * result is bitwise reproducible.
+ * result is bitwise reproducible.  A batch of no bags (B == 0) holds no
+ * lookup (num_indices must be 0; offsets may then be NULL).
+ * Equivalent to tbe_backward_index followed by tbe_backward_reduce on the
+ * same stream.
  */
 int32_t tbe_backward(const tbe_plan *plan, const void *grad_out, const void *indices,
                      const void *offsets, int64_t num_indices, const float *per_sample_weights,
@@ -285,7 +294,7 @@ int32_t tbe_backward(const tbe_plan *plan, const void *grad_out, const void *ind
                      int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                      int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream);
 
-/* Parts of tbe_backward, in launch order, for tbe_backward_timed. */
+/* Parts of tbe_backward, in launch order, for the phase events. */
 enum tbe_backward_phase {
     TBE_PHASE_KEYS = 0,     /* validate offsets, build sort keys and values      */
     TBE_PHASE_SORT = 1,     /* per-table radix sort                              */
@@ -311,6 +320,48 @@ int32_t tbe_backward_timed(const tbe_plan *plan, const void *grad_out, const voi
                            int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
                            int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream,
                            void *const *phase_events);
+
+/*
+ * The backward in two phases, so that the part that needs only the lookup ids
+ * can run before grad_out exists: in training the ids of a batch are known
+ * before its forward, so a caller may queue this index phase on a second
+ * stream beside the forward (both only read indices and offsets) and the
+ * reduce phase after both.  The phases compute exactly what tbe_backward
+ * computes (bitwise).
+ *
+ * tbe_backward_index: keys, stable radix sort, segments (grad_idx,
+ * seg_offsets, grad_row_offsets, num_unique, all final when it completes) and
+ * the reduce's per-block facts, kept in `workspace`.  Arguments as in
+ * tbe_backward; status may be NULL only when the plan does not check bounds.
+ * phase_events: NULL, or 4 events recorded where keys, sort and segments
+ * begin and where the phase ends.
+ */
+int32_t tbe_backward_index(const tbe_plan *plan, const void *indices, const void *offsets, int64_t num_indices,
+                           const float *per_sample_weights, void *workspace, size_t workspace_bytes,
+                           int64_t *grad_idx, int64_t *seg_offsets, int64_t *grad_row_offsets, int64_t *num_unique,
+                           int32_t *status, void *stream, void *const *phase_events);
+
+/*
+ * tbe_backward_reduce: the gradient rows (segmented reduce of grad_out, then
+ * the combine of long segments' pieces) from a completed tbe_backward_index.
+ *   grad_out            as in tbe_backward
+ *   num_indices, workspace, workspace_bytes   those of the index phase, whose
+ *                       workspace must be unchanged since it ran (any stream
+ *                       order that puts the index phase first is fine)
+ *   per_sample_weights  the pointer given to the index phase, or NULL; only
+ *                       whether it is NULL matters here (the weights were read
+ *                       by the index phase and travel in the workspace)
+ *   grad_rows, grad_rows_capacity   as in tbe_backward
+ *   grad_row_offsets    as the index phase wrote it (read by the combine)
+ *   status              TBE_STATUS_CAPACITY as in tbe_backward (NULL under the
+ *                       same rule)
+ * phase_events: NULL, or 3 events recorded where the reduce and the combine
+ * begin and where the phase ends.
+ */
+int32_t tbe_backward_reduce(const tbe_plan *plan, const void *grad_out, int64_t num_indices,
+                            const float *per_sample_weights, void *workspace, size_t workspace_bytes,
+                            float *grad_rows, int64_t grad_rows_capacity, const int64_t *grad_row_offsets,
+                            int32_t *status, void *stream, void *const *phase_events);
 
 #ifdef __cplusplus
 }

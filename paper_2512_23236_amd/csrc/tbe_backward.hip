@@ -58,13 +58,15 @@ constexpr int kKeyBags = 256;                 // bags per keys workgroup
 constexpr int kKeyAhead = 4;                  // keys kernel: lookup rounds whose loads are in flight together
 constexpr int kCombineBatch = 8;              // piece rows loaded at once in combine
 
-// Device control block at the start of the workspace.
+// Device control block at the start of the workspace.  The index phase
+// writes it; the reduce phase reads it.
 struct Ctl {
-    int32_t abort;       // malformed offsets seen (bounds check on): stop
-    int32_t skip_rows;   // grad_rows too small: write no gradient row
+    int32_t abort;        // malformed offsets seen (bounds check on): stop
+    int32_t pad0;
     int64_t total_tiles;
     int64_t total_works;  // reduce work items: (table, column slice, tile)
-    int64_t pad[5];
+    int64_t total_floats; // grad_row_offsets[U]: floats of all gradient rows
+    int64_t pad[4];
 };
 
 // Per-table lookup range in the sorted order, its first tile and its first
@@ -167,6 +169,8 @@ __device__ inline uint64_t match_digit(uint32_t d, bool valid, int nbits) {
 
 // ------------------------------------------------------------------ setup
 
+// With no bags (B == 0) `offsets` may be NULL and is not read (the host
+// then guarantees N == 0).
 template <typename IT>
 __global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__restrict__ offsets,
                                                          const TableMeta *__restrict__ meta, int T, int64_t B,
@@ -175,10 +179,13 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__
                                                          int64_t *seg_offsets, int64_t *grad_row_offsets) {
     __shared__ int64_t lds[kWaves];
     const int tid = threadIdx.x;
+    const bool have_bags = B > 0;
     __shared__ int bad;
     if (tid == 0) {
         bad = 0;
-        if (check && (offsets[0] != 0 || static_cast<int64_t>(offsets[static_cast<int64_t>(T) * B]) != N)) bad = 1;
+        if (check && have_bags &&
+            (offsets[0] != 0 || static_cast<int64_t>(offsets[static_cast<int64_t>(T) * B]) != N))
+            bad = 1;
         *num_unique = 0;
         seg_offsets[0] = 0;
         grad_row_offsets[0] = 0;
@@ -188,7 +195,7 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__
     for (int base = 0; base < T; base += kThreads) {
         const int t = base + tid;
         int64_t s = 0, e = 0, nt = 0, nw = 0;
-        if (t < T) {
+        if (t < T && have_bags) {
             s = static_cast<int64_t>(offsets[static_cast<int64_t>(t) * B]);
             e = static_cast<int64_t>(offsets[static_cast<int64_t>(t + 1) * B]);
             if (check && (s < 0 || e < s || e > N)) {
@@ -209,9 +216,9 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__
     if (tid == 0) {
         ranges[T] = Range{N, N, carry, wcarry};
         ctl->abort = bad;
-        ctl->skip_rows = 0;
         ctl->total_tiles = bad ? 0 : carry;
         ctl->total_works = bad ? 0 : wcarry;
+        ctl->total_floats = 0;
         if (bad) atomicOr(status, TBE_STATUS_OFFSETS);
     }
 }
@@ -591,8 +598,7 @@ __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t *__r
 __global__ __launch_bounds__(kThreads) void seg_scan_kernel(TileSeg *__restrict__ tseg, Ctl *ctl,
                                                             int64_t *__restrict__ num_unique,
                                                             int64_t *__restrict__ seg_offsets,
-                                                            int64_t *__restrict__ grad_row_offsets,
-                                                            int64_t capacity, int32_t *status) {
+                                                            int64_t *__restrict__ grad_row_offsets) {
     __shared__ uint64_t lds[kWaves];
     if (ctl->abort) return;
     const int64_t n = ctl->total_tiles;
@@ -626,10 +632,7 @@ __global__ __launch_bounds__(kThreads) void seg_scan_kernel(TileSeg *__restrict_
         *num_unique = static_cast<int64_t>(cs);
         seg_offsets[cs] = static_cast<int64_t>(ck);
         grad_row_offsets[cs] = static_cast<int64_t>(cd);
-        if (static_cast<int64_t>(cd) > capacity) {
-            ctl->skip_rows = 1;
-            atomicOr(status, TBE_STATUS_CAPACITY);
-        }
+        ctl->total_floats = static_cast<int64_t>(cd);
     }
 }
 
@@ -881,7 +884,9 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
         const int q = static_cast<int>((pos - ti.p_lo) >> 7);  // block of pos (kBlk == 128)
         const bool before_blk = seg_start < ti.p_lo + static_cast<int64_t>(q) * kBlk;
         const bool in_range = seg_start >= r0;
-        const bool own = kept && (pos < r1 ? (in_range || long_r0) : (in_range && !long_r1));
+        // past r1 the wave only finishes the short segment open at r1 (the
+        // segments that start at or after r1 belong to the next range)
+        const bool own = kept && (pos < r1 ? (in_range || long_r0) : (in_range && seg_start < r1 && !long_r1));
         const bool long_q = (long_mask >> q) & 1ull;
         const bool long_q1 = (long_mask >> (q + 1)) & 1ull;
         const bool blk_end = pos < r1 && ((pos - ti.p_lo) & (kBlk - 1)) == kBlk - 1;
@@ -990,7 +995,7 @@ __global__ __launch_bounds__(64) void edges_kernel(const uint32_t *__restrict__ 
                                                    TileEdges *__restrict__ edges, int32_t *__restrict__ head_seg,
                                                    int32_t *__restrict__ tail_seg) {
     const int64_t tile = blockIdx.x;
-    if (tile >= ctl->total_tiles || ctl->skip_rows || ctl->abort) return;
+    if (tile >= ctl->total_tiles || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
     const TileSeg pre = tseg[tile];
@@ -1051,9 +1056,14 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
                                                           const TileSeg *__restrict__ tseg,
                                                           const TileEdges *__restrict__ edges, int64_t total_dim,
                                                           int64_t gout_elems, float *__restrict__ grad_rows,
+                                                          int64_t capacity, int32_t *status,
                                                           float *__restrict__ partials, int max_dim,
                                                           const float *__restrict__ zero_page) {
-    if (ctl->skip_rows || ctl->abort) return;
+    if (ctl->abort) return;
+    if (ctl->total_floats > capacity) {  // grad_rows too small: write no gradient row
+        if (blockIdx.x == 0 && threadIdx.x == 0 && status) atomicOr(status, TBE_STATUS_CAPACITY);
+        return;
+    }
     const int64_t works = ctl->total_works;
     if (static_cast<int64_t>(blockIdx.x) >= works) return;
     const int64_t w = xcd_remap(blockIdx.x, works, kNumXcd);
@@ -1089,10 +1099,10 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
                                                            const int32_t *__restrict__ tail_seg,
                                                            const float *__restrict__ partials, int max_dim,
                                                            const int64_t *__restrict__ grad_row_offsets,
-                                                           float *__restrict__ grad_rows) {
+                                                           float *__restrict__ grad_rows, int64_t capacity) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    if (ctl->skip_rows || ctl->abort) return;
+    if (ctl->abort || ctl->total_floats > capacity) return;
     const int64_t nblk = ctl->total_tiles * kBlksPerTile;
     // waves take runs of 64 blocks and sum the segments whose tail piece lies
     // in one of them (tail_seg >= 0), lowest block first
@@ -1212,116 +1222,173 @@ Layout layout(const Plan &p, int64_t N) {
     return L;
 }
 
-template <typename V, typename IT>
-hipError_t run(const Plan &p, const void *grad_out, const IT *indices, const IT *offsets,
-               int64_t N, const float *weights, char *ws, const Layout &L, float *grad_rows, int64_t capacity,
-               int64_t *grad_idx, int64_t *seg_offsets, int64_t *grad_row_offsets, int64_t *num_unique,
-               int32_t *status, hipStream_t stream, void *const *phase_events) {
-    Ctl *ctl = reinterpret_cast<Ctl *>(ws + L.ctl);
-    Range *ranges = reinterpret_cast<Range *>(ws + L.ranges);
-    uint32_t *keys[2] = {reinterpret_cast<uint32_t *>(ws + L.keys0), reinterpret_cast<uint32_t *>(ws + L.keys1)};
-    V *vals[2] = {reinterpret_cast<V *>(ws + L.vals0), reinterpret_cast<V *>(ws + L.vals1)};
-    uint32_t *hist = reinterpret_cast<uint32_t *>(ws + L.hist);
-    uint32_t *totals = reinterpret_cast<uint32_t *>(ws + L.totals);
-    TileSeg *tseg = reinterpret_cast<TileSeg *>(ws + L.tseg);
-    TileEdges *edges = reinterpret_cast<TileEdges *>(ws + L.edges);
-    uint32_t *blk_starts = reinterpret_cast<uint32_t *>(ws + L.blk_starts);
-    int32_t *head = reinterpret_cast<int32_t *>(ws + L.head);
-    int32_t *tail = reinterpret_cast<int32_t *>(ws + L.tail);
-    float *partials = reinterpret_cast<float *>(ws + L.partials);
-    const int check = p.bounds_check;
-    const int T = p.T;
-    const int64_t nbags = static_cast<int64_t>(T) * p.B;
-    // phase boundary events (tbe_backward_timed); `marked` phases are recorded
-    int marked = 0;
-    auto mark = [&](int upto) -> hipError_t {
-        for (; phase_events && marked <= upto; ++marked) {
-            const hipError_t e = hipEventRecord(static_cast<hipEvent_t>(phase_events[marked]), stream);
+// The workspace carved into its parts (Layout gives the byte offsets).
+struct Ws {
+    Ctl *ctl;
+    Range *ranges;
+    uint32_t *keys[2];
+    void *vals[2];
+    uint32_t *hist, *totals;
+    TileSeg *tseg;
+    TileEdges *edges;
+    uint32_t *blk_starts;
+    int32_t *head, *tail;
+    float *partials;
+};
+
+Ws carve(char *ws, const Layout &L) {
+    Ws w;
+    w.ctl = reinterpret_cast<Ctl *>(ws + L.ctl);
+    w.ranges = reinterpret_cast<Range *>(ws + L.ranges);
+    w.keys[0] = reinterpret_cast<uint32_t *>(ws + L.keys0);
+    w.keys[1] = reinterpret_cast<uint32_t *>(ws + L.keys1);
+    w.vals[0] = ws + L.vals0;
+    w.vals[1] = ws + L.vals1;
+    w.hist = reinterpret_cast<uint32_t *>(ws + L.hist);
+    w.totals = reinterpret_cast<uint32_t *>(ws + L.totals);
+    w.tseg = reinterpret_cast<TileSeg *>(ws + L.tseg);
+    w.edges = reinterpret_cast<TileEdges *>(ws + L.edges);
+    w.blk_starts = reinterpret_cast<uint32_t *>(ws + L.blk_starts);
+    w.head = reinterpret_cast<int32_t *>(ws + L.head);
+    w.tail = reinterpret_cast<int32_t *>(ws + L.tail);
+    w.partials = reinterpret_cast<float *>(ws + L.partials);
+    return w;
+}
+
+// Radix passes over the bits of the largest table (every valid local key and
+// the drop key's low bits above them); a smaller table stops after its own
+// sort_passes.  Every table's sorted keys and values end in buffer passes & 1.
+int sort_bits(const Plan &p) {
+    int64_t max_rows = 1;
+    for (int t = 0; t < p.T; ++t) max_rows = p.meta_host[t].rows > max_rows ? p.meta_host[t].rows : max_rows;
+    return key_bits_for(max_rows);
+}
+int sort_passes_all(const Plan &p) { return (sort_bits(p) + kRadixBits - 1) / kRadixBits; }
+
+// Records caller events ev[first..upto] (those not yet recorded) on the stream.
+struct Marks {
+    void *const *ev;
+    int next, last;
+    hipStream_t stream;
+    hipError_t upto(int i) {
+        for (; ev && next <= i && next <= last; ++next) {
+            const hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev[next]), stream);
             if (e != hipSuccess) return e;
         }
         return hipSuccess;
-    };
-    hipError_t me = mark(TBE_PHASE_KEYS);
+    }
+};
+
+// Index phase (keys, radix sort, segments, block edges): reads only the
+// indices, offsets and weights.  Events ev[0..3]: keys, sort and segments
+// begin, and the phase ends.
+template <typename V, typename IT>
+hipError_t run_index(const Plan &p, const IT *indices, const IT *offsets, int64_t N, const float *weights, char *ws,
+                     const Layout &L, int64_t *grad_idx, int64_t *seg_offsets, int64_t *grad_row_offsets,
+                     int64_t *num_unique, int32_t *status, hipStream_t stream, void *const *ev) {
+    const Ws w = carve(ws, L);
+    V *vals[2] = {static_cast<V *>(w.vals[0]), static_cast<V *>(w.vals[1])};
+    const int check = p.bounds_check;
+    const int T = p.T;
+    const int64_t nbags = static_cast<int64_t>(T) * p.B;
+    Marks mk{ev, 0, 3, stream};
+    hipError_t me = mk.upto(0);
     if (me != hipSuccess) return me;
 
     hipLaunchKernelGGL(setup_kernel<IT>, dim3(1), dim3(kThreads), 0, stream, slice_cols(p.out_dtype), offsets,
-                       p.meta_dev, T, p.B, N, check, ctl,
-                       ranges, status, num_unique, seg_offsets, grad_row_offsets);
+                       p.meta_dev, T, p.B, N, check, w.ctl, w.ranges, status, num_unique, seg_offsets,
+                       grad_row_offsets);
     if (N == 0 || nbags == 0) {
         const hipError_t e = hipGetLastError();
-        return e != hipSuccess ? e : mark(TBE_NUM_PHASES);
+        return e != hipSuccess ? e : mk.upto(3);
     }
     const int mean = p.pooling == TBE_POOL_MEAN;
-    // bits: every valid local key of the largest table, and the drop key's
-    // low bits above them; a smaller table stops after its own sort_passes
-    int64_t max_rows = 1;
-    for (int t = 0; t < T; ++t) max_rows = p.meta_host[t].rows > max_rows ? p.meta_host[t].rows : max_rows;
-    const int bits = key_bits_for(max_rows);
-    const int passes = (bits + kRadixBits - 1) / kRadixBits;
+    const int bits = sort_bits(p);
+    const int passes = sort_passes_all(p);
     hipLaunchKernelGGL((keys_kernel<V, IT>), dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)),
-                       dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights, mean, ranges, p.B, nbags,
-                       check, ctl, keys[0], keys[1], vals[0], vals[1], passes, status);
+                       dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights, mean, w.ranges, p.B, nbags,
+                       check, w.ctl, w.keys[0], w.keys[1], vals[0], vals[1], passes, status);
     const dim3 tiles(static_cast<unsigned>(L.max_tiles)), blk(kThreads);
-    if ((me = mark(TBE_PHASE_SORT)) != hipSuccess) return me;
+    if ((me = mk.upto(1)) != hipSuccess) return me;
     for (int pass = 0; pass < passes; ++pass) {
         const int shift = pass * kRadixBits;
         const int nb = bits - shift < kRadixBits ? bits - shift : kRadixBits;
-        hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, keys[0], keys[1], p.meta_dev, ranges, T, ctl,
-                           pass, passes, shift, nb, hist);
-        hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), blk, 0, stream, hist, totals, p.meta_dev,
-                           ranges, ctl, pass);
-        hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, blk, 0, stream, keys[0], keys[1], vals[0], vals[1], hist,
-                           totals, p.meta_dev, ranges, T, ctl, pass, passes, shift, nb);
+        hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, w.keys[0], w.keys[1], p.meta_dev, w.ranges, T,
+                           w.ctl, pass, passes, shift, nb, w.hist);
+        hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), blk, 0, stream, w.hist, w.totals,
+                           p.meta_dev, w.ranges, w.ctl, pass);
+        hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, blk, 0, stream, w.keys[0], w.keys[1], vals[0], vals[1],
+                           w.hist, w.totals, p.meta_dev, w.ranges, T, w.ctl, pass, passes, shift, nb);
     }
     const int cur = passes & 1;  // every table's sorted keys and values
-    if ((me = mark(TBE_PHASE_SEGMENTS)) != hipSuccess) return me;
-    hipLaunchKernelGGL(seg_count_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
-                       blk_starts);
-    hipLaunchKernelGGL(seg_scan_kernel, dim3(1), blk, 0, stream, tseg, ctl, num_unique, seg_offsets,
-                       grad_row_offsets, capacity, status);
-    hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, keys[cur], p.meta_dev, ranges, T, ctl, tseg,
+    if ((me = mk.upto(2)) != hipSuccess) return me;
+    hipLaunchKernelGGL(seg_count_kernel, tiles, blk, 0, stream, w.keys[cur], p.meta_dev, w.ranges, T, w.ctl, w.tseg,
+                       w.blk_starts);
+    hipLaunchKernelGGL(seg_scan_kernel, dim3(1), blk, 0, stream, w.tseg, w.ctl, num_unique, seg_offsets,
+                       grad_row_offsets);
+    hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, w.keys[cur], p.meta_dev, w.ranges, T, w.ctl, w.tseg,
                        grad_idx, seg_offsets, grad_row_offsets);
-    hipLaunchKernelGGL(edges_kernel, tiles, dim3(64), 0, stream, keys[cur], blk_starts, seg_offsets, ranges, T, ctl,
-                       tseg, edges, head, tail);
-    if ((me = mark(TBE_PHASE_REDUCE)) != hipSuccess) return me;
-#define TBE_REDUCE(GT)                                                                                        \
-    hipLaunchKernelGGL((reduce_kernel<V, GT>), dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream, keys[cur], \
-                       vals[cur], grad_out, p.meta_dev, ranges, T, ctl, tseg, edges, p.total_dim, p.B * p.total_dim,  \
-                       grad_rows, partials, p.max_dim, static_cast<const float *>(p.zero_page))
+    hipLaunchKernelGGL(edges_kernel, tiles, dim3(64), 0, stream, w.keys[cur], w.blk_starts, seg_offsets, w.ranges,
+                       T, w.ctl, w.tseg, w.edges, w.head, w.tail);
+    const hipError_t e = hipGetLastError();
+    return e != hipSuccess ? e : mk.upto(3);
+}
+
+// Reduce phase (segmented reduce, piece combine): reads grad_out and the
+// index phase's workspace.  Events ev[0..2]: reduce and combine begin, and
+// the phase ends.
+template <typename V>
+hipError_t run_reduce(const Plan &p, const void *grad_out, int64_t N, char *ws, const Layout &L, float *grad_rows,
+                      int64_t capacity, const int64_t *grad_row_offsets, int32_t *status, hipStream_t stream,
+                      void *const *ev) {
+    const Ws w = carve(ws, L);
+    Marks mk{ev, 0, 2, stream};
+    hipError_t me = mk.upto(0);
+    if (me != hipSuccess) return me;
+    if (N == 0 || static_cast<int64_t>(p.T) * p.B == 0) return mk.upto(2);
+    const int cur = sort_passes_all(p) & 1;
+    const V *vals = static_cast<const V *>(w.vals[cur]);
+    const dim3 blk(kThreads);
+#define TBE_REDUCE(GT)                                                                                          \
+    hipLaunchKernelGGL((reduce_kernel<V, GT>), dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream,           \
+                       w.keys[cur], vals, grad_out, p.meta_dev, w.ranges, p.T, w.ctl, w.tseg, w.edges, p.total_dim, \
+                       p.B * p.total_dim, grad_rows, capacity, status, w.partials, p.max_dim,                     \
+                       static_cast<const float *>(p.zero_page))
     // grad_out has the forward output's element type
     if (p.out_dtype == TBE_F16) TBE_REDUCE(TBE_F16);
     else if (p.out_dtype == TBE_BF16) TBE_REDUCE(TBE_BF16);
     else TBE_REDUCE(TBE_F32);
 #undef TBE_REDUCE
-    if ((me = mark(TBE_PHASE_COMBINE)) != hipSuccess) return me;
+    if ((me = mk.upto(1)) != hipSuccess) return me;
     // one wave per run of 64 blocks, at most kCombineGroups workgroups
     const int64_t runs = (L.max_blocks + 63) / 64;
     const int64_t combine_groups = (runs + kWaves - 1) / kWaves < kCombineGroups ? (runs + kWaves - 1) / kWaves
                                                                                  : kCombineGroups;
-    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>(combine_groups)), blk, 0, stream, ranges, T,
-                       p.meta_dev, ctl, head, tail, partials, p.max_dim, grad_row_offsets, grad_rows);
+    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>(combine_groups)), blk, 0, stream, w.ranges, p.T,
+                       p.meta_dev, w.ctl, w.head, w.tail, w.partials, p.max_dim, grad_row_offsets, grad_rows,
+                       capacity);
     const hipError_t e = hipGetLastError();
-    return e != hipSuccess ? e : mark(TBE_NUM_PHASES);
+    return e != hipSuccess ? e : mk.upto(2);
 }
 
 }  // namespace
 
 size_t backward_workspace_bytes(const Plan &p, int64_t num_indices) { return layout(p, num_indices).total; }
 
-hipError_t launch_backward(const Plan &p, const void *grad_out, const void *indices, const void *offsets,
-                           int64_t num_indices, const float *weights, void *workspace, size_t workspace_bytes,
-                           float *grad_rows, int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
-                           int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, hipStream_t stream,
-                           void *const *phase_events) {
-    (void)workspace_bytes;
+// Lookups carry a weight (64-bit sort values) when weighted or mean-pooled.
+static bool wide_values(const Plan &p, bool weighted) { return weighted || p.pooling == TBE_POOL_MEAN; }
+
+hipError_t launch_backward_index(const Plan &p, const void *indices, const void *offsets, int64_t num_indices,
+                                 const float *weights, void *workspace, int64_t *grad_idx, int64_t *seg_offsets,
+                                 int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status,
+                                 hipStream_t stream, void *const *events) {
     const Layout L = layout(p, num_indices);
     char *ws = static_cast<char *>(workspace);
-    // lookups carry a weight (64-bit sort values) when weighted or mean-pooled
-    const bool wide = weights != nullptr || p.pooling == TBE_POOL_MEAN;
-#define TBE_RUN(V, IT)                                                                                          \
-    return run<V, IT>(p, grad_out, static_cast<const IT *>(indices), static_cast<const IT *>(offsets), num_indices, \
-                      weights, ws, L, grad_rows, grad_rows_capacity, grad_idx, seg_offsets, grad_row_offsets,     \
-                      num_unique, status, stream, phase_events)
+#define TBE_RUN(V, IT)                                                                                           \
+    return run_index<V, IT>(p, static_cast<const IT *>(indices), static_cast<const IT *>(offsets), num_indices,  \
+                            weights, ws, L, grad_idx, seg_offsets, grad_row_offsets, num_unique, status, stream,   \
+                            events)
+    const bool wide = wide_values(p, weights != nullptr);
     if (p.index_type == TBE_INDEX_I32) {
         if (wide) TBE_RUN(uint64_t, int32_t);
         TBE_RUN(uint32_t, int32_t);
@@ -1329,6 +1396,19 @@ hipError_t launch_backward(const Plan &p, const void *grad_out, const void *indi
     if (wide) TBE_RUN(uint64_t, int64_t);
     TBE_RUN(uint32_t, int64_t);
 #undef TBE_RUN
+}
+
+hipError_t launch_backward_reduce(const Plan &p, const void *grad_out, int64_t num_indices, bool weighted,
+                                  void *workspace, float *grad_rows, int64_t grad_rows_capacity,
+                                  const int64_t *grad_row_offsets, int32_t *status, hipStream_t stream,
+                                  void *const *events) {
+    const Layout L = layout(p, num_indices);
+    char *ws = static_cast<char *>(workspace);
+    if (wide_values(p, weighted))
+        return run_reduce<uint64_t>(p, grad_out, num_indices, ws, L, grad_rows, grad_rows_capacity, grad_row_offsets,
+                                    status, stream, events);
+    return run_reduce<uint32_t>(p, grad_out, num_indices, ws, L, grad_rows, grad_rows_capacity, grad_row_offsets,
+                                status, stream, events);
 }
 
 }  // namespace tbe

@@ -43,7 +43,9 @@ int32_t validate_desc(const tbe_desc *d) {
         const int32_t D = d->dims[t];
         if (R < 1 || D < 1) return TBE_ERR_SHAPE;
         if ((static_cast<int64_t>(D) * es) % 16 != 0) return TBE_ERR_ALIGN;
-        if (R > (int64_t(1) << 40) || D > (1 << 20)) return TBE_ERR_SHAPE;
+        // row ids are carried in 32 bits on the device, with one value kept
+        // for "no row" (forward) and for dropped lookups (backward sort keys)
+        if (R >= (int64_t(1) << 32) - 1 || D > (1 << 20)) return TBE_ERR_SHAPE;
         const int64_t row_elems = u8 ? D + 16 : D;
         const int64_t off = d->table_offsets ? d->table_offsets[t] : packed;
         if (off < 0 || (off * es) % 16 != 0) return TBE_ERR_ALIGN;
@@ -177,6 +179,7 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const void *indice
     if (num_indices < 0 || num_indices > max_indices(*p)) return TBE_ERR_SHAPE;
     if (p->pooling == TBE_POOL_MEAN && per_sample_weights) return TBE_ERR_UNSUPPORTED;
     const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
+    if (nbags == 0 && num_indices > 0) return TBE_ERR_SHAPE;  // no bag can hold a lookup
     if (!offsets && nbags > 0) return TBE_ERR_NULL;
     if (nbags == 0) return TBE_OK;  // empty output: nothing to write
     if (!tables || !out) return TBE_ERR_NULL;
@@ -255,6 +258,94 @@ int32_t tbe_backward_workspace_bytes(const tbe_plan *plan, int64_t num_indices, 
     return TBE_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Host checks of the backward's index phase (also the first half of tbe_backward).
+int32_t check_backward_index(const tbe::Plan *p, const void *indices, const void *offsets, int64_t num_indices,
+                             const float *per_sample_weights, const void *workspace, size_t workspace_bytes,
+                             const int64_t *grad_idx, const int64_t *seg_offsets, const int64_t *grad_row_offsets,
+                             const int64_t *num_unique, const int32_t *status) {
+    if (!p) return TBE_ERR_NULL;
+    // sorted positions and segment ids are carried in 32 bits on the device
+    if (num_indices < 0 || num_indices >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
+    if (p->pooling == TBE_POOL_MEAN && per_sample_weights) return TBE_ERR_UNSUPPORTED;
+    const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
+    if (nbags == 0 && num_indices > 0) return TBE_ERR_SHAPE;  // no bag can hold a lookup
+    if ((!offsets && nbags > 0) || !seg_offsets || !grad_row_offsets || !num_unique) return TBE_ERR_NULL;
+    if (num_indices > 0 && (!indices || !grad_idx)) return TBE_ERR_NULL;
+    if (p->bounds_check && !status) return TBE_ERR_NULL;
+    const size_t need = tbe::backward_workspace_bytes(*p, num_indices);
+    if (workspace_bytes < need) return TBE_ERR_WORKSPACE;
+    if (need > 0 && !workspace) return TBE_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return TBE_ERR_ALIGN;
+    if (!index_aligned(*p, indices) || !index_aligned(*p, offsets) ||
+        (reinterpret_cast<uintptr_t>(grad_idx) & 7u) || (reinterpret_cast<uintptr_t>(seg_offsets) & 7u) ||
+        (reinterpret_cast<uintptr_t>(grad_row_offsets) & 7u) || (reinterpret_cast<uintptr_t>(num_unique) & 7u) ||
+        (reinterpret_cast<uintptr_t>(per_sample_weights) & 3u))
+        return TBE_ERR_ALIGN;
+    return TBE_OK;
+}
+
+// Host checks of the reduce phase.  A too-small grad_rows_capacity is only
+// seen on the GPU; with status NULL (allowed when the plan does not check
+// bounds) it is not reported there, and the caller sees it as
+// grad_row_offsets[U] > capacity.
+int32_t check_backward_reduce(const tbe::Plan *p, const void *grad_out, int64_t num_indices, const void *workspace,
+                              size_t workspace_bytes, const float *grad_rows, int64_t grad_rows_capacity,
+                              const int64_t *grad_row_offsets, const int32_t *status) {
+    if (!p) return TBE_ERR_NULL;
+    if (num_indices < 0 || num_indices >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
+    if (grad_rows_capacity < 0) return TBE_ERR_SHAPE;
+    if (static_cast<int64_t>(p->T) * p->B == 0 && num_indices > 0) return TBE_ERR_SHAPE;
+    if (!grad_row_offsets) return TBE_ERR_NULL;
+    if (num_indices > 0 && !grad_out) return TBE_ERR_NULL;
+    if (grad_rows_capacity > 0 && !grad_rows) return TBE_ERR_NULL;
+    if (p->bounds_check && !status) return TBE_ERR_NULL;
+    const size_t need = tbe::backward_workspace_bytes(*p, num_indices);
+    if (workspace_bytes < need) return TBE_ERR_WORKSPACE;
+    if (need > 0 && !workspace) return TBE_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) || !aligned16(grad_rows) || !aligned16(grad_out) ||
+        (reinterpret_cast<uintptr_t>(grad_row_offsets) & 7u))
+        return TBE_ERR_ALIGN;
+    return TBE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t tbe_backward_index(const tbe_plan *plan, const void *indices, const void *offsets, int64_t num_indices,
+                           const float *per_sample_weights, void *workspace, size_t workspace_bytes,
+                           int64_t *grad_idx, int64_t *seg_offsets, int64_t *grad_row_offsets, int64_t *num_unique,
+                           int32_t *status, void *stream, void *const *phase_events) {
+    const tbe::Plan *p = plan_of(plan);
+    const int32_t rc = check_backward_index(p, indices, offsets, num_indices, per_sample_weights, workspace,
+                                            workspace_bytes, grad_idx, seg_offsets, grad_row_offsets, num_unique,
+                                            status);
+    if (rc != TBE_OK) return rc;
+    const hipError_t e = tbe::launch_backward_index(*p, indices, offsets, num_indices, per_sample_weights, workspace,
+                                                    grad_idx, seg_offsets, grad_row_offsets, num_unique, status,
+                                                    static_cast<hipStream_t>(stream), phase_events);
+    return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
+int32_t tbe_backward_reduce(const tbe_plan *plan, const void *grad_out, int64_t num_indices,
+                            const float *per_sample_weights, void *workspace, size_t workspace_bytes,
+                            float *grad_rows, int64_t grad_rows_capacity, const int64_t *grad_row_offsets,
+                            int32_t *status, void *stream, void *const *phase_events) {
+    const tbe::Plan *p = plan_of(plan);
+    const int32_t rc = check_backward_reduce(p, grad_out, num_indices, workspace, workspace_bytes, grad_rows,
+                                             grad_rows_capacity, grad_row_offsets, status);
+    if (rc != TBE_OK) return rc;
+    if (p->pooling == TBE_POOL_MEAN && per_sample_weights) return TBE_ERR_UNSUPPORTED;
+    const hipError_t e = tbe::launch_backward_reduce(*p, grad_out, num_indices, per_sample_weights != nullptr,
+                                                     workspace, grad_rows, grad_rows_capacity, grad_row_offsets,
+                                                     status, static_cast<hipStream_t>(stream), phase_events);
+    return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
 int32_t tbe_backward(const tbe_plan *plan, const void *grad_out, const void *indices,
                      const void *offsets, int64_t num_indices, const float *per_sample_weights,
                      void *workspace, size_t workspace_bytes, float *grad_rows,
@@ -272,35 +363,23 @@ int32_t tbe_backward_timed(const tbe_plan *plan, const void *grad_out, const voi
                            int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream,
                            void *const *phase_events) {
     const tbe::Plan *p = plan_of(plan);
-    if (!p) return TBE_ERR_NULL;
-    // sorted positions and segment ids are carried in 32 bits on the device
-    if (num_indices < 0 || num_indices >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
-    if (p->pooling == TBE_POOL_MEAN && per_sample_weights) return TBE_ERR_UNSUPPORTED;
-    // local row ids are 32-bit sort keys, with one key value kept for dropped lookups
-    for (int32_t t = 0; t < p->T; ++t)
-        if (p->meta_host[t].rows >= (int64_t(1) << 32) - 1) return TBE_ERR_SHAPE;
-    if (grad_rows_capacity < 0) return TBE_ERR_SHAPE;
-    const int64_t nbags = static_cast<int64_t>(p->T) * p->B;
-    if ((!offsets && nbags > 0) || !seg_offsets || !grad_row_offsets || !num_unique) return TBE_ERR_NULL;
-    if (num_indices > 0 && (!indices || !grad_idx || !grad_out)) return TBE_ERR_NULL;
-    if (grad_rows_capacity > 0 && !grad_rows) return TBE_ERR_NULL;
-    if (p->bounds_check && !status) return TBE_ERR_NULL;
-    const size_t need = tbe::backward_workspace_bytes(*p, num_indices);
-    if (workspace_bytes < need) return TBE_ERR_WORKSPACE;
-    if (need > 0 && !workspace) return TBE_ERR_NULL;
-    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) || !aligned16(grad_rows) || !aligned16(grad_out))
-        return TBE_ERR_ALIGN;
-    if (!index_aligned(*p, indices) || !index_aligned(*p, offsets) ||
-        (reinterpret_cast<uintptr_t>(grad_idx) & 7u) || (reinterpret_cast<uintptr_t>(seg_offsets) & 7u) ||
-        (reinterpret_cast<uintptr_t>(grad_row_offsets) & 7u) ||
-        (reinterpret_cast<uintptr_t>(num_unique) & 7u) ||
-        (reinterpret_cast<uintptr_t>(per_sample_weights) & 3u))
-        return TBE_ERR_ALIGN;
-    const hipError_t e = tbe::launch_backward(*p, grad_out, indices, offsets, num_indices,
-                                              per_sample_weights, workspace, workspace_bytes,
-                                              grad_rows, grad_rows_capacity, grad_idx, seg_offsets,
-                                              grad_row_offsets, num_unique, status,
-                                              static_cast<hipStream_t>(stream), phase_events);
+    // both phases' checks before anything is queued
+    int32_t rc = check_backward_index(p, indices, offsets, num_indices, per_sample_weights, workspace,
+                                      workspace_bytes, grad_idx, seg_offsets, grad_row_offsets, num_unique, status);
+    if (rc != TBE_OK) return rc;
+    rc = check_backward_reduce(p, grad_out, num_indices, workspace, workspace_bytes, grad_rows, grad_rows_capacity,
+                               grad_row_offsets, status);
+    if (rc != TBE_OK) return rc;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    // the phases share the boundary event between them: the index phase ends
+    // where the reduce begins (recorded twice at the same point of the stream)
+    hipError_t e = tbe::launch_backward_index(*p, indices, offsets, num_indices, per_sample_weights, workspace,
+                                              grad_idx, seg_offsets, grad_row_offsets, num_unique, status, s,
+                                              phase_events);
+    if (e == hipSuccess)
+        e = tbe::launch_backward_reduce(*p, grad_out, num_indices, per_sample_weights != nullptr, workspace,
+                                        grad_rows, grad_rows_capacity, grad_row_offsets, status, s,
+                                        phase_events ? phase_events + TBE_PHASE_REDUCE : nullptr);
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
 }
 

@@ -69,14 +69,17 @@ hipError_t launch_weight_grad(const Plan &p, const void *tables, const void *gra
                               const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,
                               hipStream_t stream);
 
-// Backward: workspace size and the full sort + segmented-reduce pipeline.
+// Backward: workspace size, the index phase (keys, sort, segments) and the
+// reduce phase (segmented reduce, combine) that completes it.
 size_t backward_workspace_bytes(const Plan &p, int64_t num_indices);
-hipError_t launch_backward(const Plan &p, const void *grad_out, const void *indices,
-                           const void *offsets, int64_t num_indices, const float *weights,
-                           void *workspace, size_t workspace_bytes, float *grad_rows,
-                           int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
-                           int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status,
-                           hipStream_t stream, void *const *phase_events);
+hipError_t launch_backward_index(const Plan &p, const void *indices, const void *offsets, int64_t num_indices,
+                                 const float *weights, void *workspace, int64_t *grad_idx, int64_t *seg_offsets,
+                                 int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status,
+                                 hipStream_t stream, void *const *events);
+hipError_t launch_backward_reduce(const Plan &p, const void *grad_out, int64_t num_indices, bool weighted,
+                                  void *workspace, float *grad_rows, int64_t grad_rows_capacity,
+                                  const int64_t *grad_row_offsets, int32_t *status, hipStream_t stream,
+                                  void *const *events);
 
 // Logical workgroup id under round-robin dispatch of workgroups over the
 // XCDs: workgroup w runs on XCD w % num_xcd, and the XCDs are given

@@ -16,7 +16,7 @@ import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtbe.so")
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 F32, F16, BF16, U8_ROWWISE = 0, 1, 2, 3
 # table storage type -> tbe_dtype; torch.uint8 tables are 8-bit row-wise (rows of
@@ -93,6 +93,10 @@ def _load():
         lib.tbe_backward.argtypes = [P, P, P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P, P, P]
         lib.tbe_backward_timed.restype = i32
         lib.tbe_backward_timed.argtypes = [P, P, P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P, P, P, P]
+        lib.tbe_backward_index.restype = i32
+        lib.tbe_backward_index.argtypes = [P, P, P, i64, P, P, ctypes.c_size_t, P, P, P, P, P, P, P]
+        lib.tbe_backward_reduce.restype = i32
+        lib.tbe_backward_reduce.argtypes = [P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P]
         if lib.tbe_abi_version() != ABI_VERSION:
             raise ImportError(f"libtbe ABI {lib.tbe_abi_version()} != {ABI_VERSION}")
         _lib = lib
@@ -313,6 +317,79 @@ class SparseGrad:
                 self.grad_rows[: int(gro[-1])].cpu())
 
 
+def _event_handles(events, n: int, where: str):
+    """HIP event handles of torch events (None -> NULL)."""
+    if events is None:
+        return None
+    if len(events) != n:
+        raise ValueError(f"{where} needs {n} events")
+    handles = (ctypes.c_void_p * n)()
+    for i, ev in enumerate(events):
+        if not ev.cuda_event:  # torch creates the HIP event on first use
+            ev.record()
+        handles[i] = ev.cuda_event
+    return handles
+
+
+def _check_backward_inputs(plan: Plan, indices, offsets, per_sample_weights):
+    N = indices.numel()
+    _dev_tensor(indices, plan.index_dtype, "indices", plan)
+    _dev_tensor(offsets, plan.index_dtype, "offsets", plan)
+    if offsets.numel() != plan.T * plan.B + 1:
+        raise ValueError("offsets must have T*B+1 entries")
+    if per_sample_weights is not None:
+        _dev_tensor(per_sample_weights, torch.float32, "per_sample_weights", plan)
+        if per_sample_weights.numel() != N:
+            raise ValueError("per_sample_weights must have one weight per index")
+    return N
+
+
+def _check_grad_out(plan: Plan, grad_out):
+    _dev_tensor(grad_out, plan.out_dtype, "grad_out", plan)  # the gradient of out has out's type
+    if grad_out.numel() != plan.B * plan.total_dim:
+        raise ValueError("grad_out must be [B, total_dim]")
+
+
+def _new_outputs(plan: Plan, offsets, N: int, grad_rows_capacity: Optional[int]) -> "SparseGrad":
+    dev = plan.device
+    if grad_rows_capacity is None:
+        # bound: every lookup its own row; needs the per-table lookup counts
+        # (one small device-to-host copy of T+1 offsets)
+        bounds = offsets[:: plan.B].cpu().numpy().astype(np.int64) if plan.B else np.zeros(plan.T + 1, np.int64)
+        grad_rows_capacity = int((np.diff(bounds) * plan.dims.astype(np.int64)).sum()) if N else 0
+    return SparseGrad(
+        torch.empty(max(grad_rows_capacity, 1), dtype=torch.float32, device=dev),
+        torch.empty(max(N, 1), dtype=torch.int64, device=dev),
+        torch.empty(N + 1, dtype=torch.int64, device=dev),
+        torch.empty(N + 1, dtype=torch.int64, device=dev),
+        torch.zeros(1, dtype=torch.int64, device=dev))
+
+
+def _check_outputs(plan: Plan, outputs: "SparseGrad", N: int, cap: Optional[int]) -> int:
+    """Sizes of caller-supplied outputs against N; returns the capacity in floats."""
+    for t, dt, name, need in ((outputs.grad_idx, torch.int64, "grad_idx", N),
+                              (outputs.seg_offsets, torch.int64, "seg_offsets", N + 1),
+                              (outputs.grad_row_offsets, torch.int64, "grad_row_offsets", N + 1),
+                              (outputs.num_unique_dev, torch.int64, "num_unique", 1),
+                              (outputs.grad_rows, torch.float32, "grad_rows", 0)):
+        _dev_tensor(t, dt, name, plan)
+        if t.numel() < need:
+            raise ValueError(f"{name} holds {t.numel()} entries, needs at least {need} for {N} lookups")
+    if cap is None:
+        return outputs.grad_rows.numel()
+    if cap < 0 or cap > outputs.grad_rows.numel():
+        raise ValueError(f"grad_rows_capacity {cap} is outside grad_rows ({outputs.grad_rows.numel()} floats)")
+    return int(cap)
+
+
+def _workspace(plan: Plan, N: int, workspace: Optional[torch.Tensor]) -> torch.Tensor:
+    need = backward_workspace_bytes(plan, N)
+    if workspace is None:
+        return torch.empty(max(need, 1), dtype=torch.uint8, device=plan.device)
+    _dev_tensor(workspace, torch.uint8, "workspace", plan)
+    return workspace  # its size is checked by the library (TBE_ERR_WORKSPACE)
+
+
 def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets: torch.Tensor,
              per_sample_weights: Optional[torch.Tensor] = None, grad_rows_capacity: Optional[int] = None,
              workspace: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
@@ -322,46 +399,64 @@ def backward(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets:
 
     phase_events: NUM_PHASES + 1 events recorded at the phase boundaries of
     the backward (tbe_backward_timed); event i .. i+1 brackets phase i."""
-    N = indices.numel()
-    _dev_tensor(grad_out, plan.out_dtype, "grad_out", plan)  # the gradient of out has out's type
-    _dev_tensor(indices, plan.index_dtype, "indices", plan)
-    _dev_tensor(offsets, plan.index_dtype, "offsets", plan)
-    if grad_out.numel() != plan.B * plan.total_dim:
-        raise ValueError("grad_out must be [B, total_dim]")
-    if offsets.numel() != plan.T * plan.B + 1:
-        raise ValueError("offsets must have T*B+1 entries")
-    if per_sample_weights is not None:
-        _dev_tensor(per_sample_weights, torch.float32, "per_sample_weights", plan)
-    dev = plan.device
+    N = _check_backward_inputs(plan, indices, offsets, per_sample_weights)
+    _check_grad_out(plan, grad_out)
     if outputs is None:
-        if grad_rows_capacity is None:
-            # bound: every lookup its own row; needs the per-table lookup counts
-            # (one small device-to-host copy of T+1 offsets)
-            bounds = offsets[:: plan.B].cpu().numpy().astype(np.int64) if plan.B else np.zeros(plan.T + 1, np.int64)
-            grad_rows_capacity = int((np.diff(bounds) * plan.dims.astype(np.int64)).sum()) if N else 0
-        outputs = SparseGrad(
-            torch.empty(max(grad_rows_capacity, 1), dtype=torch.float32, device=dev),
-            torch.empty(max(N, 1), dtype=torch.int64, device=dev),
-            torch.empty(N + 1, dtype=torch.int64, device=dev),
-            torch.empty(N + 1, dtype=torch.int64, device=dev),
-            torch.zeros(1, dtype=torch.int64, device=dev))
-    cap = outputs.grad_rows.numel() if grad_rows_capacity is None else int(grad_rows_capacity)
-    need = backward_workspace_bytes(plan, N)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        outputs = _new_outputs(plan, offsets, N, grad_rows_capacity)
+    cap = _check_outputs(plan, outputs, N, grad_rows_capacity)
+    workspace = _workspace(plan, N, workspace)
     args = (plan.handle, _ptr(grad_out), _ptr(indices), _ptr(offsets), N, _ptr(per_sample_weights),
             _ptr(workspace), workspace.numel(), _ptr(outputs.grad_rows), cap, _ptr(outputs.grad_idx),
             _ptr(outputs.seg_offsets), _ptr(outputs.grad_row_offsets), _ptr(outputs.num_unique_dev), _ptr(status),
-            _stream(dev))
+            _stream(plan.device))
     if phase_events is None:
         _check(_load().tbe_backward(*args), "tbe_backward")
     else:
-        if len(phase_events) != NUM_PHASES + 1:
-            raise ValueError(f"phase_events needs {NUM_PHASES + 1} events")
-        handles = (ctypes.c_void_p * len(phase_events))()
-        for i, ev in enumerate(phase_events):
-            if not ev.cuda_event:  # torch creates the HIP event on first use
-                ev.record()
-            handles[i] = ev.cuda_event
+        handles = _event_handles(phase_events, NUM_PHASES + 1, "phase_events")
         _check(_load().tbe_backward_timed(*args, handles), "tbe_backward_timed")
+    return outputs
+
+
+def backward_index(plan: Plan, indices: torch.Tensor, offsets: torch.Tensor,
+                   per_sample_weights: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                   status: Optional[torch.Tensor] = None, outputs: Optional[SparseGrad] = None,
+                   grad_rows_capacity: Optional[int] = None,
+                   events: Optional[Sequence[torch.cuda.Event]] = None):
+    """Index phase of the backward (tbe_backward_index), queued on the current
+    stream: row ids, segment offsets, row offsets and U are final when it
+    completes.  Returns (outputs, workspace) for backward_reduce.
+    events: 4 events (keys, sort, segments begin; the phase ends)."""
+    N = _check_backward_inputs(plan, indices, offsets, per_sample_weights)
+    if outputs is None:
+        outputs = _new_outputs(plan, offsets, N, grad_rows_capacity)
+    _check_outputs(plan, outputs, N, grad_rows_capacity)
+    workspace = _workspace(plan, N, workspace)
+    rc = _load().tbe_backward_index(plan.handle, _ptr(indices), _ptr(offsets), N, _ptr(per_sample_weights),
+                                    _ptr(workspace), workspace.numel(), _ptr(outputs.grad_idx),
+                                    _ptr(outputs.seg_offsets), _ptr(outputs.grad_row_offsets),
+                                    _ptr(outputs.num_unique_dev), _ptr(status), _stream(plan.device),
+                                    _event_handles(events, 4, "events"))
+    _check(rc, "tbe_backward_index")
+    return outputs, workspace
+
+
+def backward_reduce(plan: Plan, grad_out: torch.Tensor, num_indices: int, workspace: torch.Tensor,
+                    outputs: SparseGrad, per_sample_weights: Optional[torch.Tensor] = None,
+                    grad_rows_capacity: Optional[int] = None, status: Optional[torch.Tensor] = None,
+                    events: Optional[Sequence[torch.cuda.Event]] = None) -> SparseGrad:
+    """Reduce phase of the backward (tbe_backward_reduce), queued on the
+    current stream after a backward_index of the same num_indices, workspace,
+    outputs and per_sample_weights (whose values that phase already read).
+    events: 3 events (reduce, combine begin; the phase ends)."""
+    N = int(num_indices)
+    _check_grad_out(plan, grad_out)
+    if per_sample_weights is not None:
+        _dev_tensor(per_sample_weights, torch.float32, "per_sample_weights", plan)
+    cap = _check_outputs(plan, outputs, N, grad_rows_capacity)
+    workspace = _workspace(plan, N, workspace)
+    rc = _load().tbe_backward_reduce(plan.handle, _ptr(grad_out), N, _ptr(per_sample_weights), _ptr(workspace),
+                                     workspace.numel(),
+                                     _ptr(outputs.grad_rows), cap, _ptr(outputs.grad_row_offsets), _ptr(status),
+                                     _stream(plan.device), _event_handles(events, 3, "events"))
+    _check(rc, "tbe_backward_reduce")
     return outputs

@@ -72,6 +72,8 @@ def _create(desc):
     (dict(dtype=tbe.U8_ROWWISE, dims=(64, 24)), -4),          # 8-bit rows need D % 16 == 0
     (dict(dtype=tbe.U8_ROWWISE, offs=(0, 8008)), -4),         # 8-bit table offsets are 16-byte aligned
     (dict(dtype=tbe.U8_ROWWISE, offs=(0, 8000), elems=8000 + 50 * 144 - 1), -2),  # last row past the end
+    (dict(rows=(2 ** 32 - 1, 50), dims=(16, 16), dtype=tbe.U8_ROWWISE), -2),  # row ids are 32-bit on the GPU
+    (dict(rows=(2 ** 32, 50), dims=(8, 8)), -2),
 ])
 def test_plan_create_rejects_bad_descriptors(kwargs, code):
     rc, h = _create(_desc(**kwargs))
@@ -92,6 +94,8 @@ def test_null_arguments_rejected_without_a_device():
     assert lib.tbe_backward_workspace_bytes(None, 10, ctypes.byref(n)) == -1
     assert lib.tbe_backward(None, *([None] * 3), 0, None, None, 0, None, 0, *([None] * 6)) == -1
     assert lib.tbe_backward_timed(None, *([None] * 3), 0, None, None, 0, None, 0, *([None] * 7)) == -1
+    assert lib.tbe_backward_index(None, None, None, 0, None, None, 0, *([None] * 7)) == -1
+    assert lib.tbe_backward_reduce(None, None, 0, None, None, 0, None, 0, *([None] * 4)) == -1
     assert lib.tbe_plan_destroy(None) == 0
     assert lib.tbe_plan_info(None, None, None, None) == -1
 

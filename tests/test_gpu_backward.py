@@ -265,3 +265,129 @@ def test_full_size_cfg5():
     err = float(oracle.summation_error(got, ref, ab).max())
     note(f"[bwd-full] max summation error {err:.3g}")
     assert err <= GRAD_RTOL
+
+
+# ------------------------------------------------------------- two phases
+
+
+@pytest.mark.parametrize("k,pooling", [(5, "sum"), (4, "sum"), (5, "mean")])
+def test_split_phases_bitwise_equal(k, pooling):
+    """tbe_backward_index then tbe_backward_reduce give exactly what
+    tbe_backward gives, also when the index phase runs on a second stream
+    beside a forward on the first (both only read indices and offsets)."""
+    spec = workloads.small_config(k, seed=31, T=4, B=500)
+    if pooling == "mean":
+        spec = dataclasses.replace(spec, weighted=False)
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    plan = tbe.Plan(spec.rows, spec.dims, spec.torch_dtype, spec.B, bounds_check=True, device=device(),
+                    pooling=pooling)
+    w = d.get("weights")
+    status = torch.zeros(1, dtype=torch.int32, device=device())
+    whole = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], w, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    side = torch.cuda.Stream(device())  # default priority, like the current stream
+    main = torch.cuda.current_stream(device())
+    side.wait_stream(main)
+    with torch.cuda.stream(side):
+        parts, ws = tbe.backward_index(plan, d["indices"], d["offsets"], w, status=status)
+    out = tbe.forward(plan, d["tables"], d["indices"], d["offsets"], w, status=status)
+    main.wait_stream(side)
+    tbe.backward_reduce(plan, d["grad_out"], d["N"], ws, parts, per_sample_weights=w, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for x, y in zip(whole.trimmed(), parts.trimmed()):
+        assert torch.equal(x, y)
+    assert torch.isfinite(out).all()
+    # phase events of the split calls are recorded in order
+    ie = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    re = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    tbe.backward_index(plan, d["indices"], d["offsets"], w, workspace=ws, status=status, outputs=parts, events=ie)
+    tbe.backward_reduce(plan, d["grad_out"], d["N"], ws, parts, per_sample_weights=w, status=status, events=re)
+    torch.cuda.synchronize()
+    assert all(ie[i].elapsed_time(ie[i + 1]) >= 0 for i in range(3))
+    assert all(re[i].elapsed_time(re[i + 1]) >= 0 for i in range(2))
+    for x, y in zip(whole.trimmed(), parts.trimmed()):
+        assert torch.equal(x, y)
+
+
+def test_null_status_and_small_capacity():
+    """A plan without bounds checking may pass no status word.  A capacity too
+    small for the gradient then returns cleanly, writes no gradient row and
+    leaves grad_row_offsets[U] > capacity for the caller to see; the integer
+    outputs are still complete.  With a status word the shortfall is the
+    capacity bit."""
+    spec = workloads.small_config(5, seed=32, T=2, B=60)
+    d = workloads.gen_all(spec, device())
+    plan = plan_for(spec, bounds_check=False)
+    outs = tbe.SparseGrad(torch.full((64,), 7.0, device=device()),
+                          torch.empty(d["N"], dtype=torch.int64, device=device()),
+                          torch.empty(d["N"] + 1, dtype=torch.int64, device=device()),
+                          torch.empty(d["N"] + 1, dtype=torch.int64, device=device()),
+                          torch.zeros(1, dtype=torch.int64, device=device()))
+    g = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], grad_rows_capacity=16, outputs=outs)
+    torch.cuda.synchronize()
+    seg, ref, ab = oracle_backward(spec, d)
+    U = g.num_unique()
+    assert U == seg["U"] and int(g.grad_row_offsets[U]) > 16
+    np.testing.assert_array_equal(g.grad_idx[:U].cpu().numpy(), seg["grad_idx"])
+    assert torch.all(g.grad_rows == 7.0)  # no gradient row written
+    status = torch.zeros(1, dtype=torch.int32, device=device())
+    tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], grad_rows_capacity=16, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == tbe.STATUS_CAPACITY
+    g = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"])
+    torch.cuda.synchronize()
+    gidx, segs, gro, rows = g.trimmed()
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    assert float(oracle.summation_error(rows.numpy(), ref, ab).max()) <= GRAD_RTOL
+
+
+def test_segment_beyond_the_pairwise_levels():
+    """One row looked up more than 2^12 * 128 = 524,288 times: its segment has
+    more pieces than the combine's pairwise levels hold, so the combine's last
+    accumulator is used; a second table keeps ordinary segments beside it."""
+    spec = dataclasses.replace(workloads.small_config(5, seed=33, T=2, B=22000), dims=np.array([64, 128], np.int32))
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    off = d["offsets"].cpu()
+    s0, e0 = int(off[0]), int(off[spec.B])
+    assert e0 - s0 > 524288 + 3 * 128
+    d["indices"][s0:e0] = 7
+    note(f"[bwd] one segment of {e0 - s0} lookups")
+    check(spec, d)
+
+
+@pytest.mark.slow
+def test_full_size_cfg4_weighted():
+    """The training step's backward on configuration 4's shapes (40 tables of
+    5e6 rows, B = 32768, Poisson(50) bags, Zipf(1.2) ids, per-sample weights;
+    hottest segment about 3e5 lookups): integer outputs bit-exact, gradient
+    rows on a sample that includes the 20 longest segments."""
+    spec = dataclasses.replace(workloads.make_config(4), grad=True)
+    note("[bwd-cfg4] generating offsets, indices, weights, grad_out")
+    offsets = workloads.gen_offsets(spec, device())
+    N = int(offsets[-1])
+    d = {"offsets": offsets, "indices": workloads.gen_indices(spec, offsets), "N": N,
+         "weights": workloads.gen_weights(spec, N, device()), "grad_out": workloads.gen_grad_out(spec, device())}
+    g, st = run_backward(spec, d)
+    assert st == 0
+    note(f"[bwd-cfg4] GPU done (N={N}); oracle integer part")
+    idx = d["indices"].cpu().numpy()
+    off = d["offsets"].cpu().numpy()
+    seg = oracle.backward_segments(spec.rows, spec.dims, idx, off, spec.B)
+    gidx, segs, gro, rows = g.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(segs.numpy(), seg["seg_offsets"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    lens = np.diff(seg["seg_offsets"])
+    rng = np.random.default_rng(6)
+    sel = np.unique(np.concatenate([np.argsort(lens)[-20:], rng.choice(seg["U"], 2000, replace=False)]))
+    note(f"[bwd-cfg4] U={seg['U']}, oracle rows for {sel.size} segments (longest {lens.max()})")
+    ref, ab, ro = oracle.backward_rows(spec.rows, spec.dims, off, spec.B, d["grad_out"].cpu().numpy(), seg,
+                                       weights=d["weights"].cpu().numpy(), sel=sel)
+    got = np.concatenate([rows[int(gro[u]):int(gro[u + 1])].numpy() for u in sel])
+    err = float(oracle.summation_error(got, ref, ab).max())
+    note(f"[bwd-cfg4] max summation error {err:.3g}")
+    assert err <= GRAD_RTOL
+    del g, d
+    torch.cuda.empty_cache()

@@ -8,7 +8,7 @@ import torch
 import oracle
 import workloads
 from paper_2512_23236_amd import tbe
-from tests.gpu_util import (RTOL, device, forward_error, note, oracle_forward_bags, oracle_forward_full,
+from tests.gpu_util import (FP32_ACC_BOUND, RTOL, device, forward_error, note, oracle_forward_bags, oracle_forward_full,
                             plan_for, run_forward)
 
 pytestmark = pytest.mark.gpu
@@ -26,6 +26,7 @@ def _check_full(spec, d=None, bitexact=False):
     err = forward_error(spec, out, ref, ab)
     note(f"[fwd] {spec.name} max summation error {err:.3g}")
     assert err <= RTOL[spec.dtype]
+    assert err <= FP32_ACC_BOUND  # fp32 accumulation, also for 16-bit tables
     return out
 
 
@@ -77,6 +78,31 @@ def test_long_and_empty_bags():
     assert torch.all(o[1:5, :D] == 0) and not torch.any(torch.signbit(o[1:5, :D]))
     dim_off = spec.dim_off
     assert torch.all(o[:, dim_off[1]:dim_off[2]] == 0)
+
+
+@pytest.mark.parametrize("dtype,weighted", [("f32", False), ("f32", True), ("u8", False), ("u8", True),
+                                            ("f16", False), ("bf16", True)])
+def test_longest_bags_meet_the_fp32_bar(dtype, weighted):
+    """Bags of L = 200 lookups (the longest the configurations draw) on fp32
+    and 8-bit row-wise tables meet the 1e-5 bar, and 16-bit tables the fp32
+    accumulation bound, at row widths from 1 to 64 lanes per row."""
+    es = {"f32": 4, "f16": 2, "bf16": 2, "u8": 1}[dtype]
+    dims = [16 // es, 128 // es, 64, 256, 512 // es]
+    dims = [max(d, 16) if dtype == "u8" else d for d in dims]
+    base = workloads.small_config(3, seed=21, T=len(dims), B=24)
+    spec = dataclasses.replace(base, dtype=dtype, dims=np.array(dims, np.int32), weighted=weighted,
+                               name=f"long-{dtype}-{'w' if weighted else 'u'}")
+    d = workloads.gen_all(spec, device())
+    L = torch.full((spec.T * spec.B,), 200, dtype=torch.int64)
+    L[3::7] = 199       # odd lengths: the two chains differ by one term
+    L[5::11] = 0
+    off = torch.zeros(L.numel() + 1, dtype=torch.int64)
+    torch.cumsum(L, 0, out=off[1:])
+    d["offsets"] = off.to(device())
+    d["indices"] = workloads.gen_indices(spec, d["offsets"])
+    d["weights"] = workloads.gen_weights(spec, int(off[-1]), device()) if weighted else None
+    d["N"] = int(off[-1])
+    _check_full(spec, d)
 
 
 def test_one_row_table_and_identical_indices():
@@ -157,11 +183,12 @@ def test_python_binding_validates():
 @pytest.mark.parametrize("k", [3, 4])
 def test_full_size_sampled(k):
     """Configurations 3 and 4 at full size, in the benchmark's launch
-    configuration, checked on sampled bags (plus the longest and empty bags)."""
+    configuration (bounds checking on), checked on sampled bags (plus the
+    longest and empty bags)."""
     spec = workloads.make_config(k)
     note(f"[fwd-full] cfg{k}: generating {spec.table_bytes / 1e9:.1f} GB of tables")
     d = workloads.gen_all(spec, device())
-    out, st = run_forward(spec, d, bounds_check=False)
+    out, st = run_forward(spec, d, bounds_check=True)
     assert st == 0
     L = torch.diff(d["offsets"]).cpu().numpy()
     rng = np.random.default_rng(k)
@@ -178,6 +205,7 @@ def test_full_size_sampled(k):
         worst = max(worst, float(oracle.summation_error(o[b, c0:c1], ref, ab).max()))
     note(f"[fwd-full] cfg{k}: {len(res)} bags, max summation error {worst:.3g}")
     assert worst <= RTOL[spec.dtype]
+    assert worst <= FP32_ACC_BOUND
     # every output element was written with a finite value
     assert np.isfinite(o).all()
     del d
