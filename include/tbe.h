@@ -363,6 +363,36 @@ int32_t tbe_backward_reduce(const tbe_plan *plan, const void *grad_out, int64_t 
                             float *grad_rows, int64_t grad_rows_capacity, const int64_t *grad_row_offsets,
                             int32_t *status, void *stream, void *const *phase_events);
 
+/*
+ * Bytes of the fixed device scratch of tbe_backward_noalloc: the largest
+ * backward workspace it serves (tbe_backward_workspace_bytes), about
+ * 40 bytes per lookup with rows of up to 256 columns, so roughly 1.5 million
+ * lookups.  Every GPU that loads the library holds one such array until the
+ * process ends.
+ */
+#define TBE_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * tbe_backward without a workspace argument and without any allocation, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  The workspace is a
+ * fixed array of TBE_NOALLOC_SCRATCH_BYTES in device memory, one per GPU,
+ * located when the first plan is created on that GPU; this call makes no
+ * hipMalloc, hipFree or other allocating call.  Arguments, results and errors
+ * are those of tbe_backward, plus TBE_ERR_WORKSPACE (nothing queued) when
+ * tbe_backward_workspace_bytes for num_indices exceeds
+ * TBE_NOALLOC_SCRATCH_BYTES.  The plan must have been created on the device
+ * that `stream` belongs to.
+ * Every call on a GPU uses that GPU's one array: calls that may overlap on
+ * one GPU (other streams, other threads) race and must be ordered by the
+ * caller.  Nothing in the array needs clearing between calls (the backward
+ * never relies on the workspace's previous contents).
+ */
+int32_t tbe_backward_noalloc(const tbe_plan *plan, const void *grad_out, const void *indices, const void *offsets,
+                             int64_t num_indices, const float *per_sample_weights, float *grad_rows,
+                             int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
+                             int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

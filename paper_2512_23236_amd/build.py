@@ -9,7 +9,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB_PATH = os.path.join(HERE, "libtbe.so")
-SOURCES = ["tbe_host.hip", "tbe_forward.hip", "tbe_backward.hip", "tbe_weight_grad.hip", "tbe_map_ids.hip", "tbe_optimizer.hip"]
+SOURCES = ["tbe_host.hip", "tbe_forward.hip", "tbe_backward.hip", "tbe_weight_grad.hip", "tbe_map_ids.hip", "tbe_optimizer.hip",
+           "tbe_noalloc.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

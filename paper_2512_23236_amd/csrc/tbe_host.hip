@@ -150,6 +150,13 @@ int32_t tbe_plan_create(const tbe_desc *desc, tbe_plan **plan) {
         return TBE_ERR_HIP;
     }
     p.zero_page = reinterpret_cast<const char *>(p.meta_dev) + meta_bytes;
+    // the device's fixed backward scratch (tbe_backward_noalloc), found once per device
+    if (tbe::noalloc_scratch_init(p.device) != hipSuccess) {
+        (void)hipFree(p.meta_dev);
+        delete[] p.meta_host;
+        delete h;
+        return TBE_ERR_HIP;
+    }
     *plan = h;
     return TBE_OK;
 }
@@ -381,6 +388,21 @@ int32_t tbe_backward_timed(const tbe_plan *plan, const void *grad_out, const voi
                                         grad_rows, grad_rows_capacity, grad_row_offsets, status, s,
                                         phase_events ? phase_events + TBE_PHASE_REDUCE : nullptr);
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
+int32_t tbe_backward_noalloc(const tbe_plan *plan, const void *grad_out, const void *indices, const void *offsets,
+                             int64_t num_indices, const float *per_sample_weights, float *grad_rows,
+                             int64_t grad_rows_capacity, int64_t *grad_idx, int64_t *seg_offsets,
+                             int64_t *grad_row_offsets, int64_t *num_unique, int32_t *status, void *stream) {
+    const tbe::Plan *p = plan_of(plan);
+    if (!p) return TBE_ERR_NULL;
+    if (num_indices < 0 || num_indices >= (int64_t(1) << 31)) return TBE_ERR_SHAPE;
+    if (tbe::backward_workspace_bytes(*p, num_indices) > TBE_NOALLOC_SCRATCH_BYTES) return TBE_ERR_WORKSPACE;
+    void *scratch = tbe::noalloc_scratch(p->device);
+    if (!scratch) return TBE_ERR_HIP;
+    return tbe_backward(plan, grad_out, indices, offsets, num_indices, per_sample_weights, scratch,
+                        TBE_NOALLOC_SCRATCH_BYTES, grad_rows, grad_rows_capacity, grad_idx, seg_offsets,
+                        grad_row_offsets, num_unique, status, stream);
 }
 
 }  // extern "C"

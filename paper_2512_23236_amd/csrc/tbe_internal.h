@@ -81,6 +81,12 @@ hipError_t launch_backward_reduce(const Plan &p, const void *grad_out, int64_t n
                                   const int64_t *grad_row_offsets, int32_t *status, hipStream_t stream,
                                   void *const *events);
 
+// The fixed device scratch of tbe_backward_noalloc: looked up once per device
+// (with that device current) by noalloc_scratch_init; noalloc_scratch returns
+// the device's address, or NULL before the lookup.
+hipError_t noalloc_scratch_init(int device);
+void *noalloc_scratch(int device);
+
 // Logical workgroup id under round-robin dispatch of workgroups over the
 // XCDs: workgroup w runs on XCD w % num_xcd, and the XCDs are given
 // contiguous ranges of logical ids, so neighbouring bags (same table) share

@@ -97,6 +97,8 @@ def _load():
         lib.tbe_backward_index.argtypes = [P, P, P, i64, P, P, ctypes.c_size_t, P, P, P, P, P, P, P]
         lib.tbe_backward_reduce.restype = i32
         lib.tbe_backward_reduce.argtypes = [P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P]
+        lib.tbe_backward_noalloc.restype = i32
+        lib.tbe_backward_noalloc.argtypes = [P, P, P, P, i64, P, P, i64, P, P, P, P, P, P]
         if lib.tbe_abi_version() != ABI_VERSION:
             raise ImportError(f"libtbe ABI {lib.tbe_abi_version()} != {ABI_VERSION}")
         _lib = lib
@@ -459,4 +461,24 @@ def backward_reduce(plan: Plan, grad_out: torch.Tensor, num_indices: int, worksp
                                      _ptr(outputs.grad_rows), cap, _ptr(outputs.grad_row_offsets), _ptr(status),
                                      _stream(plan.device), _event_handles(events, 3, "events"))
     _check(rc, "tbe_backward_reduce")
+    return outputs
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TBE_NOALLOC_SCRATCH_BYTES
+
+
+def backward_noalloc(plan: Plan, grad_out: torch.Tensor, indices: torch.Tensor, offsets: torch.Tensor,
+                     outputs: SparseGrad, per_sample_weights: Optional[torch.Tensor] = None,
+                     grad_rows_capacity: Optional[int] = None, status: Optional[torch.Tensor] = None) -> SparseGrad:
+    """tbe_backward_noalloc: the backward with the library's fixed device
+    scratch as its workspace.  Neither this call nor the library allocates:
+    the caller passes every output.  Calls that may overlap on one GPU race."""
+    N = _check_backward_inputs(plan, indices, offsets, per_sample_weights)
+    _check_grad_out(plan, grad_out)
+    cap = _check_outputs(plan, outputs, N, grad_rows_capacity)
+    rc = _load().tbe_backward_noalloc(plan.handle, _ptr(grad_out), _ptr(indices), _ptr(offsets), N,
+                                      _ptr(per_sample_weights), _ptr(outputs.grad_rows), cap, _ptr(outputs.grad_idx),
+                                      _ptr(outputs.seg_offsets), _ptr(outputs.grad_row_offsets),
+                                      _ptr(outputs.num_unique_dev), _ptr(status), _stream(plan.device))
+    _check(rc, "tbe_backward_noalloc")
     return outputs
