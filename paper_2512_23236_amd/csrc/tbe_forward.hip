@@ -355,7 +355,10 @@ __global__ __launch_bounds__(kBlock) void forward_kernel(
     __shared__ float stage_all[kWavesPerBlock][64 * kBagsPerGroup * 8];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t unit = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave;
+    // workgroups are dispatched round-robin over the XCDs; the remap gives
+    // each XCD a contiguous run of work units (table-major), so the hot rows
+    // of the tables in flight on an XCD stay in that XCD's L2
+    const int64_t unit = xcd_remap(blockIdx.x, gridDim.x, kNumXcd) * kWavesPerBlock + wave;
     if (check && unit == 0 && lane == 0) {
         if (offsets[0] != 0 || static_cast<int64_t>(offsets[nbags]) != N) atomicOr(status, TBE_STATUS_OFFSETS);
     }

@@ -391,3 +391,82 @@ def test_full_size_cfg4_weighted():
     assert err <= GRAD_RTOL
     del g, d
     torch.cuda.empty_cache()
+
+
+# -------------------------------------------------- long and hot segments
+
+
+def _pattern_indices(spec, d, table, lengths):
+    """Table `table`'s lookups, in order, as consecutive runs of rows 0, 1, 2,
+    ... with the given run lengths (cycled; rows wrap at the table size)."""
+    off = d["offsets"].cpu()
+    s, e = int(off[table * spec.B]), int(off[(table + 1) * spec.B])
+    n = e - s
+    reps = np.resize(np.asarray(lengths), n)
+    pat = np.repeat(np.arange(reps.size), reps)[:n] % int(spec.rows[table])
+    d["indices"][s:e] = torch.as_tensor(pat, device=device())
+    return n
+
+
+@pytest.mark.parametrize("weighted", [False, True])
+def test_hot_segments_around_the_threshold(weighted):
+    """Segments of 1023 .. 1026 and 2000 lookups beside ones of 129 .. 1000
+    and short ones, in runs that straddle block and tile edges (every long
+    segment is summed from per-block pieces)."""
+    spec = dataclasses.replace(workloads.small_config(4 if weighted else 5, seed=51, T=2, B=3000),
+                               rows=np.array([40, 3000], np.int64), dims=np.array([64, 128], np.int32))
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    n = _pattern_indices(spec, d, 0, [1023, 1024, 1025, 1026, 2000, 129, 1000, 7, 1, 300])
+    note(f"[bwd-long] {n} lookups in table 0")
+    check(spec, d)
+
+
+def test_many_long_rows_in_one_table():
+    """A table with about 100 rows of more than 1024 lookups each."""
+    spec = dataclasses.replace(workloads.small_config(5, seed=52, T=1, B=4000), rows=np.array([500], np.int64),
+                               dims=np.array([64], np.int32))
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    n = _pattern_indices(spec, d, 0, [1100])
+    assert n // 1100 >= 90
+    check(spec, d)
+
+
+def test_hot_segment_in_a_small_batch():
+    """A batch of 50 bags whose table is hit only at one row: one segment of
+    more than 1024 lookups from few batch rows."""
+    spec = dataclasses.replace(workloads.small_config(5, seed=53, T=2, B=50), rows=np.array([9, 20], np.int64),
+                               dims=np.array([256, 64], np.int32))
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    off = d["offsets"].cpu()
+    d["indices"][int(off[0]):int(off[spec.B])] = 4
+    assert int(off[spec.B]) - int(off[0]) > 1024
+    check(spec, d)
+
+
+@pytest.mark.parametrize("out", ["bf16", "f16"])
+def test_hot_segments_mean_pooling_16bit_grad_out(out):
+    """Long segments under mean pooling (weight 1/L per lookup) with a 16-bit
+    output gradient (two columns per lane, 128-column slices)."""
+    spec = dataclasses.replace(workloads.small_config(5, seed=54, T=2, B=2500),
+                               rows=np.array([30, 700], np.int64), dims=np.array([256, 96], np.int32),
+                               weighted=False)
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    _pattern_indices(spec, d, 0, [5000, 1500, 40, 1025])
+    dt = {"bf16": torch.bfloat16, "f16": torch.float16}[out]
+    plan = tbe.Plan(spec.rows, spec.dims, spec.torch_dtype, spec.B, bounds_check=True, device=device(),
+                    pooling="mean", out_dtype=dt)
+    g16 = d["grad_out"].to(dt)
+    status = torch.zeros(1, dtype=torch.int32, device=device())
+    g = tbe.backward(plan, g16, d["indices"], d["offsets"], status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    idx, off = d["indices"].cpu().numpy(), d["offsets"].cpu().numpy()
+    seg = oracle.backward_segments(spec.rows, spec.dims, idx, off, spec.B)
+    ref, ab, _ = oracle.backward_rows(spec.rows, spec.dims, off, spec.B, g16.float().cpu().numpy(), seg,
+                                      pooling="mean")
+    gidx, segs, gro, rows = g.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    err = float(oracle.summation_error(rows.numpy(), ref, ab).max())
+    note(f"[bwd-long] mean {out}: max summation error {err:.3g}")
+    assert err <= GRAD_RTOL
