@@ -323,6 +323,67 @@ def bench_optimizer(args, spec, dev):
     }), flush=True)
 
 
+def bench_step_apply(args, spec, dev):
+    """The training step with the optimizer: forward, the backward's index
+    phase, and the reduce phase with the SGD or row-wise Adagrad step made by
+    the same kernels (tbe_backward_reduce_apply); beside it, timed in the same
+    run, the two-pass form (tbe_backward, then tbe_apply_gradient)."""
+    spec = __import__("dataclasses").replace(spec, grad=True)
+    kind = tbe.SGD if args.op == "step_sgd" else tbe.ROWWISE_ADAGRAD
+    log(f"[bench] {args.op} on {spec.name}")
+    d = workloads.gen_all(spec, dev)
+    N = d["N"]
+    plan = tbe.Plan(spec.rows, spec.dims, spec.torch_dtype, spec.B, bounds_check=True, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    out = torch.empty((spec.B, plan.total_dim), dtype=torch.float32, device=dev)
+    bounds = d["offsets"][:: spec.B].cpu().numpy().astype(np.int64)
+    cap = int((np.diff(bounds) * spec.dims.astype(np.int64)).sum())
+    grads = tbe.SparseGrad(torch.empty(cap, dtype=torch.float32, device=dev),
+                           torch.empty(N, dtype=torch.int64, device=dev), torch.empty(N + 1, dtype=torch.int64, device=dev),
+                           torch.empty(N + 1, dtype=torch.int64, device=dev), torch.zeros(1, dtype=torch.int64, device=dev))
+    workspace = torch.empty(tbe.backward_workspace_bytes(plan, N), dtype=torch.uint8, device=dev)
+    state = torch.zeros(int(spec.rows.sum()), dtype=torch.float32, device=dev) if kind else None
+    tables = d["tables"]
+    lr = 1e-3  # small: repeated steps keep the tables in range
+
+    def fused():
+        tbe.forward(plan, tables, d["indices"], d["offsets"], d["weights"], out=out, status=status)
+        tbe.backward_index(plan, d["indices"], d["offsets"], d["weights"], workspace=workspace, status=status,
+                           outputs=grads)
+        tbe.backward_reduce_apply(plan, d["grad_out"], N, workspace, grads, tables, kind, lr, 1e-8, state=state,
+                                  per_sample_weights=d["weights"], status=status)
+
+    def two_pass():
+        tbe.forward(plan, tables, d["indices"], d["offsets"], d["weights"], out=out, status=status)
+        tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], d["weights"], workspace=workspace,
+                     status=status, outputs=grads)
+        tbe.apply_gradient(plan, tables, grads, kind, lr, 1e-8, state=state, max_unique=N)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / args.steps
+
+    ms_two = timed(two_pass)
+    ms = timed(fused)
+    if int(status.item()) != 0:
+        raise RuntimeError(f"device status {int(status.item())}")
+    print(json.dumps({
+        "metric": f"training step with sparse {'SGD' if kind == tbe.SGD else 'row-wise Adagrad'}: lookups/s",
+        "op": args.op, "value": N / (ms * 1e-3), "unit": "lookups/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "dtype": "f32",
+        "data": "synthetic (seeded counter-based draws; no production data)",
+        "config": {"workload": f"{DESCRIPTIONS[args.config]}; then the optimizer step on the listed rows",
+                   "lookups": N},
+        "two_pass_ms_per_step": ms_two, "saved_ms": ms_two - ms,
+    }), flush=True)
+
+
 def bench_map_ids(args, dev, n_unique=10000, batch=50000):
     d = workloads.gen_map_ids(n_unique, batch, device=dev)
     out = torch.empty_like(d["values"])
@@ -400,11 +461,14 @@ def main():
     ap.add_argument("--flushed-steps", type=int, default=5,
                     help="extra steps, each after writing 1 GiB to evict L2 and the Infinity Cache, reported "
                          "as the secondary (cold-cache) timing; 0 skips them")
-    ap.add_argument("--op", default="step", choices=["step", "weight_grad", "map_ids", "sgd", "adagrad"],
+    ap.add_argument("--op", default="step", choices=["step", "weight_grad", "map_ids", "sgd", "adagrad", "step_sgd",
+                                                     "step_adagrad"],
                     help="step: forward (+ backward for cfg5), the default; weight_grad: the per-sample-weight "
                          "gradient alone (use --config 4); map_ids: the MapId preprocessing step at the "
                          "evaluation's largest shape (10000 ids x 50000 values); sgd / adagrad: the optimizer "
-                         "step alone, on the sparse gradient of one cfg5 backward")
+                         "step alone, on the sparse gradient of one cfg5 backward; step_sgd / step_adagrad: the "
+                         "training step with the optimizer made by the backward's reduce kernels, beside the "
+                         "two-pass form")
     ap.add_argument("--overlap-index", action="store_true",
                     help="queue the backward's index phase on a second stream beside the forward")
     ap.add_argument("--pooling", default="sum", choices=["sum", "mean"])
@@ -444,6 +508,8 @@ def main():
         return bench_weight_grad(args, spec, dev)
     if args.op in ("sgd", "adagrad"):
         return bench_optimizer(args, spec, dev)
+    if args.op in ("step_sgd", "step_adagrad"):
+        return bench_step_apply(args, spec, dev)
     log(f"[bench] generating {spec.name}: {spec.table_bytes / 1e9:.2f} GB of tables")
     t0 = time.time()
     d = workloads.gen_all(spec, dev)

@@ -364,6 +364,34 @@ int32_t tbe_backward_reduce(const tbe_plan *plan, const void *grad_out, int64_t 
                             int32_t *status, void *stream, void *const *phase_events);
 
 /*
+ * The reduce phase with the optimizer step made by the same kernels (the
+ * step right after the backward in training; the paper names training
+ * operators, no optimizer): tbe_backward_reduce, and then, for every listed
+ * row, the update of tbe_apply_gradient, made by the wave that has just
+ * summed the row, from its gradient row while that is still in cache, so no
+ * separate pass re-reads all gradient rows.  A workgroup takes one tile of
+ * the sorted lookups and sums every column slice of its rows (row-wise
+ * Adagrad needs the whole row); segments summed from per-block pieces are
+ * updated by the combine kernel.
+ *   grad_out ... grad_row_offsets, status   as in tbe_backward_reduce (the
+ *                       gradient rows are written and stay valid outputs)
+ *   grad_idx, seg_offsets   device, as the index phase wrote them
+ *   tables, opt, state  as in tbe_apply_gradient (state fp32 [total_rows],
+ *                       row-wise Adagrad only; may be NULL for SGD)
+ * The tables end bitwise as after tbe_backward followed by
+ * tbe_apply_gradient with max_unique = num_indices.  With
+ * TBE_STATUS_CAPACITY set nothing is updated.  8-bit row-wise tables are not
+ * updated in place (TBE_ERR_UNSUPPORTED).
+ * phase_events: NULL, or 3 events as in tbe_backward_reduce.
+ */
+int32_t tbe_backward_reduce_apply(const tbe_plan *plan, const void *grad_out, int64_t num_indices,
+                                  const float *per_sample_weights, void *workspace, size_t workspace_bytes,
+                                  float *grad_rows, int64_t grad_rows_capacity, const int64_t *grad_idx,
+                                  const int64_t *seg_offsets, const int64_t *grad_row_offsets, void *tables,
+                                  const tbe_optimizer *opt, float *state, int32_t *status, void *stream,
+                                  void *const *phase_events);
+
+/*
  * Bytes of the fixed device scratch of tbe_backward_noalloc: the largest
  * backward workspace it serves (tbe_backward_workspace_bytes), about
  * 40 bytes per lookup with rows of up to 256 columns, so roughly 1.5 million

@@ -33,7 +33,7 @@
 // bitwise reproducible.  Lookups whose index fails the bounds check are
 // keyed past every valid key of their table and dropped.
 
-#include "tbe_internal.h"
+#include "tbe_opt_math.h"
 
 namespace tbe {
 namespace {
@@ -1087,11 +1087,103 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
                                  max_dim, tile, slice * slice_cols(GT), zero_page);
 }
 
+// ------------------------------------------------- reduce and apply (fused)
+//
+// The backward with the optimizer step applied by the same kernels: a
+// workgroup takes one tile, and each of its waves sums its range of the tile
+// for every column slice of the table in turn (as reduce_kernel does, one
+// slice per pass), then updates the table rows of the short segments that
+// begin in its range from the gradient rows it has just written, while they
+// are still in cache.  Long segments are updated by the combine kernel once
+// their pieces are summed.  The gradient rows stay valid outputs; the update
+// is the one tbe_apply_gradient makes (opt::update_rows), so the tables end
+// bitwise as after tbe_backward followed by tbe_apply_gradient.
+
+// Makes this wave's gradient-row stores visible to its own loads that follow.
+__device__ inline void stores_then_loads() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+template <bool kAdagrad>
+__device__ inline void update_rows_any(int dt, const TableMeta &m, char *__restrict__ tables, float *state,
+                                       const float *grad_rows, int64_t my_g, int64_t my_o, int i, int e,
+                                       uint64_t skip, float lr, float eps) {
+    const int es = dt == TBE_F32 ? 4 : 2;
+    char *tab = tables + m.elem_offset * es;
+    if (dt == TBE_F32)
+        opt::update_rows<TBE_F32, kAdagrad>(m, tab, m.row_base, state, grad_rows, my_g, my_o, i, e, skip, lr, eps);
+    else if (dt == TBE_F16)
+        opt::update_rows<TBE_F16, kAdagrad>(m, tab, m.row_base, state, grad_rows, my_g, my_o, i, e, skip, lr, eps);
+    else
+        opt::update_rows<TBE_BF16, kAdagrad>(m, tab, m.row_base, state, grad_rows, my_g, my_o, i, e, skip, lr, eps);
+}
+
+template <typename V, int GT, bool kAdagrad>
+__global__ __launch_bounds__(kThreads) void reduce_apply_kernel(
+    const uint32_t *__restrict__ keys, const V *__restrict__ vals, const void *__restrict__ grad_out,
+    const TableMeta *__restrict__ meta, const Range *__restrict__ ranges, int T, const Ctl *__restrict__ ctl,
+    const TileSeg *__restrict__ tseg, const TileEdges *__restrict__ edges, int64_t total_dim, int64_t gout_elems,
+    float *__restrict__ grad_rows, int64_t capacity, int32_t *status, float *__restrict__ partials, int max_dim,
+    const float *__restrict__ zero_page, const int64_t *__restrict__ grad_idx,
+    const int64_t *__restrict__ seg_offsets, const int64_t *__restrict__ grad_row_offsets, char *__restrict__ tables,
+    int dt, float *__restrict__ state, float lr, float eps) {
+    if (ctl->abort) return;
+    if (ctl->total_floats > capacity) {  // grad_rows too small: write no gradient row, update nothing
+        if (blockIdx.x == 0 && threadIdx.x == 0 && status) atomicOr(status, TBE_STATUS_CAPACITY);
+        return;
+    }
+    const int64_t tiles = ctl->total_tiles;
+    if (static_cast<int64_t>(blockIdx.x) >= tiles) return;
+    const int64_t tile = xcd_remap(blockIdx.x, tiles, kNumXcd);
+    TileInfo ti;
+    if (!tile_info(ranges, T, tile, ti)) return;
+    const TableMeta m = meta[ti.t];
+    const TileSeg pre = tseg[tile];
+    const TileEdges te = edges[tile];
+    constexpr int GES = GT == TBE_F32 ? 4 : 2;
+    for (int c0 = 0; c0 < m.dim; c0 += slice_cols(GT)) {
+        if (gout_elems * GES < kBufferLimit)
+            reduce_wave<V, false, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
+                                      max_dim, tile, c0, zero_page);
+        else
+            reduce_wave<V, true, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
+                                     max_dim, tile, c0, zero_page);
+    }
+    stores_then_loads();
+    // the short segments that begin in this wave's range: segment ids
+    // [u_lo, u_hi), all of the tile's table
+    const int lane = threadIdx.x & 63;
+    const int wave = static_cast<int>(uni(threadIdx.x >> 6));
+    const int q0 = wave * kBlksPerWave;
+    const int64_t r0 = ti.p_lo + static_cast<int64_t>(q0) * kBlk;
+    if (r0 >= ti.p_hi) return;
+    const int64_t r1 = r0 + kBlksPerWave * kBlk < ti.p_hi ? r0 + kBlksPerWave * kBlk : ti.p_hi;
+    const int q1 = static_cast<int>((r1 - ti.p_lo + kBlk - 1) / kBlk);
+    const int64_t u_lo = pre.starts + te.starts[q0], u_hi = pre.starts + te.starts[q1];
+    for (int64_t base = u_lo; base < u_hi; base += 64) {
+        const int n = u_hi - base < 64 ? static_cast<int>(u_hi - base) : 64;
+        const int64_t u = base + lane;
+        int64_t my_g = 0, my_o = 0;
+        bool lng = false;
+        if (lane < n) {
+            my_g = grad_idx[u];
+            my_o = grad_row_offsets[u];
+            lng = seg_offsets[u + 1] - seg_offsets[u] > kBlk;  // summed from pieces: the combine updates it
+        }
+        update_rows_any<kAdagrad>(dt, m, tables, state, grad_rows, my_g, my_o, 0, n, __ballot(lng), lr, eps);
+    }
+}
+
 // Sums the pieces of every segment that crosses a block edge, in a fixed
 // pairwise order (binary-counter summation over the pieces: the tail piece of
 // the block where the segment begins, then the head pieces of the blocks that
 // follow), and writes its gradient row once.  A wave takes a run of 64 blocks
 // and handles the segments whose tail piece lies in one of them.
+// With kApply the combine then makes the optimizer step on each row it wrote
+// (kAdagrad: row-wise Adagrad, else SGD), as reduce_apply_kernel does for
+// short segments.
+template <bool kApply, bool kAdagrad>
 __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restrict__ ranges, int T,
                                                            const TableMeta *__restrict__ meta,
                                                            const Ctl *__restrict__ ctl,
@@ -1099,7 +1191,9 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
                                                            const int32_t *__restrict__ tail_seg,
                                                            const float *__restrict__ partials, int max_dim,
                                                            const int64_t *__restrict__ grad_row_offsets,
-                                                           float *__restrict__ grad_rows, int64_t capacity) {
+                                                           float *__restrict__ grad_rows, int64_t capacity,
+                                                           const int64_t *__restrict__ grad_idx, char *__restrict__ tables,
+                                                           int dt, float *__restrict__ state, float lr, float eps) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (ctl->abort || ctl->total_floats > capacity) return;
@@ -1178,6 +1272,11 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
                     }
                 }
                 if (act) store4(out + cv * 4, sum);
+            }
+            if constexpr (kApply) {
+                stores_then_loads();
+                update_rows_any<kAdagrad>(dt, meta[t], tables, state, grad_rows, grad_idx[u], grad_row_offsets[u], 0,
+                                          1, 0ull, lr, eps);
             }
         }
     }
@@ -1279,6 +1378,15 @@ struct Marks {
     }
 };
 
+// The optimizer step of the fused reduce-and-apply phase.
+struct ApplyArgs {
+    void *tables;
+    bool adagrad;
+    float lr, eps;
+    float *state;
+    const int64_t *grad_idx, *seg_offsets;
+};
+
 // Index phase (keys, radix sort, segments, block edges): reads only the
 // indices, offsets and weights.  Events ev[0..3]: keys, sort and segments
 // begin, and the phase ends.
@@ -1340,7 +1448,7 @@ hipError_t run_index(const Plan &p, const IT *indices, const IT *offsets, int64_
 template <typename V>
 hipError_t run_reduce(const Plan &p, const void *grad_out, int64_t N, char *ws, const Layout &L, float *grad_rows,
                       int64_t capacity, const int64_t *grad_row_offsets, int32_t *status, hipStream_t stream,
-                      void *const *ev) {
+                      void *const *ev, const ApplyArgs *ap) {
     const Ws w = carve(ws, L);
     Marks mk{ev, 0, 2, stream};
     hipError_t me = mk.upto(0);
@@ -1349,24 +1457,48 @@ hipError_t run_reduce(const Plan &p, const void *grad_out, int64_t N, char *ws, 
     const int cur = sort_passes_all(p) & 1;
     const V *vals = static_cast<const V *>(w.vals[cur]);
     const dim3 blk(kThreads);
+    if (!ap) {
 #define TBE_REDUCE(GT)                                                                                          \
     hipLaunchKernelGGL((reduce_kernel<V, GT>), dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream,           \
                        w.keys[cur], vals, grad_out, p.meta_dev, w.ranges, p.T, w.ctl, w.tseg, w.edges, p.total_dim, \
                        p.B * p.total_dim, grad_rows, capacity, status, w.partials, p.max_dim,                     \
                        static_cast<const float *>(p.zero_page))
-    // grad_out has the forward output's element type
-    if (p.out_dtype == TBE_F16) TBE_REDUCE(TBE_F16);
-    else if (p.out_dtype == TBE_BF16) TBE_REDUCE(TBE_BF16);
-    else TBE_REDUCE(TBE_F32);
+        // grad_out has the forward output's element type
+        if (p.out_dtype == TBE_F16) TBE_REDUCE(TBE_F16);
+        else if (p.out_dtype == TBE_BF16) TBE_REDUCE(TBE_BF16);
+        else TBE_REDUCE(TBE_F32);
 #undef TBE_REDUCE
+    } else {
+#define TBE_REDUCE_APPLY(GT, A)                                                                                 \
+    hipLaunchKernelGGL((reduce_apply_kernel<V, GT, A>), dim3(static_cast<unsigned>(L.max_tiles)), blk, 0, stream,  \
+                       w.keys[cur], vals, grad_out, p.meta_dev, w.ranges, p.T, w.ctl, w.tseg, w.edges, p.total_dim, \
+                       p.B * p.total_dim, grad_rows, capacity, status, w.partials, p.max_dim,                     \
+                       static_cast<const float *>(p.zero_page), ap->grad_idx, ap->seg_offsets, grad_row_offsets,   \
+                       static_cast<char *>(ap->tables), p.dtype, ap->state, ap->lr, ap->eps)
+#define TBE_REDUCE_APPLY_A(GT)                                                                                  \
+    do {                                                                                                        \
+        if (ap->adagrad) TBE_REDUCE_APPLY(GT, true); else TBE_REDUCE_APPLY(GT, false);                          \
+    } while (0)
+        if (p.out_dtype == TBE_F16) TBE_REDUCE_APPLY_A(TBE_F16);
+        else if (p.out_dtype == TBE_BF16) TBE_REDUCE_APPLY_A(TBE_BF16);
+        else TBE_REDUCE_APPLY_A(TBE_F32);
+#undef TBE_REDUCE_APPLY_A
+#undef TBE_REDUCE_APPLY
+    }
     if ((me = mk.upto(1)) != hipSuccess) return me;
     // one wave per run of 64 blocks, at most kCombineGroups workgroups
     const int64_t runs = (L.max_blocks + 63) / 64;
     const int64_t combine_groups = (runs + kWaves - 1) / kWaves < kCombineGroups ? (runs + kWaves - 1) / kWaves
                                                                                  : kCombineGroups;
-    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>(combine_groups)), blk, 0, stream, w.ranges, p.T,
-                       p.meta_dev, w.ctl, w.head, w.tail, w.partials, p.max_dim, grad_row_offsets, grad_rows,
-                       capacity);
+#define TBE_COMBINE(K, A)                                                                                       \
+    hipLaunchKernelGGL((combine_kernel<K, A>), dim3(static_cast<unsigned>(combine_groups)), blk, 0, stream, w.ranges, \
+                       p.T, p.meta_dev, w.ctl, w.head, w.tail, w.partials, p.max_dim, grad_row_offsets, grad_rows,  \
+                       capacity, ap ? ap->grad_idx : nullptr, ap ? static_cast<char *>(ap->tables) : nullptr,       \
+                       p.dtype, ap ? ap->state : nullptr, ap ? ap->lr : 0.f, ap ? ap->eps : 0.f)
+    if (!ap) TBE_COMBINE(false, false);
+    else if (ap->adagrad) TBE_COMBINE(true, true);
+    else TBE_COMBINE(true, false);
+#undef TBE_COMBINE
     const hipError_t e = hipGetLastError();
     return e != hipSuccess ? e : mk.upto(2);
 }
@@ -1402,13 +1534,26 @@ hipError_t launch_backward_reduce(const Plan &p, const void *grad_out, int64_t n
                                   void *workspace, float *grad_rows, int64_t grad_rows_capacity,
                                   const int64_t *grad_row_offsets, int32_t *status, hipStream_t stream,
                                   void *const *events) {
+    return launch_backward_reduce_apply(p, grad_out, num_indices, weighted, workspace, grad_rows, grad_rows_capacity,
+                                        nullptr, nullptr, grad_row_offsets, nullptr, 0, 0.f, 0.f, nullptr, status,
+                                        stream, events);
+}
+
+hipError_t launch_backward_reduce_apply(const Plan &p, const void *grad_out, int64_t num_indices, bool weighted,
+                                        void *workspace, float *grad_rows, int64_t grad_rows_capacity,
+                                        const int64_t *grad_idx, const int64_t *seg_offsets,
+                                        const int64_t *grad_row_offsets, void *tables, int32_t kind, float lr,
+                                        float eps, float *state, int32_t *status, hipStream_t stream,
+                                        void *const *events) {
     const Layout L = layout(p, num_indices);
     char *ws = static_cast<char *>(workspace);
+    const ApplyArgs a{tables, kind == TBE_OPT_ROWWISE_ADAGRAD, lr, eps, state, grad_idx, seg_offsets};
+    const ApplyArgs *ap = tables ? &a : nullptr;
     if (wide_values(p, weighted))
         return run_reduce<uint64_t>(p, grad_out, num_indices, ws, L, grad_rows, grad_rows_capacity, grad_row_offsets,
-                                    status, stream, events);
+                                    status, stream, events, ap);
     return run_reduce<uint32_t>(p, grad_out, num_indices, ws, L, grad_rows, grad_rows_capacity, grad_row_offsets,
-                                status, stream, events);
+                                status, stream, events, ap);
 }
 
 }  // namespace tbe

@@ -353,6 +353,32 @@ int32_t tbe_backward_reduce(const tbe_plan *plan, const void *grad_out, int64_t 
     return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
 }
 
+int32_t tbe_backward_reduce_apply(const tbe_plan *plan, const void *grad_out, int64_t num_indices,
+                                  const float *per_sample_weights, void *workspace, size_t workspace_bytes,
+                                  float *grad_rows, int64_t grad_rows_capacity, const int64_t *grad_idx,
+                                  const int64_t *seg_offsets, const int64_t *grad_row_offsets, void *tables,
+                                  const tbe_optimizer *opt, float *state, int32_t *status, void *stream,
+                                  void *const *phase_events) {
+    const tbe::Plan *p = plan_of(plan);
+    const int32_t rc = check_backward_reduce(p, grad_out, num_indices, workspace, workspace_bytes, grad_rows,
+                                             grad_rows_capacity, grad_row_offsets, status);
+    if (rc != TBE_OK) return rc;
+    if (!opt) return TBE_ERR_NULL;
+    if (opt->kind != TBE_OPT_SGD && opt->kind != TBE_OPT_ROWWISE_ADAGRAD) return TBE_ERR_SHAPE;
+    if (p->dtype == TBE_U8_ROWWISE) return TBE_ERR_UNSUPPORTED;
+    if (p->pooling == TBE_POOL_MEAN && per_sample_weights) return TBE_ERR_UNSUPPORTED;
+    if (!tables || !grad_idx || !seg_offsets) return TBE_ERR_NULL;
+    if (opt->kind == TBE_OPT_ROWWISE_ADAGRAD && !state) return TBE_ERR_NULL;
+    if (!aligned16(tables) || (reinterpret_cast<uintptr_t>(grad_idx) & 7u) ||
+        (reinterpret_cast<uintptr_t>(seg_offsets) & 7u) || (reinterpret_cast<uintptr_t>(state) & 3u))
+        return TBE_ERR_ALIGN;
+    const hipError_t e = tbe::launch_backward_reduce_apply(
+        *p, grad_out, num_indices, per_sample_weights != nullptr, workspace, grad_rows, grad_rows_capacity, grad_idx,
+        seg_offsets, grad_row_offsets, tables, opt->kind, opt->learning_rate, opt->eps, state, status,
+        static_cast<hipStream_t>(stream), phase_events);
+    return e == hipSuccess ? TBE_OK : TBE_ERR_HIP;
+}
+
 int32_t tbe_backward(const tbe_plan *plan, const void *grad_out, const void *indices,
                      const void *offsets, int64_t num_indices, const float *per_sample_weights,
                      void *workspace, size_t workspace_bytes, float *grad_rows,

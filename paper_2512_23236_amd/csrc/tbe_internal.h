@@ -80,6 +80,14 @@ hipError_t launch_backward_reduce(const Plan &p, const void *grad_out, int64_t n
                                   void *workspace, float *grad_rows, int64_t grad_rows_capacity,
                                   const int64_t *grad_row_offsets, int32_t *status, hipStream_t stream,
                                   void *const *events);
+// The reduce phase with the optimizer step applied by the same kernels
+// (tables != NULL; kind: tbe_optimizer_kind).
+hipError_t launch_backward_reduce_apply(const Plan &p, const void *grad_out, int64_t num_indices, bool weighted,
+                                        void *workspace, float *grad_rows, int64_t grad_rows_capacity,
+                                        const int64_t *grad_idx, const int64_t *seg_offsets,
+                                        const int64_t *grad_row_offsets, void *tables, int32_t kind, float lr,
+                                        float eps, float *state, int32_t *status, hipStream_t stream,
+                                        void *const *events);
 
 // The fixed device scratch of tbe_backward_noalloc: looked up once per device
 // (with that device current) by noalloc_scratch_init; noalloc_scratch returns

@@ -97,6 +97,9 @@ def _load():
         lib.tbe_backward_index.argtypes = [P, P, P, i64, P, P, ctypes.c_size_t, P, P, P, P, P, P, P]
         lib.tbe_backward_reduce.restype = i32
         lib.tbe_backward_reduce.argtypes = [P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P]
+        lib.tbe_backward_reduce_apply.restype = i32
+        lib.tbe_backward_reduce_apply.argtypes = [P, P, i64, P, P, ctypes.c_size_t, P, i64, P, P, P, P,
+                                                  ctypes.POINTER(_Opt), P, P, P, P]
         lib.tbe_backward_noalloc.restype = i32
         lib.tbe_backward_noalloc.argtypes = [P, P, P, P, i64, P, P, i64, P, P, P, P, P, P]
         if lib.tbe_abi_version() != ABI_VERSION:
@@ -461,6 +464,37 @@ def backward_reduce(plan: Plan, grad_out: torch.Tensor, num_indices: int, worksp
                                      _ptr(outputs.grad_rows), cap, _ptr(outputs.grad_row_offsets), _ptr(status),
                                      _stream(plan.device), _event_handles(events, 3, "events"))
     _check(rc, "tbe_backward_reduce")
+    return outputs
+
+
+def backward_reduce_apply(plan: Plan, grad_out: torch.Tensor, num_indices: int, workspace: torch.Tensor,
+                          outputs: SparseGrad, tables: torch.Tensor, kind: int, lr: float, eps: float = 0.0,
+                          state: Optional[torch.Tensor] = None, per_sample_weights: Optional[torch.Tensor] = None,
+                          grad_rows_capacity: Optional[int] = None, status: Optional[torch.Tensor] = None,
+                          events: Optional[Sequence[torch.cuda.Event]] = None) -> SparseGrad:
+    """tbe_backward_reduce_apply: the reduce phase after a backward_index, with
+    the optimizer step (SGD or row-wise Adagrad) made on `tables` (and
+    `state`) in place by the same kernels.  The gradient rows are written too.
+    events: 3 events (reduce, combine begin; the phase ends)."""
+    N = int(num_indices)
+    _check_grad_out(plan, grad_out)
+    _dev_tensor(tables, plan.dtype, "tables", plan)
+    if per_sample_weights is not None:
+        _dev_tensor(per_sample_weights, torch.float32, "per_sample_weights", plan)
+    if state is not None:
+        _dev_tensor(state, torch.float32, "state", plan)
+        if state.numel() != int(plan.rows.sum()):
+            raise ValueError("state must have one entry per table row (total_rows)")
+    cap = _check_outputs(plan, outputs, N, grad_rows_capacity)
+    workspace = _workspace(plan, N, workspace)
+    opt = _Opt(int(kind), float(lr), float(eps))
+    rc = _load().tbe_backward_reduce_apply(plan.handle, _ptr(grad_out), N, _ptr(per_sample_weights),
+                                           _ptr(workspace), workspace.numel(), _ptr(outputs.grad_rows), cap,
+                                           _ptr(outputs.grad_idx), _ptr(outputs.seg_offsets),
+                                           _ptr(outputs.grad_row_offsets), _ptr(tables), ctypes.byref(opt),
+                                           _ptr(state), _ptr(status), _stream(plan.device),
+                                           _event_handles(events, 3, "events"))
+    _check(rc, "tbe_backward_reduce_apply")
     return outputs
 
 
