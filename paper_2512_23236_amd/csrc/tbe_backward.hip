@@ -798,6 +798,7 @@ constexpr int kRing = 64;  // row loads in flight per reduce wave (one column pe
 // 32-bit-element resource.
 constexpr int64_t kBufferLimit = int64_t(1) << 31;
 constexpr int kBufferWord3 = 0x00020000;
+constexpr uint32_t kBufferOob = 0x80000000u;  // a per-lane offset past any resource's end (< kBufferLimit)
 
 // One wave walks one contiguous range of positions (kBlksPerWave blocks) in
 // order for one slice of slice_cols(GT) gradient columns, one position per step
@@ -841,10 +842,13 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     const uint32_t voff = vact ? static_cast<uint32_t>(lane * NC * GES) : 0u;  // bytes into a grad_out row
     const uint32_t doff = static_cast<uint32_t>(lane * NC * 4);                // bytes into an fp32 gradient row
     const char *const gbase = static_cast<const char *>(grad_out) + (m.dim_off + c0) * GES;
-    // grad_out below 2 GiB: rows are 32-bit byte offsets from gbase into a
-    // buffer resource; a step whose position is not owned reads through a
-    // resource of length 0, which returns zeros without a memory access
+    // grad_out below 2 GiB: rows are 32-bit byte offsets from gbase into one
+    // buffer resource; a step whose position is not owned uses an offset past
+    // the resource's end (kBufferOob), which returns zeros without a memory
+    // access
     const uint32_t gbytes = static_cast<uint32_t>((gout_elems - (m.dim_off + c0)) * GES);
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(gbase), 0, static_cast<int>(gbytes), kBufferWord3);
     float *const row_base = grad_rows + static_cast<int64_t>(pre.dimsum) + c0;
     float *const part_base = partials + part0 + c0;
     struct Raw {
@@ -902,7 +906,7 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
             const char *row = gbase + static_cast<int64_t>(b) * total_dim * GES;
             o.addr = reinterpret_cast<uint64_t>(own ? row : reinterpret_cast<const char *>(zero_page));
         } else {
-            o.addr = static_cast<uint32_t>(b) * static_cast<uint32_t>(total_dim * GES);
+            o.addr = own ? static_cast<uint32_t>(b) * static_cast<uint32_t>(total_dim * GES) : kBufferOob;
         }
         o.dst = reinterpret_cast<uint64_t>(dst);
         o.w = own ? wl : 0.f;
@@ -932,13 +936,14 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
                 d[1] = widen16<GT>(h >> 16);
             }
         } else {
-            const int n = ((ck.pmask >> j) & 1ull) ? static_cast<int>(gbytes) : 0;
-            const __amdgpu_buffer_rsrc_t rs =
-                __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(gbase), 0, n, kBufferWord3);
-            // lanes past the row slice read its first columns (voff), so every
-            // address stays inside grad_out
-            const int soff = static_cast<int>(rl(static_cast<uint32_t>(ck.addr), j));
-            const uint32_t h = __builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<int>(voff), soff, 0);
+            // the row's byte offset goes into the per-lane offset, which the
+            // buffer's range check covers: a position the wave does not own
+            // carries an offset past the end and reads zeros without a memory
+            // access, so one resource serves every step.  Lanes past the row
+            // slice read its first columns (voff), so every address stays
+            // inside grad_out.
+            const uint32_t vo = voff + rl(static_cast<uint32_t>(ck.addr), j);
+            const uint32_t h = __builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<int>(vo), 0, 0);
             if constexpr (GT == TBE_F32) {
                 d[0] = __uint_as_float(h);
             } else {
@@ -954,6 +959,10 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     float acc[NC];
 #pragma unroll
     for (int q = 0; q < NC; ++q) acc[q] = 0.f;
+    // One chunk of 64 steps.  A flush (a segment or piece end) is the rarer
+    // case, so it is laid out as the branch not taken and the common step runs
+    // straight through: the instructions per step, more than memory, set this
+    // loop's pace.
     for (int64_t c = r0;; c += 64) {
 #pragma unroll
         for (int j = 0; j < 64; ++j) {
@@ -961,7 +970,7 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
             const float w = kWeighted ? __int_as_float(static_cast<int>(rl(__float_as_uint(cur.w), j))) : 1.0f;
 #pragma unroll
             for (int q = 0; q < NC; ++q) acc[q] = __builtin_fmaf(w, ring[s][q], acc[q]);
-            if ((cur.fmask >> j) & 1ull) {
+            if (__builtin_expect((static_cast<uint32_t>(cur.fmask >> (j & 32)) >> (j & 31)) & 1u, 0)) {
                 const uint64_t dst = rl64(cur.dst, j);
                 if (vact) store_cols<NC>(dst, doff, acc);
 #pragma unroll
