@@ -12,10 +12,15 @@
 // in registers, loads up to 64 of the bag's indices with one coalesced load,
 // then issues the row loads of kAhead lookups per lane group before using
 // any, so rows stream with several loads in flight.  Each lane multiplies its
-// vector by the matching G columns in fp32 (fixed order), a fixed xor tree
-// sums across the lane group, and the group's first lane writes grad_w[j]:
-// one writer, fixed order, bitwise reproducible.  Like the forward the work
+// vector by the matching G columns in fp32 (fixed order); the kAhead partial
+// dot products of a round are summed across the lane group together, by
+// recursive halving (a fixed butterfly that exchanges half the remaining
+// values at each distance: kAhead - 1 shuffles for the round instead of
+// log2(LPR) per lookup), and the lane left holding a lookup's sum writes
+// grad_w[j]: one writer, fixed order, bitwise reproducible.  Like the forward the work
 // is bound by the row gathers (HBM, L2 and the Infinity Cache).
+
+#include <type_traits>
 
 #include "tbe_internal.h"
 
@@ -24,6 +29,7 @@ namespace {
 
 constexpr int kWgWaves = 4;
 constexpr int kAhead = 8;  // row loads in flight per lane group
+constexpr uint32_t kSkipRow = 0xffffffffu;  // no row to read (bounds check failed): the table has fewer rows
 
 // Widen element i (of kPerVec) of a 16-byte vector of table elements.
 template <int DT>
@@ -70,6 +76,59 @@ __device__ inline float grad_elem(const void *__restrict__ g, int64_t e) {
     }
 }
 
+// x of the lane at distance D (lane ^ D) within a group of lanes.  Distances
+// inside a 16-lane row are DPP moves (quad permutations; row rotations, where
+// a rotation by 8 is the xor and distance 4 picks between rotations by 4 and
+// 12); larger ones go through the LDS permute.
+template <int D>
+__device__ inline float xor_lane(float x, int v) {
+    const int xi = __float_as_int(x);
+    if constexpr (D == 1) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
+    } else if constexpr (D == 2) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
+    } else if constexpr (D == 4) {
+        const int a = __builtin_amdgcn_mov_dpp(xi, 0x124, 0xF, 0xF, false);  // row_ror:4
+        const int b = __builtin_amdgcn_mov_dpp(xi, 0x12C, 0xF, 0xF, false);  // row_ror:12
+        return __int_as_float((v & 4) ? a : b);
+    } else if constexpr (D == 8) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0x128, 0xF, 0xF, false));  // row_ror:8
+    } else {
+        return __shfl_xor(x, D);
+    }
+}
+
+// Sums x[0..kAhead) over the LPR lanes of a group, entry by entry: at each
+// distance D the lanes with bit D set keep the upper half of their remaining
+// N entries and add their partner's copy of it, the others the lower half;
+// with one entry left, the remaining distances add plainly.  Lane v ends with
+// the group sums of entries [v * M, v * M + M) in x[0..M) when LPR < kAhead
+// (M = kAhead / LPR), else of entry (v / (LPR / kAhead)) in x[0].
+template <int D, int N>
+__device__ inline void halve(float (&x)[kAhead], int v) {
+    if constexpr (D >= 1) {
+        if constexpr (N > 1) {
+            constexpr int H = N / 2;
+            const bool upper = (v & D) != 0;
+#pragma unroll
+            for (int i = 0; i < H; ++i) {
+                const float keep = upper ? x[i + H] : x[i];
+                const float send = upper ? x[i] : x[i + H];
+                x[i] = keep + xor_lane<D>(send, v);
+            }
+            halve<D / 2, H>(x, v);
+        } else {
+            x[0] = x[0] + xor_lane<D>(x[0], v);
+            halve<D / 2, 1>(x, v);
+        }
+    }
+}
+
+template <int LPR>
+__device__ inline void group_halving(float (&x)[kAhead], int v) {
+    halve<LPR / 2, kAhead>(x, v);
+}
+
 template <int DT, typename IT, int GT>
 __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
     const TableMeta *__restrict__ meta, const char *__restrict__ tables, const IT *__restrict__ indices,
@@ -94,13 +153,15 @@ __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
         e = ce;
     }
     if (e <= s) return;
-    const int lpr_log2 = m.lpr_log2;
-    const int LPR = 1 << lpr_log2, G = 64 >> lpr_log2;
-    const int g = lane >> lpr_log2, v = lane & (LPR - 1);
     const int64_t row_bytes = static_cast<int64_t>(m.nvec) * 16;
     const char *tab = tables + m.elem_offset * ES;
     const int64_t grow = b * total_dim + m.dim_off;  // first grad_out element of the bag's slice
     bool oob = false;
+    auto bag = [&](auto lpr) {
+    constexpr int LPR = decltype(lpr)::value, G = 64 / LPR;
+    constexpr int M = LPR < kAhead ? kAhead / LPR : 1;  // sums each lane holds after the halving
+    constexpr int SPREAD = LPR > kAhead ? LPR / kAhead : 1;  // lanes holding each sum
+    const int g = lane / LPR, v = lane % LPR;
     for (int c0 = 0; c0 < m.nvec; c0 += LPR) {  // chunks of 64 vectors (one chunk unless D is large)
         const bool vact = c0 + v < m.nvec;
         float gc[KV];
@@ -108,35 +169,56 @@ __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
         for (int i = 0; i < KV; ++i) gc[i] = vact ? grad_elem<GT>(grad_out, grow + (c0 + v) * KV + i) : 0.f;
         for (int64_t base = s; base < e; base += 64) {
             const int cnt = e - base < 64 ? static_cast<int>(e - base) : 64;
+            // lane l checks lookup base + l; its row id (or kSkip) is what the
+            // lane groups read, 32 bits per shuffle
             const int64_t my_idx = lane < cnt ? static_cast<int64_t>(indices[base + lane]) : 0;
+            const bool my_ok = lane < cnt && (!check || (my_idx >= 0 && my_idx < m.rows));
+            oob |= lane < cnt && !my_ok;
+            const uint32_t my_r = my_ok ? static_cast<uint32_t>(my_idx) : kSkipRow;
             for (int r0 = 0; r0 < cnt; r0 += G * kAhead) {
                 uint4 rowv[kAhead];
-                bool keep[kAhead];
 #pragma unroll
                 for (int u = 0; u < kAhead; ++u) {
                     const int i = r0 + u * G + g;
-                    const int64_t idx = __shfl(my_idx, i & 63);
-                    const bool in = i < cnt;
-                    const bool ok = in && (!check || (idx >= 0 && idx < m.rows));
-                    oob |= in && !ok;
-                    keep[u] = in;
-                    const char *addr = (ok && vact) ? tab + idx * row_bytes + static_cast<int64_t>(c0 + v) * 16
+                    const uint32_t r = static_cast<uint32_t>(__shfl(static_cast<int>(my_r), i & 63));
+                    const bool ok = i < cnt && r != kSkipRow;
+                    const char *addr = (ok && vact) ? tab + static_cast<int64_t>(r) * row_bytes +
+                                                          static_cast<int64_t>(c0 + v) * 16
                                                     : zero_page + v * 16;
                     rowv[u] = *reinterpret_cast<const uint4 *>(addr);
                 }
+                float x[kAhead];
 #pragma unroll
                 for (int u = 0; u < kAhead; ++u) {
                     float dot = 0.f;
 #pragma unroll
                     for (int i = 0; i < KV; ++i) dot = __builtin_fmaf(gc[i], Wide<DT>::at(rowv[u], i), dot);
-                    for (int off = LPR >> 1; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
-                    if (keep[u] && v == 0) {
-                        float *dst = grad_w + base + r0 + u * G + g;
-                        *dst = c0 == 0 ? dot : *dst + dot;
+                    x[u] = dot;
+                }
+                group_halving<LPR>(x, v);
+                if (v % SPREAD == 0) {
+#pragma unroll
+                    for (int j = 0; j < M; ++j) {
+                        const int u = LPR < kAhead ? v * M + j : v / SPREAD;
+                        const int i = r0 + u * G + g;
+                        if (i < cnt) {
+                            float *dst = grad_w + base + i;
+                            *dst = c0 == 0 ? x[j] : *dst + x[j];
+                        }
                     }
                 }
             }
         }
+    }
+    };
+    switch (m.lpr_log2) {
+        case 0: bag(std::integral_constant<int, 1>{}); break;
+        case 1: bag(std::integral_constant<int, 2>{}); break;
+        case 2: bag(std::integral_constant<int, 4>{}); break;
+        case 3: bag(std::integral_constant<int, 8>{}); break;
+        case 4: bag(std::integral_constant<int, 16>{}); break;
+        case 5: bag(std::integral_constant<int, 32>{}); break;
+        default: bag(std::integral_constant<int, 64>{}); break;
     }
     if (check && __ballot(oob) && lane == 0) atomicOr(status, TBE_STATUS_INDEX_OOB);
 }
