@@ -11,6 +11,8 @@
 // element is one fma rounded to the table format (round to nearest even).
 #pragma once
 
+#include <type_traits>
+
 #include "tbe_internal.h"
 
 namespace tbe {
@@ -86,12 +88,6 @@ __device__ inline int64_t lane_i64(int64_t x, int src) {
     return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-// Sum over the lane group (lanes sharing lane >> log2(LPR)), fixed xor order.
-__device__ inline float group_sum(float x, int lpr) {
-    for (int off = lpr >> 1; off > 0; off >>= 1) x += __shfl_xor(x, off);
-    return x;
-}
-
 __device__ inline float sumsq4(f4 g) {
     float s = g.x * g.x;
     s = __builtin_fmaf(g.y, g.y, s);
@@ -118,17 +114,17 @@ __device__ inline void update_rows(const TableMeta &m, char *__restrict__ tab, i
     using Q = Quad<DT>;
     constexpr int ES = DT == TBE_F32 ? 4 : 2;
     const int lane = threadIdx.x & 63;
-    const int lpr_log2 = m.glpr_log2;
-    const int LPR = 1 << lpr_log2, G = 64 >> lpr_log2;
-    const int grp = lane >> lpr_log2, v = lane & (LPR - 1);
     const int nq = m.dim >> 2;  // 4-column quads per row
     const float fd = static_cast<float>(m.dim);
-    if (nq <= LPR) {
-        // one quad per lane: kInFlight rows per lane group at once
+    // one quad per lane: kInFlight rows per lane group of LPR lanes at once
+    auto narrow = [&](auto lpr) {
+        constexpr int LPR = decltype(lpr)::value, G = 64 / LPR;
+        const int grp = lane / LPR, v = lane % LPR;
         for (int s = i; s < e; s += kInFlight * G) {
             int64_t g[kInFlight], o[kInFlight];
             bool has[kInFlight], act[kInFlight];
             f4 gr[kInFlight], wv[kInFlight];
+            float s0[kInFlight];  // the row's Adagrad state before the step
             char *p[kInFlight];
 #pragma unroll
             for (int k = 0; k < kInFlight; ++k) {
@@ -141,21 +137,34 @@ __device__ inline void update_rows(const TableMeta &m, char *__restrict__ tab, i
                 const f4 z = f4{0.f, 0.f, 0.f, 0.f};
                 gr[k] = act[k] ? *reinterpret_cast<const f4 *>(grad_rows + o[k] + v * 4) : z;
                 wv[k] = act[k] ? Q::load(p[k]) : z;
+                if constexpr (kAdagrad) s0[k] = has[k] ? state[g[k]] : 0.f;
             }
 #pragma unroll
             for (int k = 0; k < kInFlight; ++k) {
                 float step = lr;
                 if constexpr (kAdagrad) {
-                    const float sq = group_sum(sumsq4(gr[k]), LPR);
-                    const float sk = (has[k] ? state[g[k]] : 0.f) + sq / fd;
+                    const float sq = group_xsum<LPR>(sumsq4(gr[k]), v);
+                    const float sk = s0[k] + sq / fd;
                     if (has[k] && v == 0) state[g[k]] = sk;
                     step = lr / (sqrtf(sk) + eps);
                 }
                 if (act[k]) Q::store(p[k], update4(wv[k], gr[k], step));
             }
         }
+    };
+    if (nq <= (1 << m.glpr_log2)) {
+        switch (m.glpr_log2) {
+            case 0: narrow(std::integral_constant<int, 1>{}); break;
+            case 1: narrow(std::integral_constant<int, 2>{}); break;
+            case 2: narrow(std::integral_constant<int, 4>{}); break;
+            case 3: narrow(std::integral_constant<int, 8>{}); break;
+            case 4: narrow(std::integral_constant<int, 16>{}); break;
+            case 5: narrow(std::integral_constant<int, 32>{}); break;
+            default: narrow(std::integral_constant<int, 64>{}); break;
+        }
     } else {
         // wide rows (more quads than 64 lanes): one row at a time, in passes
+        const int v = lane;
         for (int r = i; r < e; ++r) {
             if ((skip >> (r & 63)) & 1ull) continue;
             const int64_t g = lane_i64(my_g, r), o = lane_i64(my_o, r);
@@ -164,7 +173,7 @@ __device__ inline void update_rows(const TableMeta &m, char *__restrict__ tab, i
             if constexpr (kAdagrad) {
                 float sq = 0.f;
                 for (int q = v; q < nq; q += 64) sq += sumsq4(*reinterpret_cast<const f4 *>(grad_rows + o + q * 4));
-                sq = group_sum(sq, 64);
+                sq = group_xsum<64>(sq, v);
                 const float sr = state[g] + sq / fd;
                 if (v == 0) state[g] = sr;
                 step = lr / (sqrtf(sr) + eps);

@@ -76,28 +76,6 @@ __device__ inline float grad_elem(const void *__restrict__ g, int64_t e) {
     }
 }
 
-// x of the lane at distance D (lane ^ D) within a group of lanes.  Distances
-// inside a 16-lane row are DPP moves (quad permutations; row rotations, where
-// a rotation by 8 is the xor and distance 4 picks between rotations by 4 and
-// 12); larger ones go through the LDS permute.
-template <int D>
-__device__ inline float xor_lane(float x, int v) {
-    const int xi = __float_as_int(x);
-    if constexpr (D == 1) {
-        return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
-    } else if constexpr (D == 2) {
-        return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
-    } else if constexpr (D == 4) {
-        const int a = __builtin_amdgcn_mov_dpp(xi, 0x124, 0xF, 0xF, false);  // row_ror:4
-        const int b = __builtin_amdgcn_mov_dpp(xi, 0x12C, 0xF, 0xF, false);  // row_ror:12
-        return __int_as_float((v & 4) ? a : b);
-    } else if constexpr (D == 8) {
-        return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0x128, 0xF, 0xF, false));  // row_ror:8
-    } else {
-        return __shfl_xor(x, D);
-    }
-}
-
 // Sums x[0..kAhead) over the LPR lanes of a group, entry by entry: at each
 // distance D the lanes with bit D set keep the upper half of their remaining
 // N entries and add their partner's copy of it, the others the lower half;
