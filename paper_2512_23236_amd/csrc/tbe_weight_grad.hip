@@ -23,6 +23,7 @@
 #include <type_traits>
 
 #include "tbe_internal.h"
+#include "tbe_lanes.h"
 
 namespace tbe {
 namespace {
