@@ -188,8 +188,8 @@ int32_t tbe_forward(const tbe_plan *plan, const void *tables, const void *indice
  *                       output is unspecified
  * Needs sum pooling and fp32 / fp16 / bf16 tables (else TBE_ERR_UNSUPPORTED).
  * One wavefront per bag; each entry has one writer and a fixed summation
- * order (per lane in column order, then a fixed tree across lanes), so results
- * are bitwise reproducible.
+ * order (per lane in column order, then a fixed butterfly across lanes), so
+ * results are bitwise reproducible.
  */
 int32_t tbe_weight_grad(const tbe_plan *plan, const void *tables, const void *grad_out, const void *indices,
                         const void *offsets, int64_t num_indices, float *grad_weights, int32_t *status,

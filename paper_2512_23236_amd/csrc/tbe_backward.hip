@@ -798,7 +798,9 @@ constexpr int kRing = 64;  // row loads in flight per reduce wave (one column pe
 // 32-bit-element resource.
 constexpr int64_t kBufferLimit = int64_t(1) << 31;
 constexpr int kBufferWord3 = 0x00020000;
-constexpr uint32_t kBufferOob = 0x80000000u;  // a per-lane offset past any resource's end (< kBufferLimit)
+// A per-lane offset past the end of every resource (each is below
+// kBufferLimit bytes): the load returns zeros without a memory access.
+constexpr uint32_t kBufferOob = 0x80000000u;
 
 // One wave walks one contiguous range of positions (kBlksPerWave blocks) in
 // order for one slice of slice_cols(GT) gradient columns, one position per step
@@ -808,7 +810,8 @@ constexpr uint32_t kBufferOob = 0x80000000u;  // a per-lane offset past any reso
 // chunk ahead, from key / value loads issued two chunks ahead; every step then
 // moves its position's values into scalar registers, so addressing and the
 // flush test are uniform.  A ring of kRing row loads stays in flight;
-// positions the wave does not own read the zero page with weight 0.
+// positions the wave does not own load zeros (an offset past the buffer's end,
+// or, for grad_out of 2 GiB and more, the zero page with weight 0).
 template <typename V, bool kWide, int GT>
 __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
                                    const void *__restrict__ grad_out, const TableMeta &m, const TileInfo &ti,

@@ -7,7 +7,7 @@
 // A row of D columns is updated by a lane group of LPR = D / 4 lanes (at most
 // 64), each lane moving 4 columns (a 16-byte gradient vector and 4 table
 // elements).  Arithmetic is fp32: the mean of squares is a per-lane chain
-// over its 4 columns then a fixed xor tree across the group, and each new
+// over its 4 columns then a fixed butterfly across the group, and each new
 // element is one fma rounded to the table format (round to nearest even).
 #pragma once
 
