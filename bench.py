@@ -469,6 +469,8 @@ def main():
                          "step alone, on the sparse gradient of one cfg5 backward; step_sgd / step_adagrad: the "
                          "training step with the optimizer made by the backward's reduce kernels, beside the "
                          "two-pass form")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured in a HIP graph and replayed (reported under 'graph')")
     ap.add_argument("--overlap-index", action="store_true",
                     help="queue the backward's index phase on a second stream beside the forward")
     ap.add_argument("--pooling", default="sum", choices=["sum", "mean"])
@@ -682,6 +684,30 @@ def main():
     # the roofline of the step's dominant kernel (the longest average launch)
     res["roofline"] = max(rf.values(), key=lambda r: r["ms"])
     res["roofline_forward"] = rf["forward_kernel"]
+    if args.graph:
+        # the same serial step captured once in a HIP graph and replayed (the
+        # library queues only kernels, so a step is graph nodes end to end);
+        # the saving is the host launch overhead between the step's kernels
+        warm = torch.cuda.Stream(dev)
+        warm.wait_stream(torch.cuda.current_stream(dev))
+        with torch.cuda.stream(warm):
+            serial_step()
+        torch.cuda.current_stream(dev).wait_stream(warm)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            serial_step()
+        graph.replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record()
+        for _ in range(args.steps):
+            graph.replay()
+        g1.record()
+        torch.cuda.synchronize()
+        res["graph"] = {"steps": args.steps, "step_ms": g0.elapsed_time(g1) / args.steps,
+                        "eager_step_ms": ms_per_step}
+        del graph
     if args.flushed_steps > 0:
         # secondary timing: every step starts with cold caches (1 GiB written
         # first, outside the timed events), parts serial
