@@ -53,10 +53,10 @@ static_assert(kBlk == 128 && kBlksPerTile <= 62, "reduce block indexing");
 constexpr int kBuckets = 1 << kRadixBits;
 constexpr uint32_t kSentinel = 0xffffffffu;
 constexpr int kPairLevels = 12;               // pairwise-sum depth in combine
-constexpr int kCombineGroups = 2048;          // combine grid (waves loop over runs of 64 blocks)
+constexpr int kCombineGroups = 1 << 16;       // combine grid (one-wave workgroups loop over tiles)
 constexpr int kKeyBags = 256;                 // bags per keys workgroup
 constexpr int kKeyAhead = 4;                  // keys kernel: lookup rounds whose loads are in flight together
-constexpr int kCombineBatch = 8;              // piece rows loaded at once in combine
+constexpr int kCombineBatch = 16;             // piece rows loaded at once in combine
 
 // Device control block at the start of the workspace.  The index phase
 // writes it; the reduce phase reads it.
@@ -789,7 +789,8 @@ __device__ inline int top_bit(uint64_t m) { return 63 - __clzll(static_cast<long
 struct TileEdges {
     uint64_t long_mask;                 // bit e: block edge e lies inside a long segment
     uint32_t starts[kBlksPerTile + 1];  // segment starts in the tile before block e
-    uint32_t pad[5];
+    uint32_t table;                     // the tile's table
+    uint32_t pad[4];
 };
 static_assert(sizeof(TileEdges) % 16 == 0, "TileEdges layout");
 
@@ -998,13 +999,14 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
 // wave per tile (lane e for block edge e): segment starts before each block
 // (from the per-block counts of the segment-count kernel), which block edges
 // lie inside a long segment (one with more than kBlk lookups), and the head /
-// tail pieces of every block (read by the combine kernel).
+// long segments that begin in each block with their piece counts (read by
+// the combine kernel).
 __global__ __launch_bounds__(64) void edges_kernel(const uint32_t *__restrict__ keys,
                                                    const uint32_t *__restrict__ blk_starts,
                                                    const int64_t *__restrict__ seg_offsets,
                                                    const Range *__restrict__ ranges, int T, Ctl *ctl,
                                                    const TileSeg *__restrict__ tseg,
-                                                   TileEdges *__restrict__ edges, int32_t *__restrict__ head_seg,
+                                                   TileEdges *__restrict__ edges, int32_t *__restrict__ tail_np,
                                                    int32_t *__restrict__ tail_seg) {
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->abort) return;
@@ -1029,18 +1031,33 @@ __global__ __launch_bounds__(64) void edges_kernel(const uint32_t *__restrict__ 
         const bool open = edge && pos > ti.start && pos < ti.end && kk != kSentinel && kk == kb;
         const uint32_t u = static_cast<uint32_t>(pre.starts) + before - 1u;  // segment open at the edge
         bool lng = false;
-        if (open) lng = seg_offsets[u + 1] - seg_offsets[u] > kBlk;
+        int32_t npc = 0;
+        if (open) {
+            const int64_t s0 = seg_offsets[u], s1 = seg_offsets[u + 1];
+            lng = s1 - s0 > kBlk;
+            // Pieces of the segment: the blocks from the one holding its first
+            // lookup through the one holding its last.  The tile's lookups
+            // before the segment's end are all kept (dropped lookups sort
+            // last in their table), so kept positions s - pre.kept are
+            // offsets from the tile's first position.  Used only where the
+            // segment begins in this tile (s0 >= pre.kept).
+            const int64_t k0 = static_cast<int64_t>(pre.kept);
+            if (lng && s0 >= k0) npc = static_cast<int32_t>((s1 - 1 - k0) / kBlk - (s0 - k0) / kBlk + 1);
+        }
         const uint64_t lmask = __ballot(lng);
         if (edge) edges[tile].starts[e] = before;
-        if (e == 0) edges[tile].long_mask = lmask;
+        if (e == 0) {
+            edges[tile].long_mask = lmask;
+            edges[tile].table = static_cast<uint32_t>(ti.t);
+        }
         const uint32_t u_next = __shfl(u, (e + 1) & 63);
+        const int32_t np_next = __shfl(npc, (e + 1) & 63);
         const bool valid = e < kBlksPerTile && pos < ti.p_hi;
-        const bool head = valid && lng;
         const bool tail = valid && ((lmask >> (e + 1)) & 1ull) && cnt > 0;
         const int64_t gq = tile * kBlksPerTile + e;
         if (e < kBlksPerTile) {
-            head_seg[gq] = head ? static_cast<int32_t>(u) : -1;
             tail_seg[gq] = tail ? static_cast<int32_t>(u_next) : -1;
+            tail_np[gq] = tail ? np_next : 0;
         }
     }
 }
@@ -1187,109 +1204,215 @@ __global__ __launch_bounds__(kThreads) void reduce_apply_kernel(
     }
 }
 
-// Sums the pieces of every segment that crosses a block edge, in a fixed
-// pairwise order (binary-counter summation over the pieces: the tail piece of
-// the block where the segment begins, then the head pieces of the blocks that
-// follow), and writes its gradient row once.  A wave takes a run of 64 blocks
-// and handles the segments whose tail piece lies in one of them.
+// Pairwise summation of a long segment's pieces in piece order, as a binary
+// counter: after n pieces, for each set bit l of n, the sum of an aligned run
+// of 2^l pieces (left operand always the earlier half), and the segment's sum
+// adds those runs from the largest to the smallest; runs of 2^kPairLevels
+// pieces go into `top` one after another.  The combine splits the counter at
+// level kRunLevel: whole runs of 2^kRunLevel pieces, each summed as a fixed
+// tree, are pushed into RunSum (levels kRunLevel and up); the segment's last
+// pieces, fewer than 2^kRunLevel, are counted by a position known at compile
+// time (levels below).  The state after each push is exactly that of pushing
+// the pieces one by one.
+constexpr int kRunLevel = 4;
+struct RunSum {
+    float4 st[kPairLevels - kRunLevel];  // st[l - kRunLevel]: level l
+    float4 top;
+    bool top_used;
+    uint32_t n;  // pieces so far, a multiple of 2^kRunLevel
+};
+
+__device__ inline float4 add4(const float4 &a, const float4 &b) {
+    return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+// Pushes an aligned run of 2^kFrom pieces, already summed (n a multiple of
+// 2^kFrom).
+template <int kFrom>
+__device__ __attribute__((always_inline)) inline void run_push(RunSum &rs, float4 x) {
+    static_assert(kFrom >= kRunLevel, "run level");
+    bool done = false;
+#pragma unroll
+    for (int l = kFrom; l < kPairLevels; ++l) {
+        if (!done) {
+            if ((rs.n >> l) & 1u) {
+                x = add4(rs.st[l - kRunLevel], x);
+            } else {
+                rs.st[l - kRunLevel] = x;
+                done = true;
+            }
+        }
+    }
+    if (!done) {
+        rs.top = rs.top_used ? add4(rs.top, x) : x;
+        rs.top_used = true;
+    }
+    rs.n += 1u << kFrom;
+}
+
+// Sum of the first `full` pieces' runs, from the largest; `have` tells whether
+// there was any.
+__device__ __attribute__((always_inline)) inline float4 run_total(const RunSum &rs, bool &have) {
+    float4 sum = rs.top;
+    have = rs.top_used;
+#pragma unroll
+    for (int l = kPairLevels - 1; l >= kRunLevel; --l) {
+        if ((rs.n >> l) & 1u) {
+            sum = have ? add4(sum, rs.st[l - kRunLevel]) : rs.st[l - kRunLevel];
+            have = true;
+        }
+    }
+    return sum;
+}
+
+// Sum of xs[0 .. 2^kRunLevel) as a fixed tree (the counter's run order).
+__device__ __attribute__((always_inline)) inline float4 run_tree(float4 (&xs)[1 << kRunLevel]) {
+#pragma unroll
+    for (int w = 1; w < (1 << kRunLevel); w *= 2) {
+#pragma unroll
+        for (int r = 0; r < (1 << kRunLevel); r += 2 * w) xs[r] = add4(xs[r], xs[r + w]);
+    }
+    return xs[0];
+}
+
+// The last rem (< 2^kRunLevel) pieces xs[0 .. rem), counted from an aligned
+// start, added after `sum` (have: whether sum holds anything) in the
+// counter's order: the runs of rem's set bits, largest first.
+__device__ __attribute__((always_inline)) inline float4 tail_total(float4 (&xs)[1 << kRunLevel], uint32_t rem,
+                                                                  float4 sum, bool have) {
+    float4 lo[kRunLevel];
+#pragma unroll
+    for (int l = 0; l < kRunLevel; ++l) lo[l] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int r = 0; r < (1 << kRunLevel) - 1; ++r) {
+        // push piece r with r pieces before it: the carries follow r's
+        // trailing ones, known here
+        float4 x = xs[r];
+        int l = 0;
+#pragma unroll
+        for (; l < kRunLevel && ((r >> l) & 1); ++l) x = add4(lo[l], x);
+        if (static_cast<uint32_t>(r) < rem) lo[l] = x;
+    }
+#pragma unroll
+    for (int l = kRunLevel - 1; l >= 0; --l) {
+        if ((rem >> l) & 1u) {
+            sum = have ? add4(sum, lo[l]) : lo[l];
+            have = true;
+        }
+    }
+    return sum;
+}
+
+// Sums the pieces of every long segment in the counter's order (the tail
+// piece of the block where the segment begins, then the head pieces of the
+// blocks that follow) and writes its gradient row once.  A wave takes one
+// tile and the long segments that begin in it.  A segment of at least
+// 2^kRunLevel pieces is summed a whole run at a time (the run's loads in
+// flight together, then its fixed tree; with rows of at most 32 quads the two
+// halves of the wave take two runs at once), then its last pieces; shorter
+// segments are summed in one round each, two at a time (one per half of the
+// wave) when the rows have at most 32 quads.
 // With kApply the combine then makes the optimizer step on each row it wrote
 // (kAdagrad: row-wise Adagrad, else SGD), as reduce_apply_kernel does for
 // short segments.
 template <bool kApply, bool kAdagrad>
-__global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restrict__ ranges, int T,
-                                                           const TableMeta *__restrict__ meta,
+__global__ __launch_bounds__(64) void combine_kernel(const TableMeta *__restrict__ meta,
                                                            const Ctl *__restrict__ ctl,
-                                                           const int32_t *__restrict__ head_seg,
+                                                           const TileEdges *__restrict__ edges,
+                                                           const int32_t *__restrict__ tail_np,
                                                            const int32_t *__restrict__ tail_seg,
                                                            const float *__restrict__ partials, int max_dim,
                                                            const int64_t *__restrict__ grad_row_offsets,
                                                            float *__restrict__ grad_rows, int64_t capacity,
                                                            const int64_t *__restrict__ grad_idx, char *__restrict__ tables,
                                                            int dt, float *__restrict__ state, float lr, float eps) {
+    constexpr int kB = 1 << kRunLevel;
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (ctl->abort || ctl->total_floats > capacity) return;
-    const int64_t nblk = ctl->total_tiles * kBlksPerTile;
-    // waves take runs of 64 blocks and sum the segments whose tail piece lies
-    // in one of them (tail_seg >= 0), lowest block first
-    for (int64_t b0 = (static_cast<int64_t>(blockIdx.x) * kWaves + wave) * 64; b0 < nblk;
-         b0 += static_cast<int64_t>(gridDim.x) * kWaves * 64) {
-        uint64_t todo = __ballot(b0 + lane < nblk && tail_seg[b0 + lane] >= 0);
-        while (todo) {
-            const int64_t q = b0 + __builtin_ctzll(todo);
-            todo &= todo - 1;
-            const int32_t u = tail_seg[q];
-            const int t = find_table(ranges, T, q / kBlksPerTile);
-            const int nvec = meta[t].dim / 4;
-            float *out = grad_rows + grad_row_offsets[u];
-            // pieces: the tail of block q, then the heads of blocks q+1 .. q+nh
-            int64_t nh = 0;
-            for (;;) {
-                const int64_t qq = q + 1 + nh + lane;
-                const bool same = qq < nblk && head_seg[qq] == u;
-                const uint64_t run = ~__ballot(same);  // first lane that is not a head of u
-                const int c = run ? __ffsll(static_cast<long long>(run)) - 1 : 64;
-                nh += c;
-                if (c < 64) break;
-            }
-            const int64_t npieces = nh + 1;
-            for (int c0 = 0; c0 < nvec; c0 += 64) {
-                const int cv = c0 + lane;
-                const bool act = cv < nvec;
-                float4 st[kPairLevels];
-                float4 top = make_float4(0.f, 0.f, 0.f, 0.f);
-                bool top_used = false;
-                uint32_t n = 0;
-                // piece p lives in partial slot 2q+1 (p = 0) or 2(q+p) (p > 0)
-                auto slot_of = [&](int64_t pc) { return pc == 0 ? 2 * q + 1 : 2 * (q + pc); };
-                for (int64_t p0 = 0; p0 < npieces; p0 += kCombineBatch) {
-                    float4 xs[kCombineBatch];
+    const int64_t tiles = ctl->total_tiles, nblk = tiles * kBlksPerTile;
+    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+        // lane j: the long segment that begins in block j of the tile, if any
+        const int64_t q = tile * kBlksPerTile + lane;
+        const int32_t u = lane < kBlksPerTile ? tail_seg[q] : -1;
+        const int t = static_cast<int>(uni(edges[tile].table));
+        const uint64_t segs = __ballot(u >= 0);
+        if (!segs) continue;
+        uint32_t np = 0;
+        int64_t my_o = 0, my_g = 0;
+        if (u >= 0) {
+            const int64_t n = tail_np[q];
+            np = static_cast<uint32_t>(n < 1 ? 1 : (n > nblk - q ? nblk - q : n));  // within the block list
+            my_o = grad_row_offsets[u];
+            if constexpr (kApply) my_g = grad_idx[u];
+        }
+        const TableMeta m = meta[t];
+        const int nvec = m.dim / 4;
+        // rows of at most 32 quads: the halves of the wave work side by side
+        // (half h on columns lane & 31)
+        const bool halves = nvec <= 32;
+        const int h = halves ? lane >> 5 : 0;
+        // piece pc of the segment whose tail piece is in block sq lives in
+        // partial slot 2sq+1 (pc = 0) or 2(sq+pc) (pc > 0)
+        auto slot_row = [&](int64_t sq, uint32_t pc) {
+            return partials + (pc == 0 ? 2 * sq + 1 : 2 * (sq + pc)) * max_dim;
+        };
+        for (int c0 = 0; c0 < nvec; c0 += 64) {
+            const int cw = halves ? (lane & 31) : c0 + lane;
+            const bool aw = cw < nvec;
+            // a wave-uniform row plus the lane's 32-bit byte offset (its
+            // columns, and `extra` bytes further)
+            auto piece = [&](int64_t sq, uint32_t pc, uint32_t extra = 0u) {
+                const gptr<char> row = reinterpret_cast<gptr<char>>(reinterpret_cast<uint64_t>(slot_row(sq, pc)));
+                const f32x4 x = *reinterpret_cast<gptr<f32x4>>(row + (static_cast<uint32_t>(cw) * 16u + extra));
+                return make_float4(x.x, x.y, x.z, x.w);
+            };
+            for (uint64_t bs = segs; bs; bs &= bs - 1) {
+                const int sl = __builtin_ctzll(bs);
+                const uint32_t snp = __builtin_amdgcn_readlane(np, sl);
+                const int64_t sq = tile * kBlksPerTile + sl;
+                RunSum rs;
+                rs.top = zero;
+                rs.top_used = false;
+                rs.n = 0;
+                const uint32_t full = snp / kB * kB;
+                float4 xs[kB];
+                uint32_t p0 = 0;
+                if (halves) {
+                    // half h sums the run at p0 + h kB; the two sums, earlier
+                    // plus later, make the run of 2 kB pieces (the same value
+                    // in both halves, as the sum commutes)
+                    // piece p0 + kB + r lies 2 kB slots past piece p0 + r
+                    // (2 kB - 1 past piece 0, which sits in the tail slot)
+                    const uint32_t row_bytes = static_cast<uint32_t>(max_dim) * 4u;
+                    const uint32_t skip = h ? 2u * kB * row_bytes : 0u;
+                    for (; p0 + 2 * kB <= full; p0 += 2 * kB) {
 #pragma unroll
-                    for (int r = 0; r < kCombineBatch; ++r) {
-                        const int64_t pc = p0 + r < npieces ? p0 + r : npieces - 1;  // clamped, unconditional
-                        xs[r] = act ? *reinterpret_cast<const float4 *>(partials + slot_of(pc) * max_dim + cv * 4)
-                                    : make_float4(0.f, 0.f, 0.f, 0.f);
-                    }
-#pragma unroll
-                    for (int r = 0; r < kCombineBatch; ++r) {
-                        if (p0 + r >= npieces) break;
-                        float4 x = xs[r];
-                        bool done = false;
-#pragma unroll
-                        for (int l = 0; l < kPairLevels; ++l) {
-                            if (!done) {
-                                if ((n >> l) & 1u) {
-                                    x = make_float4(st[l].x + x.x, st[l].y + x.y, st[l].z + x.z, st[l].w + x.w);
-                                } else {
-                                    st[l] = x;
-                                    done = true;
-                                }
-                            }
-                        }
-                        if (!done) {
-                            top = top_used ? make_float4(top.x + x.x, top.y + x.y, top.z + x.z, top.w + x.w) : x;
-                            top_used = true;
-                        }
-                        ++n;
-                    }
-                }
-                float4 sum = top;
-                bool have = top_used;
-#pragma unroll
-                for (int l = kPairLevels - 1; l >= 0; --l) {
-                    if ((n >> l) & 1u) {
-                        sum = have ? make_float4(sum.x + st[l].x, sum.y + st[l].y, sum.z + st[l].z, sum.w + st[l].w)
-                                   : st[l];
-                        have = true;
+                        for (int r = 0; r < kB; ++r)
+                            xs[r] = aw ? piece(sq, p0 + r, r == 0 && p0 == 0 && h ? skip - row_bytes : skip) : zero;
+                        const float4 a = run_tree(xs);
+                        const float4 o = make_float4(xor_lane<32>(a.x, lane), xor_lane<32>(a.y, lane),
+                                                     xor_lane<32>(a.z, lane), xor_lane<32>(a.w, lane));
+                        run_push<kRunLevel + 1>(rs, add4(a, o));
                     }
                 }
-                if (act) store4(out + cv * 4, sum);
+                for (; p0 < full; p0 += kB) {
+#pragma unroll
+                    for (int r = 0; r < kB; ++r) xs[r] = aw ? piece(sq, p0 + r) : zero;
+                    run_push<kRunLevel>(rs, run_tree(xs));
+                }
+                bool have;
+                const float4 hi = run_total(rs, have);
+                const uint32_t rem = snp - full;
+#pragma unroll
+                for (int r = 0; r < kB - 1; ++r) xs[r] = aw && static_cast<uint32_t>(r) < rem ? piece(sq, full + r) : zero;
+                const float4 sum = tail_total(xs, rem, hi, have);
+                if (aw && h == 0) store4(grad_rows + opt::lane_i64(my_o, sl) + cw * 4, sum);
             }
-            if constexpr (kApply) {
-                stores_then_loads();
-                update_rows_any<kAdagrad>(dt, meta[t], tables, state, grad_rows, grad_idx[u], grad_row_offsets[u], 0,
-                                          1, 0ull, lr, eps);
-            }
+        }
+        if constexpr (kApply) {
+            stores_then_loads();
+            update_rows_any<kAdagrad>(dt, m, tables, state, grad_rows, my_g, my_o, 0, kBlksPerTile, ~segs, lr, eps);
         }
     }
 }
@@ -1297,7 +1420,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const Range *__restri
 // ------------------------------------------------------------- workspace
 
 struct Layout {
-    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, totals, tseg, edges, blk_starts, head, tail, partials, total;
+    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, totals, tseg, edges, blk_starts, tail_np, tail, partials, total;
     int64_t max_tiles, max_blocks, max_works;
 };
 
@@ -1326,7 +1449,7 @@ Layout layout(const Plan &p, int64_t N) {
     L.tseg = take(sizeof(TileSeg) * L.max_tiles);
     L.edges = take(sizeof(TileEdges) * L.max_tiles);
     L.blk_starts = take(sizeof(uint32_t) * L.max_blocks);
-    L.head = take(sizeof(int32_t) * L.max_blocks);
+    L.tail_np = take(sizeof(int32_t) * L.max_blocks);
     L.tail = take(sizeof(int32_t) * L.max_blocks);
     L.partials = take(sizeof(float) * 2 * L.max_blocks * static_cast<size_t>(p.max_dim));
     L.total = o;
@@ -1343,7 +1466,7 @@ struct Ws {
     TileSeg *tseg;
     TileEdges *edges;
     uint32_t *blk_starts;
-    int32_t *head, *tail;
+    int32_t *tail_np, *tail;
     float *partials;
 };
 
@@ -1360,7 +1483,7 @@ Ws carve(char *ws, const Layout &L) {
     w.tseg = reinterpret_cast<TileSeg *>(ws + L.tseg);
     w.edges = reinterpret_cast<TileEdges *>(ws + L.edges);
     w.blk_starts = reinterpret_cast<uint32_t *>(ws + L.blk_starts);
-    w.head = reinterpret_cast<int32_t *>(ws + L.head);
+    w.tail_np = reinterpret_cast<int32_t *>(ws + L.tail_np);
     w.tail = reinterpret_cast<int32_t *>(ws + L.tail);
     w.partials = reinterpret_cast<float *>(ws + L.partials);
     return w;
@@ -1449,7 +1572,7 @@ hipError_t run_index(const Plan &p, const IT *indices, const IT *offsets, int64_
     hipLaunchKernelGGL(seg_write_kernel, tiles, blk, 0, stream, w.keys[cur], p.meta_dev, w.ranges, T, w.ctl, w.tseg,
                        grad_idx, seg_offsets, grad_row_offsets);
     hipLaunchKernelGGL(edges_kernel, tiles, dim3(64), 0, stream, w.keys[cur], w.blk_starts, seg_offsets, w.ranges,
-                       T, w.ctl, w.tseg, w.edges, w.head, w.tail);
+                       T, w.ctl, w.tseg, w.edges, w.tail_np, w.tail);
     const hipError_t e = hipGetLastError();
     return e != hipSuccess ? e : mk.upto(3);
 }
@@ -1498,13 +1621,12 @@ hipError_t run_reduce(const Plan &p, const void *grad_out, int64_t N, char *ws, 
 #undef TBE_REDUCE_APPLY
     }
     if ((me = mk.upto(1)) != hipSuccess) return me;
-    // one wave per run of 64 blocks, at most kCombineGroups workgroups
-    const int64_t runs = (L.max_blocks + 63) / 64;
-    const int64_t combine_groups = (runs + kWaves - 1) / kWaves < kCombineGroups ? (runs + kWaves - 1) / kWaves
-                                                                                 : kCombineGroups;
+    // one one-wave workgroup per tile (a wave that sums a hot row's pieces
+    // holds no sibling waves), at most kCombineGroups of them
+    const int64_t combine_groups = L.max_tiles < kCombineGroups ? L.max_tiles : kCombineGroups;
 #define TBE_COMBINE(K, A)                                                                                       \
-    hipLaunchKernelGGL((combine_kernel<K, A>), dim3(static_cast<unsigned>(combine_groups)), blk, 0, stream, w.ranges, \
-                       p.T, p.meta_dev, w.ctl, w.head, w.tail, w.partials, p.max_dim, grad_row_offsets, grad_rows,  \
+    hipLaunchKernelGGL((combine_kernel<K, A>), dim3(static_cast<unsigned>(combine_groups)), dim3(64), 0, stream,    \
+                       p.meta_dev, w.ctl, w.edges, w.tail_np, w.tail, w.partials, p.max_dim, grad_row_offsets, grad_rows,  \
                        capacity, ap ? ap->grad_idx : nullptr, ap ? static_cast<char *>(ap->tables) : nullptr,       \
                        p.dtype, ap ? ap->state : nullptr, ap ? ap->lr : 0.f, ap ? ap->eps : 0.f)
     if (!ap) TBE_COMBINE(false, false);
