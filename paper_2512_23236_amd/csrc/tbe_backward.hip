@@ -233,6 +233,12 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__
 // (L = the bag's lookup count, read from the staged offsets).  A table's keys
 // go to the buffer from which its own sort_passes radix passes end in buffer
 // passes & 1, where every table's sorted keys then lie.
+//
+// The kernel also counts the first radix pass's digits (key & mask0) per tile
+// into `hist` (zeroed beforehand), so that pass needs no histogram kernel: the
+// run's lookups fall in a few consecutive tiles, counted in LDS for the first
+// kKeyTiles of them (global atomics beyond) and added to `hist` at the end.
+constexpr int kKeyTiles = 8;
 template <typename V, typename IT>
 __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restrict__ meta,
                                                         const IT *__restrict__ indices,
@@ -242,11 +248,15 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
                                                         int64_t nbags, int check, Ctl *ctl,
                                                         uint32_t *__restrict__ keys0, uint32_t *__restrict__ keys1,
                                                         V *__restrict__ vals0, V *__restrict__ vals1, int passes,
+                                                        uint32_t mask0, uint32_t *__restrict__ hist,
                                                         int32_t *status) {
     __shared__ int64_t off[kKeyBags + 1];
     __shared__ int64_t bag_rows[kKeyBags];  // R_t of each bag's table
+    __shared__ int64_t bag_tile[kKeyBags];  // kTile * (the table's first tile) - (its first position)
     __shared__ uint32_t bag_b[kKeyBags];    // batch row of each bag
     __shared__ uint8_t bag_buf[kKeyBags];   // buffer the bag's table starts its sort in
+    __shared__ uint32_t h0[kKeyTiles * kBuckets];  // first-pass digit counts of the run's first tiles
+    __shared__ int64_t tile_lo;
     __shared__ int bad;
     const int tid = threadIdx.x;
     const int64_t k0 = static_cast<int64_t>(blockIdx.x) * kKeyBags;
@@ -254,12 +264,16 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
     const int nk = nbags - k0 < kKeyBags ? static_cast<int>(nbags - k0) : kKeyBags;
     if (tid == 0) bad = 0;
     for (int i = tid; i <= nk; i += kThreads) off[i] = static_cast<int64_t>(offsets[k0 + i]);
+    for (int i = tid; i < kKeyTiles * kBuckets; i += kThreads) h0[i] = 0u;
     // table and batch row once per bag, not per lookup
     for (int i = tid; i < nk; i += kThreads) {
         const int64_t t = (k0 + i) / B;
         bag_b[i] = static_cast<uint32_t>(k0 + i - t * B);
         bag_rows[i] = meta[t].rows;
         bag_buf[i] = static_cast<uint8_t>((passes - meta[t].sort_passes) & 1);
+        // position j of the bag's table lies in tile (bag_tile + j) / kTile
+        const Range r = ranges[t];
+        bag_tile[i] = r.tile_base * kTile - r.start;
     }
     __syncthreads();
     if (check) {
@@ -280,6 +294,18 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         }
     }
     const int64_t first = off[0], last = off[nk];
+    if (first >= last) return;
+    auto bag_of = [&](int64_t j) {  // off[lo] <= j < off[lo + 1]
+        int lo = 0, hi = nk;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (off[mid] <= j) lo = mid; else hi = mid;
+        }
+        return lo;
+    };
+    if (tid == 0) tile_lo = (bag_tile[bag_of(first)] + first) / kTile;
+    __syncthreads();
+    const int64_t t_lo = tile_lo;
     // kKeyAhead rounds of the run's lookups at a time: their index (and
     // weight) loads are all issued before the first is used
     for (int64_t j0 = first + tid; j0 < last; j0 += static_cast<int64_t>(kThreads) * kKeyAhead) {
@@ -295,11 +321,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         for (int r = 0; r < kKeyAhead; ++r) {
             const int64_t j = j0 + static_cast<int64_t>(r) * kThreads;
             if (j >= last) break;
-            int lo = 0, hi = nk;  // off[lo] <= j < off[hi]
-            while (hi - lo > 1) {
-                const int mid = (lo + hi) >> 1;
-                if (off[mid] <= j) lo = mid; else hi = mid;
-            }
+            const int lo = bag_of(j);
             const uint32_t b = bag_b[lo];
             const int64_t idx = ids[r];
             uint32_t key = static_cast<uint32_t>(idx);
@@ -311,6 +333,10 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
             uint32_t *const keys = second ? keys1 : keys0;
             V *const vals = second ? vals1 : vals0;
             keys[j] = key;
+            const int64_t tj = (bag_tile[lo] + j) / kTile;  // the lookup's tile
+            const uint32_t d = key & mask0;
+            if (tj - t_lo < kKeyTiles) atomicAdd(&h0[(tj - t_lo) * kBuckets + d], 1u);
+            else atomicAdd(&hist[tj * kBuckets + d], 1u);
             if constexpr (sizeof(V) == 8) {
                 const float w = mean ? 1.0f / static_cast<float>(off[lo + 1] - off[lo]) : wts[r];
                 vals[j] = static_cast<uint64_t>(b) | (static_cast<uint64_t>(__float_as_uint(w)) << 32);
@@ -319,6 +345,22 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
             }
         }
     }
+    __syncthreads();
+    for (int i = tid; i < kKeyTiles * kBuckets; i += kThreads) {
+        const uint32_t c = h0[i];
+        if (c) atomicAdd(&hist[(t_lo + i / kBuckets) * kBuckets + i % kBuckets], c);
+    }
+}
+
+// Zeroes the tile-count rows of every tile (the first radix pass's counts are
+// added into them by the keys kernel).
+__global__ __launch_bounds__(kThreads) void hist_zero_kernel(uint32_t *__restrict__ hist, const Ctl *__restrict__ ctl) {
+    if (ctl->abort) return;
+    const int64_t n = ctl->total_tiles * kBuckets / 4;  // uint4 words
+    uint4 *const h = reinterpret_cast<uint4 *>(hist);
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * kThreads)
+        h[i] = make_uint4(0u, 0u, 0u, 0u);
 }
 
 // ------------------------------------------------------------ radix sort
@@ -382,31 +424,55 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__
 
 // Per table, per digit: the exclusive prefix of the digit's counts over the
 // table's tiles (in place), and the digit's total over the table.  One
-// workgroup per table, one thread per digit; a wave's loads cover 64
-// consecutive digits of one tile row (coalesced), several tiles in flight.
+// workgroup per table: kColGroups groups of one thread per digit, group g on
+// the g-th contiguous share of the table's tiles (a wave's loads cover 64
+// consecutive digits of one tile row, coalesced, several tiles in flight).
+// Each group sums its share, the groups' sums are scanned in LDS, and each
+// group then writes its share's prefixes.
 constexpr int kColAhead = 8;
+constexpr int kColGroups = 4;
+constexpr int kColThreads = kColGroups * kBuckets;
 
-__global__ __launch_bounds__(kThreads) void col_scan_kernel(uint32_t *__restrict__ hist,
-                                                            uint32_t *__restrict__ totals,
-                                                            const TableMeta *__restrict__ meta,
-                                                            const Range *__restrict__ ranges,
-                                                            const Ctl *__restrict__ ctl, int pass) {
+__global__ __launch_bounds__(kColThreads) void col_scan_kernel(uint32_t *__restrict__ hist,
+                                                               uint32_t *__restrict__ totals,
+                                                               const TableMeta *__restrict__ meta,
+                                                               const Range *__restrict__ ranges,
+                                                               const Ctl *__restrict__ ctl, int pass) {
+    __shared__ uint32_t gsum[kColGroups][kBuckets];
     if (ctl->abort) return;
-    const int t = blockIdx.x, d = threadIdx.x;
+    const int t = blockIdx.x, d = threadIdx.x % kBuckets, g = threadIdx.x / kBuckets;
     if (pass >= meta[t].sort_passes) return;
     const int64_t t0 = ranges[t].tile_base, t1 = ranges[t + 1].tile_base;
-    uint32_t run = 0;
-    for (int64_t c = t0; c < t1; c += kColAhead) {
+    const int64_t share = (t1 - t0 + kColGroups - 1) / kColGroups;
+    const int64_t c0 = t0 + g * share < t1 ? t0 + g * share : t1;
+    const int64_t c1 = c0 + share < t1 ? c0 + share : t1;
+    uint32_t sum = 0;
+    for (int64_t c = c0; c < c1; c += kColAhead) {
         uint32_t h[kColAhead];
 #pragma unroll
-        for (int r = 0; r < kColAhead; ++r) h[r] = c + r < t1 ? hist[(c + r) * kBuckets + d] : 0u;
+        for (int r = 0; r < kColAhead; ++r) h[r] = c + r < c1 ? hist[(c + r) * kBuckets + d] : 0u;
+#pragma unroll
+        for (int r = 0; r < kColAhead; ++r) sum += h[r];
+    }
+    gsum[g][d] = sum;
+    __syncthreads();
+    uint32_t run = 0, total = 0;
+#pragma unroll
+    for (int k = 0; k < kColGroups; ++k) {
+        if (k < g) run += gsum[k][d];
+        total += gsum[k][d];
+    }
+    for (int64_t c = c0; c < c1; c += kColAhead) {
+        uint32_t h[kColAhead];
+#pragma unroll
+        for (int r = 0; r < kColAhead; ++r) h[r] = c + r < c1 ? hist[(c + r) * kBuckets + d] : 0u;
 #pragma unroll
         for (int r = 0; r < kColAhead; ++r) {
-            if (c + r < t1) hist[(c + r) * kBuckets + d] = run;
+            if (c + r < c1) hist[(c + r) * kBuckets + d] = run;
             run += h[r];
         }
     }
-    totals[static_cast<int64_t>(t) * kBuckets + d] = run;
+    if (g == 0) totals[static_cast<int64_t>(t) * kBuckets + d] = total;
 }
 
 template <typename V>
@@ -1548,17 +1614,23 @@ hipError_t run_index(const Plan &p, const IT *indices, const IT *offsets, int64_
     const int mean = p.pooling == TBE_POOL_MEAN;
     const int bits = sort_bits(p);
     const int passes = sort_passes_all(p);
+    const int nb0 = bits < kRadixBits ? bits : kRadixBits;  // the first pass's digit bits
+    const int64_t zero_groups = L.max_tiles < 1024 ? L.max_tiles : 1024;
+    hipLaunchKernelGGL(hist_zero_kernel, dim3(static_cast<unsigned>(zero_groups)), dim3(kThreads), 0, stream, w.hist,
+                       w.ctl);
     hipLaunchKernelGGL((keys_kernel<V, IT>), dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)),
                        dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights, mean, w.ranges, p.B, nbags,
-                       check, w.ctl, w.keys[0], w.keys[1], vals[0], vals[1], passes, status);
+                       check, w.ctl, w.keys[0], w.keys[1], vals[0], vals[1], passes, (1u << nb0) - 1u, w.hist,
+                       status);
     const dim3 tiles(static_cast<unsigned>(L.max_tiles)), blk(kThreads);
     if ((me = mk.upto(1)) != hipSuccess) return me;
     for (int pass = 0; pass < passes; ++pass) {
         const int shift = pass * kRadixBits;
         const int nb = bits - shift < kRadixBits ? bits - shift : kRadixBits;
-        hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, w.keys[0], w.keys[1], p.meta_dev, w.ranges, T,
-                           w.ctl, pass, passes, shift, nb, w.hist);
-        hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), blk, 0, stream, w.hist, w.totals,
+        if (pass > 0)  // the first pass's counts come from the keys kernel
+            hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, w.keys[0], w.keys[1], p.meta_dev, w.ranges,
+                               T, w.ctl, pass, passes, shift, nb, w.hist);
+        hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), dim3(kColThreads), 0, stream, w.hist, w.totals,
                            p.meta_dev, w.ranges, w.ctl, pass);
         hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, blk, 0, stream, w.keys[0], w.keys[1], vals[0], vals[1],
                            w.hist, w.totals, p.meta_dev, w.ranges, T, w.ctl, pass, passes, shift, nb);
