@@ -27,10 +27,61 @@
 // Infinity Cache that serve hot rows): about one fma per element read, far
 // below the fp32 vector ridge point.
 
+#include <type_traits>
+#include <utility>
+
 #include "tbe_internal.h"
 
 namespace tbe {
 namespace {
+
+// f(integral_constant<int, S>) for S = 0 .. N-1, in order.
+template <typename F, int... S>
+__device__ inline void static_for_seq(F &&f, std::integer_sequence<int, S...>) {
+    (f(std::integral_constant<int, S>{}), ...);
+}
+template <int N, typename F>
+__device__ inline void static_for(F &&f) {
+    static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// x of lane c (wave-uniform) of this lane's group of LPR >= 32 lanes.
+template <int LPR>
+__device__ inline uint32_t group_lane_at(uint32_t x, int c) {
+    static_assert(LPR == 32 || LPR == 64, "lane reads");
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x), c));
+    if constexpr (LPR == 64) {
+        return lo;
+    } else {
+        const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x), 32 + c));
+        return (threadIdx.x & 32) ? hi : lo;
+    }
+}
+
+// x of lane C of this lane's group of LPR lanes (groups of consecutive
+// lanes), without the LDS: DPP quad permutations for groups of 2 and 4, row
+// broadcasts (row_newbcast) for 8 and 16, lane reads for 32 and 64.
+template <int LPR, int C>
+__device__ inline uint32_t group_lane(uint32_t x) {
+    static_assert(C >= 0 && C < LPR, "lane");
+    const int xi = static_cast<int>(x);
+    if constexpr (LPR == 1) {
+        return x;
+    } else if constexpr (LPR == 2) {
+        return static_cast<uint32_t>(
+            __builtin_amdgcn_mov_dpp(xi, C | (C << 2) | ((2 + C) << 4) | ((2 + C) << 6), 0xF, 0xF, false));
+    } else if constexpr (LPR == 4) {
+        return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(xi, C * 0x55, 0xF, 0xF, false));
+    } else if constexpr (LPR == 8) {
+        const int a = __builtin_amdgcn_mov_dpp(xi, 0x150 + C, 0xF, 0xF, false);
+        const int b = __builtin_amdgcn_mov_dpp(xi, 0x150 + 8 + C, 0xF, 0xF, false);
+        return static_cast<uint32_t>((threadIdx.x & 8) ? b : a);
+    } else if constexpr (LPR == 16) {
+        return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(xi, 0x150 + C, 0xF, 0xF, false));
+    } else {
+        return group_lane_at<LPR>(x, C);
+    }
+}
 
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = 64 * kWavesPerBlock;
@@ -246,9 +297,8 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
         VT ring[U];
         float ring_w[WEIGHTED ? U : 1];
         f2 ring_sb[kQuant ? U : 1];
-        auto issue = [&](int src_lane, bool from_next, VT &dst, float &dw, f2 &dsb) {
-            const int src = g * LPR + src_lane;
-            const uint32_t r = from_next ? __shfl(nxt_r, src) : __shfl(cur_r, src);
+        // the row load for checked row id r (kSkip: the zero page) and weight w
+        auto issue_row = [&](uint32_t r, float w, VT &dst, float &dw, f2 &dsb) {
             const bool ok = r != kSkip && vact;
             const char *addr = ok ? colp + static_cast<uint64_t>(r) * row_bytes : zerop;
             dst = *reinterpret_cast<const VT *>(addr);
@@ -257,14 +307,22 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
                 const char *sba = ok ? table + static_cast<uint64_t>(r) * row_bytes + m.dim : zerop;
                 dsb = *reinterpret_cast<const f2 *>(sba);
             }
-            if constexpr (WEIGHTED) {
-                const float w = from_next ? __shfl(nxt_w, src) : __shfl(cur_w, src);
-                dw = ok ? w : 0.f;
-            }
+            if constexpr (WEIGHTED) dw = ok ? w : 0.f;
         };
-#pragma unroll
-        for (int sl = 0; sl < U; ++sl)
-            issue(sl, false, ring[sl], ring_w[WEIGHTED ? sl : 0], ring_sb[kQuant ? sl : 0]);
+        // the load for lookup c of the current (or, from_next, the next)
+        // chunk, the row id and weight taken from lane c of the group
+        auto issue_c = [&](auto cc, bool from_next, VT &dst, float &dw, f2 &dsb) {
+            constexpr int C = decltype(cc)::value;
+            const uint32_t r = group_lane<LPR, C>(from_next ? nxt_r : cur_r);
+            float w = 1.0f;
+            if constexpr (WEIGHTED)
+                w = __uint_as_float(group_lane<LPR, C>(__float_as_uint(from_next ? nxt_w : cur_w)));
+            issue_row(r, w, dst, dw, dsb);
+        };
+        static_for<U>([&](auto sc) {
+            constexpr int sl = decltype(sc)::value;
+            issue_c(sc, false, ring[sl], ring_w[WEIGHTED ? sl : 0], ring_sb[kQuant ? sl : 0]);
+        });
 
         // two chains: stream positions of even and of odd parity (the ring
         // slot's parity when U >= 2; with U == 1 the chains swap every step)
@@ -279,34 +337,54 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
         int32_t bag_end = bnd[1];
         while (bag + 1 < nbs && bag_end == 0) bag_end = end_of(++bag);
 
+        // consume ring slot sl, the lookup at stream position rp
+        auto consume = [&](int32_t rp, auto sc) {
+            constexpr int sl = decltype(sc)::value;
+            E::fma(acc[sl & 1], ring[sl], WEIGHTED ? ring_w[WEIGHTED ? sl : 0] : 1.0f,
+                   kQuant ? ring_sb[kQuant ? sl : 0] : f2{0.f, 0.f});
+            if (rp < Q && rp + 1 == bag_end) {
+                float *st = my_stage + bag * LPR * E::kPerVec;
+#pragma unroll
+                for (int i = 0; i < E::kPerVec; ++i) {
+                    st[i] = acc[0][i] + acc[1][i];
+                    acc[0][i] = acc[1][i] = 0.0f;
+                }
+                while (bag + 1 < nbs && bag_end == rp + 1) bag_end = end_of(++bag);
+            }
+            if constexpr (U == 1) {
+#pragma unroll
+                for (int i = 0; i < E::kPerVec; ++i) {
+                    const float x = acc[0][i];
+                    acc[0][i] = acc[1][i];
+                    acc[1][i] = x;
+                }
+            }
+        };
         for (int32_t base = 0; base < span; base += LPR) {
+            if constexpr (LPR <= 16) {
+                // every step of the chunk unrolled: the source lane of each
+                // row id is known here
+                static_for<LPR>([&](auto stc) {
+                    constexpr int S = decltype(stc)::value, sl = S % U, ahead = S + U;
+                    consume(base + S, std::integral_constant<int, sl>{});
+                    issue_c(std::integral_constant<int, ahead & (LPR - 1)>{}, ahead >= LPR, ring[sl],
+                            ring_w[WEIGHTED ? sl : 0], ring_sb[kQuant ? sl : 0]);
+                });
+            } else {
 #pragma unroll 1
-            for (int s0 = 0; s0 < LPR; s0 += U) {
-#pragma unroll
-                for (int sl = 0; sl < U; ++sl) {
-                    const int32_t rp = base + s0 + sl;
-                    E::fma(acc[sl & 1], ring[sl], WEIGHTED ? ring_w[WEIGHTED ? sl : 0] : 1.0f,
-                           kQuant ? ring_sb[kQuant ? sl : 0] : f2{0.f, 0.f});
-                    if (rp < Q && rp + 1 == bag_end) {
-                        float *st = my_stage + bag * LPR * E::kPerVec;
-#pragma unroll
-                        for (int i = 0; i < E::kPerVec; ++i) {
-                            st[i] = acc[0][i] + acc[1][i];
-                            acc[0][i] = acc[1][i] = 0.0f;
-                        }
-                        while (bag + 1 < nbs && bag_end == rp + 1) bag_end = end_of(++bag);
-                    }
-                    if constexpr (U == 1) {
-#pragma unroll
-                        for (int i = 0; i < E::kPerVec; ++i) {
-                            const float x = acc[0][i];
-                            acc[0][i] = acc[1][i];
-                            acc[1][i] = x;
-                        }
-                    }
-                    const int ahead = s0 + sl + U;
-                    issue(ahead & (LPR - 1), ahead >= LPR, ring[sl], ring_w[WEIGHTED ? sl : 0],
-                          ring_sb[kQuant ? sl : 0]);
+                for (int s0 = 0; s0 < LPR; s0 += U) {
+                    static_for<U>([&](auto sc) {
+                        constexpr int sl = decltype(sc)::value;
+                        consume(base + s0 + sl, sc);
+                        const int ahead = s0 + sl + U;
+                        const bool from_next = ahead >= LPR;
+                        const uint32_t r = group_lane_at<LPR>(from_next ? nxt_r : cur_r, ahead & (LPR - 1));
+                        float w = 1.0f;
+                        if constexpr (WEIGHTED)
+                            w = __uint_as_float(
+                                group_lane_at<LPR>(__float_as_uint(from_next ? nxt_w : cur_w), ahead & (LPR - 1)));
+                        issue_row(r, w, ring[sl], ring_w[WEIGHTED ? sl : 0], ring_sb[kQuant ? sl : 0]);
+                    });
                 }
             }
             cur_r = nxt_r;

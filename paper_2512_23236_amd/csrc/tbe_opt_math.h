@@ -127,13 +127,19 @@ __device__ inline void update_rows(const TableMeta &m, char *__restrict__ tab, i
             f4 gr[kInFlight], wv[kInFlight];
             float s0[kInFlight];  // the row's Adagrad state before the step
             char *p[kInFlight];
+            // every row's id and offset first (the shuffles' LDS round trips
+            // overlap), then the loads
+#pragma unroll
+            for (int k = 0; k < kInFlight; ++k) {
+                const int r = s + k * G + grp;
+                g[k] = __shfl(my_g, r & 63);
+                o[k] = __shfl(my_o, r & 63);
+            }
 #pragma unroll
             for (int k = 0; k < kInFlight; ++k) {
                 const int r = s + k * G + grp;
                 has[k] = r < e && !((skip >> (r & 63)) & 1ull);
                 act[k] = has[k] && v < nq;
-                g[k] = __shfl(my_g, r & 63);
-                o[k] = __shfl(my_o, r & 63);
                 p[k] = tab + ((g[k] - t_lo) * m.dim + v * 4) * ES;
                 const f4 z = f4{0.f, 0.f, 0.f, 0.f};
                 gr[k] = act[k] ? *reinterpret_cast<const f4 *>(grad_rows + o[k] + v * 4) : z;

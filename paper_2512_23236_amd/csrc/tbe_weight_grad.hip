@@ -155,11 +155,17 @@ __global__ __launch_bounds__(64 * kWgWaves) void weight_grad_kernel(
             oob |= lane < cnt && !my_ok;
             const uint32_t my_r = my_ok ? static_cast<uint32_t>(my_idx) : kSkipRow;
             for (int r0 = 0; r0 < cnt; r0 += G * kAhead) {
+                // every row id of the round first (the shuffles' LDS round
+                // trips overlap), then the row loads
+                uint32_t rr[kAhead];
+#pragma unroll
+                for (int u = 0; u < kAhead; ++u)
+                    rr[u] = static_cast<uint32_t>(__shfl(static_cast<int>(my_r), (r0 + u * G + g) & 63));
                 uint4 rowv[kAhead];
 #pragma unroll
                 for (int u = 0; u < kAhead; ++u) {
                     const int i = r0 + u * G + g;
-                    const uint32_t r = static_cast<uint32_t>(__shfl(static_cast<int>(my_r), i & 63));
+                    const uint32_t r = rr[u];
                     const bool ok = i < cnt && r != kSkipRow;
                     const char *addr = (ok && vact) ? tab + static_cast<int64_t>(r) * row_bytes +
                                                           static_cast<int64_t>(c0 + v) * 16
