@@ -421,6 +421,22 @@ def test_hot_segments_around_the_threshold(weighted):
     check(spec, d)
 
 
+@pytest.mark.parametrize("weighted", [False, True])
+def test_long_segments_at_run_edges(weighted):
+    """Long segments whose piece counts lie around multiples of 16 and 32
+    (the combine sums whole runs of 16 pieces as fixed trees, two runs at
+    once on the wave's halves for rows of at most 128 fp32 columns, then the
+    last pieces one by one), on rows of 64, 128 and 256 columns."""
+    spec = dataclasses.replace(workloads.small_config(4 if weighted else 5, seed=55, T=3, B=3000),
+                               rows=np.array([50, 50, 50], np.int64), dims=np.array([64, 128, 256], np.int32))
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    runs = [128 * p for p in (15, 16, 17, 31, 32, 33, 47, 48, 49, 64, 65, 97)]
+    for t in range(3):
+        n = _pattern_indices(spec, d, t, runs[t:] + runs[:t])
+        note(f"[bwd-runs] table {t}: {n} lookups")
+    check(spec, d)
+
+
 def test_many_long_rows_in_one_table():
     """A table with about 100 rows of more than 1024 lookups each."""
     spec = dataclasses.replace(workloads.small_config(5, seed=52, T=1, B=4000), rows=np.array([500], np.int64),
