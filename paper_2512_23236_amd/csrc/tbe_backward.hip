@@ -8,27 +8,33 @@
 //   setup     per-table lookup ranges [offsets[tB], offsets[(t+1)B]) and the
 //             tiling of each range into tiles of kTile positions.
 //   keys      one workgroup per run of bags writes key_j = idx_j (32-bit,
-//             local to the table) and val_j = b(j) (plus the weight).  A
-//             table's lookups already occupy exactly the positions its rows
-//             take in the global order, so sorting every table's range by
-//             its local key yields the global stable sort.
-//   radix     stable LSD radix sort of each range, 8-bit digits, over the
-//             bits of the largest table: per pass a tile histogram (one
-//             contiguous row per tile), a per-table scan of every digit's
-//             column over the table's tiles, and a stable scatter that
-//             ranks keys with wave ballots, derives its digits' final
-//             positions from the table's digit totals and its tile's row,
-//             and stages the tile in LDS so global writes run in digit order.
+//             local to the table) and val_j = b(j) (plus the weight), and
+//             counts the first radix pass's digits per tile.  A table's
+//             lookups already occupy exactly the positions its rows take in
+//             the global order, so sorting every table's range by its local
+//             key yields the global stable sort.
+//   radix     stable LSD radix sort of each range, 8-bit digits, each table
+//             over the bits of its own row count: per pass a tile histogram
+//             (one contiguous row per tile; the first pass's come from the
+//             keys kernel), a per-table scan of every digit's column over the
+//             table's tiles, and a stable scatter that ranks keys with wave
+//             ballots, derives its digits' final positions from the table's
+//             digit totals and its tile's row, and stages the tile in LDS so
+//             global writes run in digit order.
 //   segments  per tile: segment starts (key change) per block and tile and
 //             kept lookups; one scan over tiles; then grad_idx / seg_offsets /
-//             grad_row_offsets are written for every segment start.
+//             grad_row_offsets are written for every segment start, and the
+//             per-tile facts of the reduce (block edges inside long segments,
+//             the long segments that begin in each block, with their piece
+//             counts).
 //   reduce    sorted positions are cut into fixed blocks of kBlk; a wave
-//             walks one block in order, accumulating fp32 rows of
-//             grad_out; a segment that lies inside the block is written
-//             straight to its gradient row (its only writer); a segment
-//             cut by a block edge leaves a head / tail piece.
-//   combine   each segment that crosses block edges is summed from its
-//             pieces in a fixed pairwise order and written once.
+//             walks a range of blocks in order for one column slice,
+//             accumulating fp32 rows of grad_out; a segment of at most kBlk
+//             lookups is summed whole and written straight to its gradient
+//             row (its only writer); a longer one leaves one piece per block
+//             it touches.
+//   combine   each long segment is summed from its pieces in a fixed
+//             pairwise order and written once.
 // Every output has one writer and a fixed summation order, so the result is
 // bitwise reproducible.  Lookups whose index fails the bounds check are
 // keyed past every valid key of their table and dropped.
@@ -1064,9 +1070,9 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
 // Per-tile facts of the reduce, computed once for all column slices by one
 // wave per tile (lane e for block edge e): segment starts before each block
 // (from the per-block counts of the segment-count kernel), which block edges
-// lie inside a long segment (one with more than kBlk lookups), and the head /
-// long segments that begin in each block with their piece counts (read by
-// the combine kernel).
+// lie inside a long segment (one with more than kBlk lookups), and the long
+// segments that begin in each block with their piece counts (read by the
+// combine kernel).
 __global__ __launch_bounds__(64) void edges_kernel(const uint32_t *__restrict__ keys,
                                                    const uint32_t *__restrict__ blk_starts,
                                                    const int64_t *__restrict__ seg_offsets,
@@ -1372,26 +1378,24 @@ __device__ __attribute__((always_inline)) inline float4 tail_total(float4 (&xs)[
 // Sums the pieces of every long segment in the counter's order (the tail
 // piece of the block where the segment begins, then the head pieces of the
 // blocks that follow) and writes its gradient row once.  A wave takes one
-// tile and the long segments that begin in it.  A segment of at least
-// 2^kRunLevel pieces is summed a whole run at a time (the run's loads in
-// flight together, then its fixed tree; with rows of at most 32 quads the two
-// halves of the wave take two runs at once), then its last pieces; shorter
-// segments are summed in one round each, two at a time (one per half of the
-// wave) when the rows have at most 32 quads.
+// tile (a one-wave workgroup, so a wave summing a hot row holds no finished
+// siblings' slots) and the long segments that begin in it, one after
+// another: whole runs of 2^kRunLevel pieces (the run's loads in flight
+// together, then its fixed tree; with rows of at most 32 quads the two halves
+// of the wave take two runs at once), then the last pieces in one round.
 // With kApply the combine then makes the optimizer step on each row it wrote
 // (kAdagrad: row-wise Adagrad, else SGD), as reduce_apply_kernel does for
 // short segments.
 template <bool kApply, bool kAdagrad>
-__global__ __launch_bounds__(64) void combine_kernel(const TableMeta *__restrict__ meta,
-                                                           const Ctl *__restrict__ ctl,
-                                                           const TileEdges *__restrict__ edges,
-                                                           const int32_t *__restrict__ tail_np,
-                                                           const int32_t *__restrict__ tail_seg,
-                                                           const float *__restrict__ partials, int max_dim,
-                                                           const int64_t *__restrict__ grad_row_offsets,
-                                                           float *__restrict__ grad_rows, int64_t capacity,
-                                                           const int64_t *__restrict__ grad_idx, char *__restrict__ tables,
-                                                           int dt, float *__restrict__ state, float lr, float eps) {
+__global__ __launch_bounds__(64) void combine_kernel(const TableMeta *__restrict__ meta, const Ctl *__restrict__ ctl,
+                                                     const TileEdges *__restrict__ edges,
+                                                     const int32_t *__restrict__ tail_np,
+                                                     const int32_t *__restrict__ tail_seg,
+                                                     const float *__restrict__ partials, int max_dim,
+                                                     const int64_t *__restrict__ grad_row_offsets,
+                                                     float *__restrict__ grad_rows, int64_t capacity,
+                                                     const int64_t *__restrict__ grad_idx, char *__restrict__ tables,
+                                                     int dt, float *__restrict__ state, float lr, float eps) {
     constexpr int kB = 1 << kRunLevel;
     const int lane = threadIdx.x & 63;
     if (ctl->abort || ctl->total_floats > capacity) return;
