@@ -432,6 +432,8 @@ def variant_tag(args, spec) -> str:
         tag += f"_{args.index_type}"
     if args.out_dtype != "f32":
         tag += f"_out{args.out_dtype}"
+    if args.train and not workloads.make_config(args.config, args.seed).grad:
+        tag += "_train"
     return tag
 
 
@@ -446,6 +448,9 @@ def variant_text(args, spec) -> str:
         parts.append("int32 indices and offsets")
     if args.out_dtype != "f32":
         parts.append(f"{args.out_dtype} output" + (" and grad_out" if spec.grad else ""))
+    if args.train and not workloads.make_config(args.config, args.seed).grad:
+        parts.append("training step (forward, backward" + (", per-sample weights' gradient)" if spec.weighted else ")")
+                     + "; grad_out N(0,1)")
     return ("; " + ", ".join(parts)) if parts else ""
 
 
@@ -473,6 +478,9 @@ def main():
                     help="also time the step captured in a HIP graph and replayed (reported under 'graph')")
     ap.add_argument("--overlap-index", action="store_true",
                     help="queue the backward's index phase on a second stream beside the forward")
+    ap.add_argument("--train", action="store_true",
+                    help="time the training step on any configuration: forward and backward, and with "
+                         "per-sample weights also their gradient (cfg5 is a training step already)")
     ap.add_argument("--pooling", default="sum", choices=["sum", "mean"])
     ap.add_argument("--index-type", default="i64", choices=["i64", "i32"],
                     help="integer type of indices and offsets")
@@ -506,6 +514,8 @@ def main():
         spec = __import__("dataclasses").replace(spec, dtype=args.table_dtype)
     if args.pooling == "mean" and spec.weighted:
         spec = __import__("dataclasses").replace(spec, weighted=False)  # mean pooling takes no weights
+    if args.train:
+        spec = __import__("dataclasses").replace(spec, grad=True)
     if args.op == "weight_grad":
         return bench_weight_grad(args, spec, dev)
     if args.op in ("sgd", "adagrad"):
@@ -529,6 +539,9 @@ def main():
     if spec.grad and out_dtype != torch.float32:
         d["grad_out"] = d["grad_out"].to(out_dtype)  # the gradient of out has out's type
     training = spec.grad
+    # with per-sample weights the training step also takes their gradient
+    wgrad = training and spec.weighted
+    gw = torch.empty(d["N"], dtype=torch.float32, device=dev) if wgrad else None
     grads = None
     side = torch.cuda.Stream(dev)  # the backward's index phase (default priority, like the main stream)
     if training:
@@ -570,13 +583,25 @@ def main():
         forward(ev)
         main.wait_stream(side)
         reduce_phase(None if ev is None else ev[6:9])
+        if wgrad:
+            weight_grad_phase(None if ev is None else ev[9:11])
+
+    def weight_grad_phase(ev=None):
+        if ev is not None:
+            ev[0].record()
+        tbe.weight_grad(plan, d["tables"], d["grad_out"], d["indices"], d["offsets"], out=gw, status=status)
+        if ev is not None:
+            ev[1].record()
 
     def serial_step(ev=None):
-        """Forward, index phase, reduce phase in order on one stream."""
+        """Forward, index phase, reduce phase (and the weights' gradient) in
+        order on one stream."""
         forward(ev)
         if training:
             index_phase(None if ev is None else ev[2:6])
             reduce_phase(None if ev is None else ev[6:9])
+        if wgrad:
+            weight_grad_phase(None if ev is None else ev[9:11])
 
     step = overlapped_step if args.overlap_index else serial_step
 
@@ -586,7 +611,7 @@ def main():
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())}")
 
-    nev = 2 + (7 if training else 0)
+    nev = 2 + (7 if training else 0) + (2 if wgrad else 0)
     evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(nev)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -631,7 +656,8 @@ def main():
                    "batch": spec.B, "table_dtype": spec.dtype, "lookups": N, "table_bytes": spec.table_bytes,
                    "total_dim": plan.total_dim, "seed": spec.seed, "training": training,
                    "pooling": args.pooling, "index_type": args.index_type, "out_dtype": args.out_dtype,
-                   "schedule": ("forward, then the backward's index and reduce phases, on one stream"
+                   "schedule": ("forward, then the backward's index and reduce phases"
+                                + (", then the per-sample weights' gradient" if wgrad else "") + ", on one stream"
                                 if training and not args.overlap_index else
                                 "backward index phase on a second stream beside the forward, then the reduce"
                                 if training else "forward only")},
@@ -678,6 +704,10 @@ def main():
                            "frac_of_hbm_peak": bbytes / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
                            "phases_ms": {k: float(np.mean(v)) for k, v in phase_ms.items()},
                            "serial_step_ms": fwd_avg + bwd_avg}
+        if wgrad:
+            wg_ms = [e[9].elapsed_time(e[10]) for e in sev]
+            res["weight_grad"] = {"ms": float(np.mean(wg_ms)), "lookups_per_s": N / (float(np.mean(wg_ms)) * 1e-3)}
+            res["backward"]["serial_step_ms"] += res["weight_grad"]["ms"]
         red_ms = float(np.mean(red_ph))
         rbytes = reduce_bytes(spec, N, gro_total, spec.weighted or args.pooling == "mean", ob)
         rf["reduce_kernel"] = roof("reduce_kernel", red_ms, rbytes)
@@ -718,14 +748,17 @@ def main():
             ev = tuple(torch.cuda.Event(enable_timing=True) for _ in range(nev))
             serial_step(ev)
             torch.cuda.synchronize()
-            fl.append((ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[-1]) if training else 0.0))
+            fl.append((ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[8]) if training else 0.0,
+                       ev[9].elapsed_time(ev[10]) if wgrad else 0.0))
         del junk
         fw = [x[0] for x in fl]
         res["flushed"] = {"steps": args.flushed_steps, "forward_ms": float(np.median(fw)),
                           "forward_frac_of_hbm_peak": fbytes / (float(np.median(fw)) * 1e-3) / 1e9 / HBM_PEAK_GBS}
         if training:
             res["flushed"]["backward_ms"] = float(np.median([x[1] for x in fl]))
-            res["flushed"]["serial_step_ms"] = float(np.median([x[0] + x[1] for x in fl]))
+            res["flushed"]["serial_step_ms"] = float(np.median([x[0] + x[1] + x[2] for x in fl]))
+        if wgrad:
+            res["flushed"]["weight_grad_ms"] = float(np.median([x[2] for x in fl]))
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())}")
     if not args.no_cpu_baseline:
