@@ -481,18 +481,45 @@ __global__ __launch_bounds__(kColThreads) void col_scan_kernel(uint32_t *__restr
     if (g == 0) totals[static_cast<int64_t>(t) * kBuckets + d] = total;
 }
 
+// The scatter runs a tile on kScWaves waves of kScItems keys per lane: with
+// 8-byte values its LDS staging (48 KB) allows two workgroups per CU, so
+// eight waves each keep twice the waves in flight of four.
+constexpr int kScWaves = 8;
+constexpr int kScThreads = 64 * kScWaves;
+constexpr int kScItems = kTile / kScThreads;
+static_assert(kScItems * kScThreads == kTile, "scatter tile");
+
+// Exclusive scan of one value per thread over a scatter workgroup; the total
+// through *total.  `lds` holds kScWaves entries.
+__device__ inline uint32_t scatter_scan(uint32_t v, uint32_t *lds, uint32_t *total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint32_t inc = wave_incl_scan(v);
+    if (lane == 63) lds[wave] = inc;
+    __syncthreads();
+    uint32_t before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kScWaves; ++w) {
+        const uint32_t s = lds[w];
+        if (w < wave) before += s;
+        all += s;
+    }
+    __syncthreads();
+    *total = all;
+    return before + inc - v;
+}
+
 template <typename V>
-__global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
+__global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
     uint32_t *__restrict__ keys0, uint32_t *__restrict__ keys1, V *__restrict__ vals0, V *__restrict__ vals1,
     const uint32_t *__restrict__ prefix, const uint32_t *__restrict__ totals, const TableMeta *__restrict__ meta,
     const Range *__restrict__ ranges, int T, const Ctl *__restrict__ ctl, int pass, int passes, int shift,
     int nbits) {
-    __shared__ uint32_t cnt[kWaves][kBuckets];  // per-wave digit counts, then wave offsets
+    __shared__ uint32_t cnt[kScWaves][kBuckets];  // per-wave digit counts, then wave offsets
     __shared__ uint32_t tstart[kBuckets];       // first tile-local slot of each digit
     __shared__ uint32_t goff[kBuckets];         // first global slot of each digit for this tile
     __shared__ uint32_t sk[kTile];
     __shared__ V sv[kTile];
-    __shared__ uint32_t lds[kWaves];
+    __shared__ uint32_t lds[kScWaves];
 
     const int64_t tile = blockIdx.x;
     if (tile >= ctl->total_tiles || ctl->abort) return;
@@ -506,23 +533,22 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     V *__restrict__ vals_out = src ? vals0 : vals1;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint32_t mask = (1u << nbits) - 1u;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) cnt[w][tid] = 0;
+    for (int i = tid; i < kScWaves * kBuckets; i += kScThreads) (&cnt[0][0])[i] = 0;
     __syncthreads();
 
-    // Wave w ranks positions [p_lo + w*1024, +1024) in order, 64 per round.
-    const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
-    uint32_t key[kItems], rank[kItems];
-    V val[kItems];
+    // Wave w ranks positions [p_lo + w*512, +512) in order, 64 per round.
+    const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kScWaves);
+    uint32_t key[kScItems], rank[kScItems];
+    V val[kScItems];
 #pragma unroll
-    for (int r = 0; r < kItems; ++r) {
+    for (int r = 0; r < kScItems; ++r) {
         const int64_t pos = wbase + r * 64 + lane;
         const bool valid = pos < ti.p_hi;
         key[r] = valid ? keys_in[pos] : 0u;
         val[r] = valid ? vals_in[pos] : V(0);
     }
 #pragma unroll
-    for (int r = 0; r < kItems; ++r) {
+    for (int r = 0; r < kScItems; ++r) {
         const int64_t pos = wbase + r * 64 + lane;
         const bool valid = pos < ti.p_hi;
         const uint32_t d = digit_of(key[r], shift, mask);
@@ -544,25 +570,33 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     }
     __syncthreads();
     {
+        // thread d < kBuckets: digit d (the other threads join the scans with 0)
         const int d = tid;
+        const bool dig = d < kBuckets;
         uint32_t run = 0;
+        if (dig) {
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
-            const uint32_t c = cnt[w][d];
-            cnt[w][d] = run;
-            run += c;
+            for (int w = 0; w < kScWaves; ++w) {
+                const uint32_t c = cnt[w][d];
+                cnt[w][d] = run;
+                run += c;
+            }
         }
         uint32_t tot;
-        tstart[d] = block_excl_scan<uint32_t>(run, lds, &tot);
+        const uint32_t ts = scatter_scan(run, lds, &tot);
         // first global slot of digit d for this tile: the table's first
         // position, the table's keys of smaller digits, then this digit's keys
         // in the table's earlier tiles
-        const uint32_t below = block_excl_scan<uint32_t>(totals[static_cast<int64_t>(ti.t) * kBuckets + d], lds, &tot);
-        goff[d] = static_cast<uint32_t>(ranges[ti.t].start) + below + prefix[tile * kBuckets + d];
+        const uint32_t below =
+            scatter_scan(dig ? totals[static_cast<int64_t>(ti.t) * kBuckets + d] : 0u, lds, &tot);
+        if (dig) {
+            tstart[d] = ts;
+            goff[d] = static_cast<uint32_t>(ranges[ti.t].start) + below + prefix[tile * kBuckets + d];
+        }
     }
     __syncthreads();
 #pragma unroll
-    for (int r = 0; r < kItems; ++r) {
+    for (int r = 0; r < kScItems; ++r) {
         const int64_t pos = wbase + r * 64 + lane;
         if (pos < ti.p_hi) {
             const uint32_t d = digit_of(key[r], shift, mask);
@@ -573,7 +607,7 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     }
     __syncthreads();
     const int n = static_cast<int>(ti.p_hi - ti.p_lo);
-    for (int i = tid; i < n; i += kThreads) {
+    for (int i = tid; i < n; i += kScThreads) {
         const uint32_t k = sk[i];
         const uint32_t d = digit_of(k, shift, mask);
         const int64_t dst = static_cast<int64_t>(goff[d]) + (i - static_cast<int64_t>(tstart[d]));
@@ -1636,7 +1670,7 @@ hipError_t run_index(const Plan &p, const IT *indices, const IT *offsets, int64_
                                T, w.ctl, pass, passes, shift, nb, w.hist);
         hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), dim3(kColThreads), 0, stream, w.hist, w.totals,
                            p.meta_dev, w.ranges, w.ctl, pass);
-        hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, blk, 0, stream, w.keys[0], w.keys[1], vals[0], vals[1],
+        hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, dim3(kScThreads), 0, stream, w.keys[0], w.keys[1], vals[0], vals[1],
                            w.hist, w.totals, p.meta_dev, w.ranges, T, w.ctl, pass, passes, shift, nb);
     }
     const int cur = passes & 1;  // every table's sorted keys and values
