@@ -62,7 +62,6 @@ constexpr int kPairLevels = 12;               // pairwise-sum depth in combine
 constexpr int kCombineGroups = 1 << 16;       // combine grid (one-wave workgroups loop over tiles)
 constexpr int kKeyBags = 256;                 // bags per keys workgroup
 constexpr int kKeyAhead = 4;                  // keys kernel: lookup rounds whose loads are in flight together
-constexpr int kCombineBatch = 16;             // piece rows loaded at once in combine
 
 // Device control block at the start of the workspace.  The index phase
 // writes it; the reduce phase reads it.
