@@ -92,6 +92,21 @@ def test_bounds_check_zeroes_bad_lookups():
     assert float(oracle.summation_error(got[keep], ref[keep], ab[keep]).max()) <= RTOL_W
 
 
+def test_bounds_check_flags_bad_offsets():
+    """Malformed offsets under the bounds check (a bag ending past N, a bag
+    ending before it starts): the offsets bit is set and every access stays
+    inside the inputs (the weight gradients are then unspecified)."""
+    spec = workloads.small_config(4, seed=11, T=2, B=40)
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    N = d["N"]
+    off = d["offsets"].cpu().numpy().copy()
+    off[5] = N + 7            # bag 4 ends past N
+    off[13] = off[12] - 1     # bag 12 ends before it starts
+    d["offsets"] = torch.as_tensor(off, device=device())
+    _, st = run_wg(spec, d)
+    assert st & tbe.STATUS_OFFSETS
+
+
 def test_deterministic_repeat():
     spec = workloads.small_config(3, seed=8, T=4, B=200)
     d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
