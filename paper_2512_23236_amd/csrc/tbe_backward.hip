@@ -921,7 +921,7 @@ constexpr uint32_t kBufferOob = 0x80000000u;
 template <typename V, bool kWide, int GT>
 __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
                                    const void *__restrict__ grad_out, const TableMeta &m, const TileInfo &ti,
-                                   const TileSeg &pre, const TileEdges &te, int64_t total_dim,
+                                   const TileSeg &pre, const TileEdges *__restrict__ te, int64_t total_dim,
                                    int64_t gout_elems, float *__restrict__ grad_rows,
                                    float *__restrict__ partials, int max_dim, int64_t tile, int c0,
                                    const float *__restrict__ zero_page) {
@@ -938,11 +938,11 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
     const int64_t r1 = r0 + kBlksPerWave * kBlk < ti.p_hi ? r0 + kBlksPerWave * kBlk : ti.p_hi;
     // a short segment begun in the range is finished past its end
     const int64_t lim = r1 + kBlk < ti.end ? r1 + kBlk : ti.end;
-    const uint64_t long_mask = te.long_mask;
+    const uint64_t long_mask = te->long_mask;
     const bool long_r0 = (long_mask >> q0) & 1ull;
     const int q1 = static_cast<int>((r1 - ti.p_lo + kBlk - 1) / kBlk);
     const bool long_r1 = r1 < ti.end && ((long_mask >> q1) & 1ull);
-    const uint32_t u_r0 = static_cast<uint32_t>(pre.starts) + te.starts[q0];
+    const uint32_t u_r0 = static_cast<uint32_t>(pre.starts) + te->starts[q0];
     const int64_t part0 = 2 * (tile * kBlksPerTile) * max_dim;
 
     constexpr int GES = GT == TBE_F32 ? 4 : 2;  // bytes per grad_out element
@@ -1211,7 +1211,7 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
     if (!tile_info(ranges, T, tile, ti)) return;
     const TableMeta m = meta[t];
     const TileSeg pre = tseg[tile];
-    const TileEdges te = edges[tile];
+    const TileEdges *const te = edges + tile;  // read in place (indexed by wave)
     constexpr int GES = GT == TBE_F32 ? 4 : 2;
     if (gout_elems * GES < kBufferLimit)
         reduce_wave<V, false, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
@@ -1274,7 +1274,7 @@ __global__ __launch_bounds__(kThreads) void reduce_apply_kernel(
     if (!tile_info(ranges, T, tile, ti)) return;
     const TableMeta m = meta[ti.t];
     const TileSeg pre = tseg[tile];
-    const TileEdges te = edges[tile];
+    const TileEdges *const te = edges + tile;  // read in place (indexed by wave)
     constexpr int GES = GT == TBE_F32 ? 4 : 2;
     for (int c0 = 0; c0 < m.dim; c0 += slice_cols(GT)) {
         if (gout_elems * GES < kBufferLimit)
@@ -1294,7 +1294,7 @@ __global__ __launch_bounds__(kThreads) void reduce_apply_kernel(
     if (r0 >= ti.p_hi) return;
     const int64_t r1 = r0 + kBlksPerWave * kBlk < ti.p_hi ? r0 + kBlksPerWave * kBlk : ti.p_hi;
     const int q1 = static_cast<int>((r1 - ti.p_lo + kBlk - 1) / kBlk);
-    const int64_t u_lo = pre.starts + te.starts[q0], u_hi = pre.starts + te.starts[q1];
+    const int64_t u_lo = pre.starts + te->starts[q0], u_hi = pre.starts + te->starts[q1];
     for (int64_t base = u_lo; base < u_hi; base += 64) {
         const int n = u_hi - base < 64 ? static_cast<int>(u_hi - base) : 64;
         const int64_t u = base + lane;
