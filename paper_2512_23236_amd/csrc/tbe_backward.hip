@@ -230,6 +230,25 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__
 
 // ------------------------------------------------------------------- keys
 
+// Bits of a table's local keys: the smallest b >= 1 with 2^b > R_t (at most
+// 32), so that the drop key's low b bits (all ones) sort after every row.
+__device__ inline int table_key_bits(int64_t rows) {
+    const int b = rows > 0 ? 64 - __clzll(static_cast<unsigned long long>(rows)) : 1;
+    return b > 32 ? 32 : b;
+}
+
+// Packed sort records.  Without per-lookup weights the sort value is the
+// batch row alone.  When a table's key bits and the batch row's bits (pbits)
+// fit in one 32-bit word together, the table's records are that word, key
+// field above batch row, through every radix pass but its last, which writes
+// key and value apart again: those passes move 4 bytes per lookup instead of
+// 8.  The digits are the key field's, so the stable order is the same.
+// pbits < 0: no packing (64-bit values).  Returns the shift of the key field
+// in table t's records, or -1 when they are not packed.
+__device__ inline int packed_shift(int64_t rows, int pbits) {
+    return pbits >= 0 && table_key_bits(rows) + pbits <= 32 ? pbits : -1;
+}
+
 // One workgroup per run of kKeyBags consecutive bags (table-major order).  The
 // run's offsets are staged in LDS; the threads then walk the run's lookups in
 // order, 256 at a time (coalesced loads and stores), and find each lookup's
@@ -239,8 +258,12 @@ __global__ __launch_bounds__(kThreads) void setup_kernel(int scols, const IT *__
 // go to the buffer from which its own sort_passes radix passes end in buffer
 // passes & 1, where every table's sorted keys then lie.
 //
-// The kernel also counts the first radix pass's digits (key & mask0) per tile
-// into `hist` (zeroed beforehand), so that pass needs no histogram kernel: the
+// Records of tables that fit go out packed (packed_shift): the key word then
+// holds key field and batch row, and no value is written.
+//
+// The kernel also counts the first radix pass's digits (the key field's low
+// bits, & mask0) per tile into `hist` (zeroed beforehand), so that pass needs
+// no histogram kernel: the
 // run's lookups fall in a few consecutive tiles, counted in LDS for the first
 // kKeyTiles of them (global atomics beyond) and added to `hist` at the end.
 constexpr int kKeyTiles = 8;
@@ -253,13 +276,15 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
                                                         int64_t nbags, int check, Ctl *ctl,
                                                         uint32_t *__restrict__ keys0, uint32_t *__restrict__ keys1,
                                                         V *__restrict__ vals0, V *__restrict__ vals1, int passes,
-                                                        uint32_t mask0, uint32_t *__restrict__ hist,
+                                                        uint32_t mask0, uint32_t *__restrict__ hist, int pbits,
                                                         int32_t *status) {
     __shared__ int64_t off[kKeyBags + 1];
     __shared__ int64_t bag_rows[kKeyBags];  // R_t of each bag's table
     __shared__ int64_t bag_tile[kKeyBags];  // kTile * (the table's first tile) - (its first position)
     __shared__ uint32_t bag_b[kKeyBags];    // batch row of each bag
     __shared__ uint8_t bag_buf[kKeyBags];   // buffer the bag's table starts its sort in
+    __shared__ int8_t bag_ps[kKeyBags];     // shift of the key field in packed records, or -1
+    __shared__ uint32_t bag_kf[kKeyBags];   // mask of the table's key field
     __shared__ uint32_t h0[kKeyTiles * kBuckets];  // first-pass digit counts of the run's first tiles
     __shared__ int64_t tile_lo;
     __shared__ int bad;
@@ -276,6 +301,8 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         bag_b[i] = static_cast<uint32_t>(k0 + i - t * B);
         bag_rows[i] = meta[t].rows;
         bag_buf[i] = static_cast<uint8_t>((passes - meta[t].sort_passes) & 1);
+        bag_ps[i] = static_cast<int8_t>(sizeof(V) == 4 ? packed_shift(meta[t].rows, pbits) : -1);
+        bag_kf[i] = 0xffffffffu >> (32 - table_key_bits(meta[t].rows));
         // position j of the bag's table lies in tile (bag_tile + j) / kTile
         const Range r = ranges[t];
         bag_tile[i] = r.tile_base * kTile - r.start;
@@ -337,16 +364,19 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
             const bool second = bag_buf[lo] != 0;
             uint32_t *const keys = second ? keys1 : keys0;
             V *const vals = second ? vals1 : vals0;
-            keys[j] = key;
+            const int ps = bag_ps[lo];
+            // the record's key word: the key, or key field and batch row packed
+            const uint32_t rec = ps >= 0 ? ((key & bag_kf[lo]) << ps) | b : key;
+            keys[j] = rec;
             const int64_t tj = (bag_tile[lo] + j) / kTile;  // the lookup's tile
-            const uint32_t d = key & mask0;
+            const uint32_t d = (rec >> (ps > 0 ? ps : 0)) & mask0;
             if (tj - t_lo < kKeyTiles) atomicAdd(&h0[(tj - t_lo) * kBuckets + d], 1u);
             else atomicAdd(&hist[tj * kBuckets + d], 1u);
             if constexpr (sizeof(V) == 8) {
                 const float w = mean ? 1.0f / static_cast<float>(off[lo + 1] - off[lo]) : wts[r];
                 vals[j] = static_cast<uint64_t>(b) | (static_cast<uint64_t>(__float_as_uint(w)) << 32);
             } else {
-                vals[j] = static_cast<uint32_t>(b);
+                if (ps < 0) vals[j] = static_cast<uint32_t>(b);
             }
         }
     }
@@ -382,7 +412,8 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__
                                                               const TableMeta *__restrict__ meta,
                                                               const Range *__restrict__ ranges, int T,
                                                               const Ctl *__restrict__ ctl, int pass, int passes,
-                                                              int shift, int nbits, uint32_t *__restrict__ hist) {
+                                                              int shift, int nbits, int pbits,
+                                                              uint32_t *__restrict__ hist) {
     // counts only (order does not matter here): one LDS histogram per wave,
     // plain atomic increments, summed at the end
     __shared__ uint32_t cnt[kWaves][kBuckets];
@@ -398,6 +429,8 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__
     for (int w = 0; w < kWaves; ++w) cnt[w][tid] = 0;
     __syncthreads();
     const uint32_t mask = (1u << nbits) - 1u;
+    const int ps = packed_shift(meta[ti.t].rows, pbits);
+    shift += ps > 0 ? ps : 0;  // the key field's digit
     const int64_t wbase = ti.p_lo + static_cast<int64_t>(wave) * (kTile / kWaves);
     uint32_t k[kItems];
 #pragma unroll
@@ -512,7 +545,7 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
     uint32_t *__restrict__ keys0, uint32_t *__restrict__ keys1, V *__restrict__ vals0, V *__restrict__ vals1,
     const uint32_t *__restrict__ prefix, const uint32_t *__restrict__ totals, const TableMeta *__restrict__ meta,
     const Range *__restrict__ ranges, int T, const Ctl *__restrict__ ctl, int pass, int passes, int shift,
-    int nbits) {
+    int nbits, int pbits) {
     __shared__ uint32_t cnt[kScWaves][kBuckets];  // per-wave digit counts, then wave offsets
     __shared__ uint32_t tstart[kBuckets];       // first tile-local slot of each digit
     __shared__ uint32_t goff[kBuckets];         // first global slot of each digit for this tile
@@ -524,8 +557,16 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
     if (tile >= ctl->total_tiles || ctl->abort) return;
     TileInfo ti;
     if (!tile_info(ranges, T, tile, ti)) return;
-    const int src = sort_src(meta[ti.t], pass, passes);
+    const TableMeta &tm = meta[ti.t];
+    const int src = sort_src(tm, pass, passes);
     if (src < 0) return;
+    // packed records (a key word only) until the table's last pass, which
+    // writes key and batch row apart
+    const int ps = sizeof(V) == 4 ? packed_shift(tm.rows, pbits) : -1;
+    const bool packed = ps >= 0;
+    const bool unpack = packed && pass == tm.sort_passes - 1;
+    const uint32_t kfield = 0xffffffffu >> (32 - table_key_bits(tm.rows));
+    if (packed) shift += ps;
     const uint32_t *__restrict__ keys_in = src ? keys1 : keys0;
     const V *__restrict__ vals_in = src ? vals1 : vals0;
     uint32_t *__restrict__ keys_out = src ? keys0 : keys1;
@@ -544,7 +585,7 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
         const int64_t pos = wbase + r * 64 + lane;
         const bool valid = pos < ti.p_hi;
         key[r] = valid ? keys_in[pos] : 0u;
-        val[r] = valid ? vals_in[pos] : V(0);
+        val[r] = valid && !packed ? vals_in[pos] : V(0);
     }
 #pragma unroll
     for (int r = 0; r < kScItems; ++r) {
@@ -601,7 +642,7 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
             const uint32_t d = digit_of(key[r], shift, mask);
             const uint32_t slot = tstart[d] + cnt[wave][d] + rank[r];
             sk[slot] = key[r];
-            sv[slot] = val[r];
+            if (!packed) sv[slot] = val[r];
         }
     }
     __syncthreads();
@@ -610,8 +651,16 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
         const uint32_t k = sk[i];
         const uint32_t d = digit_of(k, shift, mask);
         const int64_t dst = static_cast<int64_t>(goff[d]) + (i - static_cast<int64_t>(tstart[d]));
-        keys_out[dst] = k;
-        vals_out[dst] = sv[i];
+        if (!packed) {
+            keys_out[dst] = k;
+            vals_out[dst] = sv[i];
+        } else if (!unpack) {
+            keys_out[dst] = k;
+        } else {
+            const uint32_t kf = k >> ps;  // the drop key's field is all ones
+            keys_out[dst] = kf == kfield ? kSentinel : kf;
+            vals_out[dst] = static_cast<V>(k & ((1u << ps) - 1u));
+        }
     }
 }
 
@@ -1652,13 +1701,20 @@ hipError_t run_index(const Plan &p, const IT *indices, const IT *offsets, int64_
     const int bits = sort_bits(p);
     const int passes = sort_passes_all(p);
     const int nb0 = bits < kRadixBits ? bits : kRadixBits;  // the first pass's digit bits
+    // bits of a batch row (for packed records; 64-bit values are not packed)
+    int pbits = -1;
+    if (sizeof(V) == 4) {
+        pbits = 0;
+        while (pbits < 32 && (int64_t(1) << pbits) < p.B) ++pbits;
+        if (pbits >= 32) pbits = -1;
+    }
     const int64_t zero_groups = L.max_tiles < 1024 ? L.max_tiles : 1024;
     hipLaunchKernelGGL(hist_zero_kernel, dim3(static_cast<unsigned>(zero_groups)), dim3(kThreads), 0, stream, w.hist,
                        w.ctl);
     hipLaunchKernelGGL((keys_kernel<V, IT>), dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)),
                        dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights, mean, w.ranges, p.B, nbags,
                        check, w.ctl, w.keys[0], w.keys[1], vals[0], vals[1], passes, (1u << nb0) - 1u, w.hist,
-                       status);
+                       pbits, status);
     const dim3 tiles(static_cast<unsigned>(L.max_tiles)), blk(kThreads);
     if ((me = mk.upto(1)) != hipSuccess) return me;
     for (int pass = 0; pass < passes; ++pass) {
@@ -1666,11 +1722,11 @@ hipError_t run_index(const Plan &p, const IT *indices, const IT *offsets, int64_
         const int nb = bits - shift < kRadixBits ? bits - shift : kRadixBits;
         if (pass > 0)  // the first pass's counts come from the keys kernel
             hipLaunchKernelGGL(radix_hist_kernel, tiles, blk, 0, stream, w.keys[0], w.keys[1], p.meta_dev, w.ranges,
-                               T, w.ctl, pass, passes, shift, nb, w.hist);
+                               T, w.ctl, pass, passes, shift, nb, pbits, w.hist);
         hipLaunchKernelGGL(col_scan_kernel, dim3(static_cast<unsigned>(T)), dim3(kColThreads), 0, stream, w.hist, w.totals,
                            p.meta_dev, w.ranges, w.ctl, pass);
         hipLaunchKernelGGL(radix_scatter_kernel<V>, tiles, dim3(kScThreads), 0, stream, w.keys[0], w.keys[1], vals[0], vals[1],
-                           w.hist, w.totals, p.meta_dev, w.ranges, T, w.ctl, pass, passes, shift, nb);
+                           w.hist, w.totals, p.meta_dev, w.ranges, T, w.ctl, pass, passes, shift, nb, pbits);
     }
     const int cur = passes & 1;  // every table's sorted keys and values
     if ((me = mk.upto(2)) != hipSuccess) return me;

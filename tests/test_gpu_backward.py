@@ -152,6 +152,47 @@ def test_mixed_sort_passes(k):
     check(dataclasses.replace(base, rows=rows, name=f"bwd-passes-{k}"))
 
 
+@pytest.mark.parametrize("B", [1024, 1025])
+def test_packed_records_at_the_width_limit(B):
+    # Unweighted sort records pack key field and batch row into one word when
+    # both fit in 32 bits: at B = 1024 (10 batch-row bits) a table of
+    # 2^22 - 1 rows (22 key bits) packs and one of 2^22 rows does not; at
+    # B = 1025 (11 bits) neither does, the 2^21 - 1 row table does.  Bad
+    # lookups (drop keys, whose key field is all ones) sit in every table, and
+    # the last batch row (all ones in its bits) looks up every table.
+    rows = np.array([3, (1 << 21) - 1, (1 << 22) - 1, 1 << 22], np.int64)
+    spec = dataclasses.replace(workloads.small_config(5, seed=12, T=len(rows), B=B), rows=rows,
+                               name=f"bwd-packed-{B}")
+    d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
+    off = d["offsets"].cpu()
+    N = d["N"]
+    good = d["indices"].clone()
+    # one bad lookup in the first bag with lookups of each table
+    bad = []
+    for t in range(spec.T):
+        s0, s1 = int(off[t * B]), int(off[(t + 1) * B])
+        if s1 > s0:
+            bad.append(s0)
+    bad = torch.tensor(bad, device=device())
+    d["indices"][bad] = torch.tensor([int(rows.max()) + 5] * len(bad), device=device())
+    lens = torch.diff(off)
+    assert all(int(lens[(t + 1) * B - 1]) > 0 for t in range(spec.T)), "the last batch row looks up every table"
+    g, st = run_backward(spec, d)
+    assert st & tbe.STATUS_INDEX_OOB
+    keep = torch.ones(N, dtype=torch.bool)
+    keep[bad.cpu()] = False
+    bag = torch.repeat_interleave(torch.arange(off.numel() - 1), lens)
+    off2 = torch.zeros_like(off)
+    torch.cumsum(torch.bincount(bag[keep], minlength=off.numel() - 1), 0, out=off2[1:])
+    d2 = dict(d, indices=good[keep.to(device())], offsets=off2.to(device()))
+    seg, ref, ab = oracle_backward(spec, d2)
+    gidx, segs, gro, grows = g.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(segs.numpy(), seg["seg_offsets"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    assert float(oracle.summation_error(grows.numpy(), ref, ab).max()) <= GRAD_RTOL
+
+
 def test_deterministic_repeat():
     spec = workloads.small_config(4, seed=8, T=3, B=400)
     d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())
