@@ -147,9 +147,10 @@ struct TileInfo {
     int64_t local, ntiles, p_lo, p_hi, start, end;
 };
 
-__device__ inline bool tile_info(const Range *__restrict__ ranges, int T, int64_t tile, TileInfo &ti) {
-    ti.t = find_table(ranges, T, tile);
-    const Range r = ranges[ti.t];
+// Tile `tile` of table t (known to own it).
+__device__ inline bool tile_info_of(const Range *__restrict__ ranges, int t, int64_t tile, TileInfo &ti) {
+    ti.t = t;
+    const Range r = ranges[t];
     ti.start = r.start;
     ti.end = r.end;
     ti.local = tile - r.tile_base;
@@ -157,6 +158,10 @@ __device__ inline bool tile_info(const Range *__restrict__ ranges, int T, int64_
     ti.p_lo = r.start + ti.local * kTile;
     ti.p_hi = ti.p_lo + kTile < r.end ? ti.p_lo + kTile : r.end;
     return ti.p_lo < ti.p_hi;
+}
+
+__device__ inline bool tile_info(const Range *__restrict__ ranges, int T, int64_t tile, TileInfo &ti) {
+    return tile_info_of(ranges, find_table(ranges, T, tile), tile, ti);
 }
 
 __device__ inline uint32_t digit_of(uint32_t key, int shift, uint32_t mask) { return (key >> shift) & mask; }
@@ -1257,7 +1262,7 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
     const int slice = static_cast<int>(local / ntiles);
     const int64_t tile = r.tile_base + local % ntiles;
     TileInfo ti;
-    if (!tile_info(ranges, T, tile, ti)) return;
+    if (!tile_info_of(ranges, t, tile, ti)) return;
     const TableMeta m = meta[t];
     const TileSeg pre = tseg[tile];
     const TileEdges *const te = edges + tile;  // read in place (indexed by wave)
