@@ -258,8 +258,9 @@ __device__ inline int packed_shift(int64_t rows, int pbits) {
 // run's offsets are staged in LDS; the threads then walk the run's lookups in
 // order, 256 at a time (coalesced loads and stores), and find each lookup's
 // bag by binary search over the staged offsets.  With 64-bit values the
-// weight rides along: the per-sample weight, or fl32(1/L) under mean pooling
-// (L = the bag's lookup count, read from the staged offsets).  A table's keys
+// per-sample weight rides along.  Under mean pooling (4-byte values) the
+// kernel writes each bag's fl32(1/L) to inv_len (L = the bag's lookup count,
+// from the staged offsets), which the reduce reads by batch row.  A table's keys
 // go to the buffer from which its own sort_passes radix passes end in buffer
 // passes & 1, where every table's sorted keys then lie.
 //
@@ -276,7 +277,8 @@ template <typename V, typename IT>
 __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restrict__ meta,
                                                         const IT *__restrict__ indices,
                                                         const IT *__restrict__ offsets,
-                                                        const float *__restrict__ weights, int mean,
+                                                        const float *__restrict__ weights,
+                                                        float *__restrict__ inv_len,
                                                         const Range *__restrict__ ranges, int64_t B,
                                                         int64_t nbags, int check, Ctl *ctl,
                                                         uint32_t *__restrict__ keys0, uint32_t *__restrict__ keys1,
@@ -313,6 +315,12 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         bag_tile[i] = r.tile_base * kTile - r.start;
     }
     __syncthreads();
+    if (inv_len) {
+        for (int i = tid; i < nk; i += kThreads) {
+            const int64_t L = off[i + 1] - off[i];
+            inv_len[k0 + i] = L > 0 ? 1.0f / static_cast<float>(L) : 0.f;
+        }
+    }
     if (check) {
         // each bag lies inside its table's range, in order
         for (int i = tid; i < nk; i += kThreads) {
@@ -352,7 +360,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         for (int r = 0; r < kKeyAhead; ++r) {
             const int64_t j = j0 + static_cast<int64_t>(r) * kThreads;
             ids[r] = j < last ? static_cast<int64_t>(__builtin_nontemporal_load(indices + j)) : 0;
-            if constexpr (sizeof(V) == 8) wts[r] = (!mean && j < last) ? weights[j] : 0.f;
+            if constexpr (sizeof(V) == 8) wts[r] = j < last ? weights[j] : 0.f;
         }
 #pragma unroll
         for (int r = 0; r < kKeyAhead; ++r) {
@@ -378,8 +386,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
             if (tj - t_lo < kKeyTiles) atomicAdd(&h0[(tj - t_lo) * kBuckets + d], 1u);
             else atomicAdd(&hist[tj * kBuckets + d], 1u);
             if constexpr (sizeof(V) == 8) {
-                const float w = mean ? 1.0f / static_cast<float>(off[lo + 1] - off[lo]) : wts[r];
-                vals[j] = static_cast<uint64_t>(b) | (static_cast<uint64_t>(__float_as_uint(w)) << 32);
+                vals[j] = static_cast<uint64_t>(b) | (static_cast<uint64_t>(__float_as_uint(wts[r])) << 32);
             } else {
                 if (ps < 0) vals[j] = static_cast<uint32_t>(b);
             }
@@ -972,16 +979,18 @@ constexpr uint32_t kBufferOob = 0x80000000u;
 // flush test are uniform.  A ring of kRing row loads stays in flight;
 // positions the wave does not own load zeros (an offset past the buffer's end,
 // or, for grad_out of 2 GiB and more, the zero page with weight 0).
-template <typename V, bool kWide, int GT>
+template <typename V, bool kMean, bool kWide, int GT>
 __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *__restrict__ vals,
                                    const void *__restrict__ grad_out, const TableMeta &m, const TileInfo &ti,
                                    const TileSeg &pre, const TileEdges *__restrict__ te, int64_t total_dim,
                                    int64_t gout_elems, float *__restrict__ grad_rows,
                                    float *__restrict__ partials, int max_dim, int64_t tile, int c0,
-                                   const float *__restrict__ zero_page) {
+                                   const float *__restrict__ zero_page, const float *__restrict__ bag_inv) {
     constexpr int NC = GT == TBE_F32 ? 1 : 2;  // columns per lane: a 256-byte slice of a grad_out row
     constexpr int U = kRing / NC;              // same registers for the ring either way
-    constexpr bool kWeighted = sizeof(V) == 8;
+    // a weight per lookup: from the 64-bit value, or under mean pooling the
+    // bag's fl32(1/L) (bag_inv: the table's row of them, by batch row)
+    constexpr bool kWeighted = sizeof(V) == 8 || kMean;
     const int lane = threadIdx.x & 63;
     const int wave = static_cast<int>(uni(threadIdx.x >> 6));
     const uint64_t le_mask = lanemask_lt() | (1ull << lane);
@@ -1065,6 +1074,7 @@ __device__ inline void reduce_wave(const uint32_t *__restrict__ keys, const V *_
         uint32_t b;
         float wl;
         val_split<V>(r.val, b, wl);
+        if constexpr (kMean) wl = bag_inv[b];
         if constexpr (kWide) {
             const char *row = gbase + static_cast<int64_t>(b) * total_dim * GES;
             o.addr = reinterpret_cast<uint64_t>(own ? row : reinterpret_cast<const char *>(zero_page));
@@ -1234,7 +1244,7 @@ __device__ inline int find_work_table(const Range *__restrict__ r, int T, int64_
 // One workgroup per work item (table, column slice, tile), slice-major within
 // a table, numbered so that each XCD takes a contiguous run of work items:
 // the waves of one XCD then share one table slice of grad_out in their L2.
-template <typename V, int GT>
+template <typename V, int GT, bool kMean>
 __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__restrict__ keys,
                                                           const V *__restrict__ vals,
                                                           const void *__restrict__ grad_out,
@@ -1246,7 +1256,8 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
                                                           int64_t gout_elems, float *__restrict__ grad_rows,
                                                           int64_t capacity, int32_t *status,
                                                           float *__restrict__ partials, int max_dim,
-                                                          const float *__restrict__ zero_page) {
+                                                          const float *__restrict__ zero_page,
+                                                          const float *__restrict__ inv_len, int64_t B) {
     if (ctl->abort) return;
     if (ctl->total_floats > capacity) {  // grad_rows too small: write no gradient row
         if (blockIdx.x == 0 && threadIdx.x == 0 && status) atomicOr(status, TBE_STATUS_CAPACITY);
@@ -1267,12 +1278,13 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const uint32_t *__rest
     const TileSeg pre = tseg[tile];
     const TileEdges *const te = edges + tile;  // read in place (indexed by wave)
     constexpr int GES = GT == TBE_F32 ? 4 : 2;
+    const float *const bag_inv = kMean ? inv_len + static_cast<int64_t>(t) * B : nullptr;
     if (gout_elems * GES < kBufferLimit)
-        reduce_wave<V, false, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
-                                  max_dim, tile, slice * slice_cols(GT), zero_page);
+        reduce_wave<V, kMean, false, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows,
+                                         partials, max_dim, tile, slice * slice_cols(GT), zero_page, bag_inv);
     else
-        reduce_wave<V, true, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
-                                 max_dim, tile, slice * slice_cols(GT), zero_page);
+        reduce_wave<V, kMean, true, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows,
+                                        partials, max_dim, tile, slice * slice_cols(GT), zero_page, bag_inv);
 }
 
 // ------------------------------------------------- reduce and apply (fused)
@@ -1307,7 +1319,7 @@ __device__ inline void update_rows_any(int dt, const TableMeta &m, char *__restr
         opt::update_rows<TBE_BF16, kAdagrad>(m, tab, m.row_base, state, grad_rows, my_g, my_o, i, e, skip, lr, eps);
 }
 
-template <typename V, int GT, bool kAdagrad>
+template <typename V, int GT, bool kMean, bool kAdagrad>
 __global__ __launch_bounds__(kThreads) void reduce_apply_kernel(
     const uint32_t *__restrict__ keys, const V *__restrict__ vals, const void *__restrict__ grad_out,
     const TableMeta *__restrict__ meta, const Range *__restrict__ ranges, int T, const Ctl *__restrict__ ctl,
@@ -1315,7 +1327,7 @@ __global__ __launch_bounds__(kThreads) void reduce_apply_kernel(
     float *__restrict__ grad_rows, int64_t capacity, int32_t *status, float *__restrict__ partials, int max_dim,
     const float *__restrict__ zero_page, const int64_t *__restrict__ grad_idx,
     const int64_t *__restrict__ seg_offsets, const int64_t *__restrict__ grad_row_offsets, char *__restrict__ tables,
-    int dt, float *__restrict__ state, float lr, float eps) {
+    int dt, float *__restrict__ state, float lr, float eps, const float *__restrict__ inv_len, int64_t B) {
     if (ctl->abort) return;
     if (ctl->total_floats > capacity) {  // grad_rows too small: write no gradient row, update nothing
         if (blockIdx.x == 0 && threadIdx.x == 0 && status) atomicOr(status, TBE_STATUS_CAPACITY);
@@ -1330,13 +1342,14 @@ __global__ __launch_bounds__(kThreads) void reduce_apply_kernel(
     const TileSeg pre = tseg[tile];
     const TileEdges *const te = edges + tile;  // read in place (indexed by wave)
     constexpr int GES = GT == TBE_F32 ? 4 : 2;
+    const float *const bag_inv = kMean ? inv_len + static_cast<int64_t>(ti.t) * B : nullptr;
     for (int c0 = 0; c0 < m.dim; c0 += slice_cols(GT)) {
         if (gout_elems * GES < kBufferLimit)
-            reduce_wave<V, false, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
-                                      max_dim, tile, c0, zero_page);
+            reduce_wave<V, kMean, false, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows,
+                                             partials, max_dim, tile, c0, zero_page, bag_inv);
         else
-            reduce_wave<V, true, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows, partials,
-                                     max_dim, tile, c0, zero_page);
+            reduce_wave<V, kMean, true, GT>(keys, vals, grad_out, m, ti, pre, te, total_dim, gout_elems, grad_rows,
+                                            partials, max_dim, tile, c0, zero_page, bag_inv);
     }
     stores_then_loads();
     // the short segments that begin in this wave's range: segment ids
@@ -1577,7 +1590,8 @@ __global__ __launch_bounds__(64) void combine_kernel(const TableMeta *__restrict
 // ------------------------------------------------------------- workspace
 
 struct Layout {
-    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, totals, tseg, edges, blk_starts, tail_np, tail, partials, total;
+    size_t ctl, ranges, keys0, keys1, vals0, vals1, hist, totals, tseg, edges, blk_starts, tail_np, tail, partials, inv_len,
+        total;
     int64_t max_tiles, max_blocks, max_works;
 };
 
@@ -1609,6 +1623,8 @@ Layout layout(const Plan &p, int64_t N) {
     L.tail_np = take(sizeof(int32_t) * L.max_blocks);
     L.tail = take(sizeof(int32_t) * L.max_blocks);
     L.partials = take(sizeof(float) * 2 * L.max_blocks * static_cast<size_t>(p.max_dim));
+    // mean pooling: fl32(1/L) of every bag
+    L.inv_len = take(p.pooling == TBE_POOL_MEAN ? sizeof(float) * static_cast<size_t>(p.T) * p.B : 0);
     L.total = o;
     return L;
 }
@@ -1625,6 +1641,7 @@ struct Ws {
     uint32_t *blk_starts;
     int32_t *tail_np, *tail;
     float *partials;
+    float *inv_len;  // mean pooling only
 };
 
 Ws carve(char *ws, const Layout &L) {
@@ -1643,6 +1660,7 @@ Ws carve(char *ws, const Layout &L) {
     w.tail_np = reinterpret_cast<int32_t *>(ws + L.tail_np);
     w.tail = reinterpret_cast<int32_t *>(ws + L.tail);
     w.partials = reinterpret_cast<float *>(ws + L.partials);
+    w.inv_len = reinterpret_cast<float *>(ws + L.inv_len);
     return w;
 }
 
@@ -1717,7 +1735,8 @@ hipError_t run_index(const Plan &p, const IT *indices, const IT *offsets, int64_
     hipLaunchKernelGGL(hist_zero_kernel, dim3(static_cast<unsigned>(zero_groups)), dim3(kThreads), 0, stream, w.hist,
                        w.ctl);
     hipLaunchKernelGGL((keys_kernel<V, IT>), dim3(static_cast<unsigned>((nbags + kKeyBags - 1) / kKeyBags)),
-                       dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights, mean, w.ranges, p.B, nbags,
+                       dim3(kThreads), 0, stream, p.meta_dev, indices, offsets, weights,
+                       mean && sizeof(V) == 4 ? w.inv_len : nullptr, w.ranges, p.B, nbags,
                        check, w.ctl, w.keys[0], w.keys[1], vals[0], vals[1], passes, (1u << nb0) - 1u, w.hist,
                        pbits, status);
     const dim3 tiles(static_cast<unsigned>(L.max_tiles)), blk(kThreads);
@@ -1762,27 +1781,45 @@ hipError_t run_reduce(const Plan &p, const void *grad_out, int64_t N, char *ws, 
     const int cur = sort_passes_all(p) & 1;
     const V *vals = static_cast<const V *>(w.vals[cur]);
     const dim3 blk(kThreads);
+    // mean pooling rides on 4-byte values, its weights read from inv_len
+    const bool mean = sizeof(V) == 4 && p.pooling == TBE_POOL_MEAN;
     if (!ap) {
-#define TBE_REDUCE(GT)                                                                                          \
-    hipLaunchKernelGGL((reduce_kernel<V, GT>), dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream,           \
+#define TBE_REDUCE(GT, M)                                                                                       \
+    hipLaunchKernelGGL((reduce_kernel<V, GT, M>), dim3(static_cast<unsigned>(L.max_works)), blk, 0, stream,        \
                        w.keys[cur], vals, grad_out, p.meta_dev, w.ranges, p.T, w.ctl, w.tseg, w.edges, p.total_dim, \
                        p.B * p.total_dim, grad_rows, capacity, status, w.partials, p.max_dim,                     \
-                       static_cast<const float *>(p.zero_page))
+                       static_cast<const float *>(p.zero_page), w.inv_len, p.B)
+#define TBE_REDUCE_M(GT)                                                                                        \
+    do {                                                                                                        \
+        if constexpr (sizeof(V) == 4) {                                                                         \
+            if (mean) TBE_REDUCE(GT, true); else TBE_REDUCE(GT, false);                                         \
+        } else {                                                                                                \
+            TBE_REDUCE(GT, false);                                                                              \
+        }                                                                                                       \
+    } while (0)
         // grad_out has the forward output's element type
-        if (p.out_dtype == TBE_F16) TBE_REDUCE(TBE_F16);
-        else if (p.out_dtype == TBE_BF16) TBE_REDUCE(TBE_BF16);
-        else TBE_REDUCE(TBE_F32);
+        if (p.out_dtype == TBE_F16) TBE_REDUCE_M(TBE_F16);
+        else if (p.out_dtype == TBE_BF16) TBE_REDUCE_M(TBE_BF16);
+        else TBE_REDUCE_M(TBE_F32);
+#undef TBE_REDUCE_M
 #undef TBE_REDUCE
     } else {
-#define TBE_REDUCE_APPLY(GT, A)                                                                                 \
-    hipLaunchKernelGGL((reduce_apply_kernel<V, GT, A>), dim3(static_cast<unsigned>(L.max_tiles)), blk, 0, stream,  \
-                       w.keys[cur], vals, grad_out, p.meta_dev, w.ranges, p.T, w.ctl, w.tseg, w.edges, p.total_dim, \
-                       p.B * p.total_dim, grad_rows, capacity, status, w.partials, p.max_dim,                     \
+#define TBE_REDUCE_APPLY(GT, M, A)                                                                              \
+    hipLaunchKernelGGL((reduce_apply_kernel<V, GT, M, A>), dim3(static_cast<unsigned>(L.max_tiles)), blk, 0,      \
+                       stream, w.keys[cur], vals, grad_out, p.meta_dev, w.ranges, p.T, w.ctl, w.tseg, w.edges,      \
+                       p.total_dim, p.B * p.total_dim, grad_rows, capacity, status, w.partials, p.max_dim,        \
                        static_cast<const float *>(p.zero_page), ap->grad_idx, ap->seg_offsets, grad_row_offsets,   \
-                       static_cast<char *>(ap->tables), p.dtype, ap->state, ap->lr, ap->eps)
+                       static_cast<char *>(ap->tables), p.dtype, ap->state, ap->lr, ap->eps, w.inv_len, p.B)
 #define TBE_REDUCE_APPLY_A(GT)                                                                                  \
     do {                                                                                                        \
-        if (ap->adagrad) TBE_REDUCE_APPLY(GT, true); else TBE_REDUCE_APPLY(GT, false);                          \
+        if constexpr (sizeof(V) == 4) {                                                                         \
+            if (mean && ap->adagrad) TBE_REDUCE_APPLY(GT, true, true);                                          \
+            else if (mean) TBE_REDUCE_APPLY(GT, true, false);                                                   \
+            else if (ap->adagrad) TBE_REDUCE_APPLY(GT, false, true);                                            \
+            else TBE_REDUCE_APPLY(GT, false, false);                                                            \
+        } else {                                                                                                \
+            if (ap->adagrad) TBE_REDUCE_APPLY(GT, false, true); else TBE_REDUCE_APPLY(GT, false, false);        \
+        }                                                                                                       \
     } while (0)
         if (p.out_dtype == TBE_F16) TBE_REDUCE_APPLY_A(TBE_F16);
         else if (p.out_dtype == TBE_BF16) TBE_REDUCE_APPLY_A(TBE_BF16);
@@ -1811,8 +1848,10 @@ hipError_t run_reduce(const Plan &p, const void *grad_out, int64_t N, char *ws, 
 
 size_t backward_workspace_bytes(const Plan &p, int64_t num_indices) { return layout(p, num_indices).total; }
 
-// Lookups carry a weight (64-bit sort values) when weighted or mean-pooled.
-static bool wide_values(const Plan &p, bool weighted) { return weighted || p.pooling == TBE_POOL_MEAN; }
+// Lookups carry a per-sample weight (64-bit sort values) when weighted; mean
+// pooling (which takes no per-sample weights) keeps 4-byte values and reads
+// each bag's fl32(1/L) in the reduce.
+static bool wide_values(const Plan &p, bool weighted) { return weighted && p.pooling != TBE_POOL_MEAN; }
 
 hipError_t launch_backward_index(const Plan &p, const void *indices, const void *offsets, int64_t num_indices,
                                  const float *weights, void *workspace, int64_t *grad_idx, int64_t *seg_offsets,
