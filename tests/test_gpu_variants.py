@@ -196,6 +196,37 @@ def test_mean_backward(index):
     check_backward(spec, d, backward(spec, d, pooling="mean", index=index), "mean")
 
 
+@pytest.mark.slow
+def test_full_size_cfg5_mean_backward_sampled():
+    """cfg5 at full size with mean pooling and int32 indices, in the
+    benchmark's launch configuration: the sort runs on 4-byte values (packed
+    records for the tables that fit) and the reduce reads each bag's
+    fl32(1/L).  Integer outputs bit-exact; gradient rows on a sample that
+    includes the longest segments."""
+    spec = workloads.make_config(5)
+    offsets = workloads.gen_offsets(spec, device())
+    d = {"offsets": offsets.to(torch.int32), "indices": workloads.gen_indices(spec, offsets).to(torch.int32),
+         "N": int(offsets[-1]), "grad_out": workloads.gen_grad_out(spec, device())}
+    g = backward(spec, d, pooling="mean", index="i32")
+    note("[var] cfg5 full mean/i32 backward: GPU done; oracle integer part")
+    idx = d["indices"].cpu().numpy().astype(np.int64)
+    off = d["offsets"].cpu().numpy().astype(np.int64)
+    seg = oracle.backward_segments(spec.rows, spec.dims, idx, off, spec.B)
+    gidx, segs, gro, rows = g.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(segs.numpy(), seg["seg_offsets"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    lens = np.diff(seg["seg_offsets"])
+    rng = np.random.default_rng(6)
+    sel = np.unique(np.concatenate([np.argsort(lens)[-20:], rng.choice(seg["U"], 2000, replace=False)]))
+    ref, ab, _ = oracle.backward_rows(spec.rows, spec.dims, off, spec.B, d["grad_out"].cpu().numpy(), seg, sel=sel,
+                                      pooling="mean")
+    got = np.concatenate([rows[int(gro[u]):int(gro[u + 1])].numpy() for u in sel])
+    err = float(oracle.summation_error(got, ref, ab).max())
+    note(f"[var] cfg5 full mean/i32 backward: U={seg['U']}, max summation error {err:.3g}")
+    assert err <= GRAD_RTOL
+
+
 @pytest.mark.parametrize("k", [5, 4])
 def test_int32_backward_equals_int64(k):
     spec = small(k=k, seed=2, T=4, B=300, grad=True, name=f"i32-bwd-cfg{k}")
