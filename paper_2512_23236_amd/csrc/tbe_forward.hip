@@ -337,10 +337,16 @@ __device__ inline void pool_unit(const TableMeta &m, const char *__restrict__ ta
         int32_t bag_end = bnd[1];
         while (bag + 1 < nbs && bag_end == 0) bag_end = end_of(++bag);
 
+        // The unweighted weight 1.0, hidden from the optimizer for fp16
+        // rows: fma(1, x, acc) is x + acc exactly, and kept as an fma it
+        // widens and adds in one mixed-precision instruction (v_fma_mix)
+        // where the folded form takes a convert and an add.
+        float one = 1.0f;
+        if constexpr (DT == TBE_F16 && !WEIGHTED) asm volatile("" : "+s"(one));
         // consume ring slot sl, the lookup at stream position rp
         auto consume = [&](int32_t rp, auto sc) {
             constexpr int sl = decltype(sc)::value;
-            E::fma(acc[sl & 1], ring[sl], WEIGHTED ? ring_w[WEIGHTED ? sl : 0] : 1.0f,
+            E::fma(acc[sl & 1], ring[sl], WEIGHTED ? ring_w[WEIGHTED ? sl : 0] : one,
                    kQuant ? ring_sb[kQuant ? sl : 0] : f2{0.f, 0.f});
             if (rp < Q && rp + 1 == bag_end) {
                 float *st = my_stage + bag * LPR * E::kPerVec;
