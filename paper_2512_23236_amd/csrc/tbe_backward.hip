@@ -8,11 +8,14 @@
 //   setup     per-table lookup ranges [offsets[tB], offsets[(t+1)B]) and the
 //             tiling of each range into tiles of kTile positions.
 //   keys      one workgroup per run of bags writes key_j = idx_j (32-bit,
-//             local to the table) and val_j = b(j) (plus the weight), and
-//             counts the first radix pass's digits per tile.  A table's
-//             lookups already occupy exactly the positions its rows take in
-//             the global order, so sorting every table's range by its local
-//             key yields the global stable sort.
+//             local to the table) and val_j = b(j) (plus the per-sample
+//             weight, when there is one), or, where key and batch row fit
+//             one 32-bit word together, that packed word alone; under mean
+//             pooling it writes each bag's fl32(1/L).  It also counts the
+//             first radix pass's digits per tile.  A table's lookups already
+//             occupy exactly the positions its rows take in the global order,
+//             so sorting every table's range by its local key yields the
+//             global stable sort.
 //   radix     stable LSD radix sort of each range, 8-bit digits, each table
 //             over the bits of its own row count: per pass a tile histogram
 //             (one contiguous row per tile; the first pass's come from the
@@ -20,7 +23,8 @@
 //             table's tiles, and a stable scatter that ranks keys with wave
 //             ballots, derives its digits' final positions from the table's
 //             digit totals and its tile's row, and stages the tile in LDS so
-//             global writes run in digit order.
+//             global writes run in digit order.  A table's last pass writes
+//             packed records apart again.
 //   segments  per tile: segment starts (key change) per block and tile and
 //             kept lookups; one scan over tiles; then grad_idx / seg_offsets /
 //             grad_row_offsets are written for every segment start, and the
@@ -29,7 +33,8 @@
 //             counts).
 //   reduce    sorted positions are cut into fixed blocks of kBlk; a wave
 //             walks a range of blocks in order for one column slice,
-//             accumulating fp32 rows of grad_out; a segment of at most kBlk
+//             accumulating fp32 rows of grad_out (times the lookup's weight,
+//             or its bag's fl32(1/L)); a segment of at most kBlk
 //             lookups is summed whole and written straight to its gradient
 //             row (its only writer); a longer one leaves one piece per block
 //             it touches.
