@@ -193,6 +193,18 @@ def test_packed_records_at_the_width_limit(B):
     assert float(oracle.summation_error(grows.numpy(), ref, ab).max()) <= GRAD_RTOL
 
 
+@pytest.mark.parametrize("k", [5, 4])
+@pytest.mark.parametrize("B", [1, 2])
+def test_tiny_batches(k, B):
+    # a batch row of 0 (B = 1) or 1 (B = 2) bits: every unweighted table's
+    # records pack with the key field alone (B = 1) or above one bit; k = 4
+    # carries weights (8-byte values, never packed)
+    rows = np.array([1, 7, 300, 70000], np.int64)
+    spec = dataclasses.replace(workloads.small_config(k, seed=13, T=len(rows), B=B), rows=rows,
+                               name=f"bwd-tiny-{k}-{B}")
+    check(spec)
+
+
 def test_deterministic_repeat():
     spec = workloads.small_config(4, seed=8, T=3, B=400)
     d = workloads.gen_all(dataclasses.replace(spec, grad=True), device())

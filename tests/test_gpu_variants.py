@@ -189,6 +189,16 @@ def check_backward(spec, d, g, pooling):
     assert err <= GRAD_RTOL
 
 
+@pytest.mark.parametrize("B", [1, 2])
+def test_mean_backward_tiny_batches(B):
+    # one or two batch rows: packed records with 0 or 1 batch-row bits, and
+    # each bag's fl32(1/L) read back by batch row
+    spec = dataclasses.replace(small(k=5, seed=2, T=4, B=B, name=f"mean-bwd-B{B}"),
+                               rows=np.array([1, 7, 300, 70000], np.int64))
+    d = inputs(spec)
+    check_backward(spec, d, backward(spec, d, pooling="mean"), "mean")
+
+
 @pytest.mark.parametrize("index", ["i64", "i32"])
 def test_mean_backward(index):
     spec = small(k=5, seed=1, T=4, B=300, name=f"mean-bwd-{index}")
