@@ -15,7 +15,9 @@ import numpy as np
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libtbe.so")
+# the in-tree build; TBE_LIBRARY names another build of the same ABI (for
+# side-by-side timing of two builds)
+LIB_PATH = os.environ.get("TBE_LIBRARY") or os.path.join(HERE, "libtbe.so")
 ABI_VERSION = 3
 
 F32, F16, BF16, U8_ROWWISE = 0, 1, 2, 3

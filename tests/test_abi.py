@@ -115,6 +115,18 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
         tbe.lib()
 
 
+def test_library_override_fails_loudly_when_missing(tmp_path):
+    """TBE_LIBRARY names another build; a missing one raises, never falls back."""
+    import subprocess
+    import sys
+    code = ("from paper_2512_23236_amd import tbe\n"
+            "try:\n    tbe.lib()\nexcept ImportError as e:\n    print('raised', e)\n")
+    env = dict(os.environ, TBE_LIBRARY=str(tmp_path / "other.so"))
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert "raised" in r.stdout and "other.so" in r.stdout
+
+
 def test_product_path_does_not_touch_the_oracle():
     """The package and its sources never import or link the CPU oracle."""
     pkg = os.path.join(ROOT, "paper_2512_23236_amd")
