@@ -189,6 +189,44 @@ def check_backward(spec, d, g, pooling):
     assert err <= GRAD_RTOL
 
 
+def test_mean_backward_counts_dropped_lookups():
+    """Mean-pooled backward with bounds checking: a bad lookup is dropped but
+    still counts in its bag's L, so every good lookup of the bag carries
+    fl32(1/L) of the full bag.  Expected: the oracle's weighted backward of the
+    good lookups alone, each weighted by fl32(1/L) of its original bag."""
+    spec = small(k=5, seed=4, T=3, B=150, name="mean-bwd-oob")
+    d = inputs(spec)
+    N = d["N"]
+    off = d["offsets"].cpu().numpy().astype(np.int64)
+    lens = np.diff(off)
+    bags = np.nonzero(lens >= 2)[0][:5]
+    bad = off[bags]  # the first lookup of five bags
+    good = d["indices"].clone()
+    d["indices"][torch.as_tensor(bad, device=device())] = int(spec.rows.max()) + 7
+    plan = make_plan(spec, pooling="mean")
+    st = torch.zeros(1, dtype=torch.int32, device=device())
+    g = tbe.backward(plan, d["grad_out"], d["indices"], d["offsets"], None, status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == tbe.STATUS_INDEX_OOB
+    keep = np.ones(N, bool)
+    keep[bad] = False
+    bag_of = np.repeat(np.arange(lens.size), lens)
+    with np.errstate(divide="ignore"):  # empty bags have no lookups to weight
+        inv = (np.float32(1.0) / lens.astype(np.float32)).astype(np.float32)  # fl32(1/L) of every bag
+    w = inv[bag_of][keep]
+    off2 = np.zeros_like(off)
+    np.cumsum(np.bincount(bag_of[keep], minlength=lens.size), out=off2[1:])
+    idx = good.cpu().numpy().astype(np.int64)[keep]
+    seg = oracle.backward_segments(spec.rows, spec.dims, idx, off2, spec.B)
+    ref, ab, _ = oracle.backward_rows(spec.rows, spec.dims, off2, spec.B, d["grad_out"].cpu().numpy(), seg,
+                                      weights=w, pooling="sum")
+    gidx, segs, gro, rows = g.trimmed()
+    np.testing.assert_array_equal(gidx.numpy(), seg["grad_idx"])
+    np.testing.assert_array_equal(segs.numpy(), seg["seg_offsets"])
+    np.testing.assert_array_equal(gro.numpy(), seg["grad_row_offsets"])
+    assert float(oracle.summation_error(rows.numpy(), ref, ab).max()) <= GRAD_RTOL
+
+
 @pytest.mark.parametrize("B", [1, 2])
 def test_mean_backward_tiny_batches(B):
     # one or two batch rows: packed records with 0 or 1 batch-row bits, and
