@@ -278,6 +278,7 @@ __device__ inline int packed_shift(int64_t rows, int pbits) {
 // run's lookups fall in a few consecutive tiles, counted in LDS for the first
 // kKeyTiles of them (global atomics beyond) and added to `hist` at the end.
 constexpr int kKeyTiles = 8;
+constexpr int kKeyHints = 2048;  // keys kernel: bag hints per run (one per 2^gsh lookups)
 template <typename V, typename IT>
 __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restrict__ meta,
                                                         const IT *__restrict__ indices,
@@ -298,6 +299,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
     __shared__ int8_t bag_ps[kKeyBags];     // shift of the key field in packed records, or -1
     __shared__ uint32_t bag_kf[kKeyBags];   // mask of the table's key field
     __shared__ uint32_t h0[kKeyTiles * kBuckets];  // first-pass digit counts of the run's first tiles
+    __shared__ uint8_t hint[kKeyHints];            // bag holding every 2^gsh-th lookup of the run
     __shared__ int64_t tile_lo;
     __shared__ int bad;
     const int tid = threadIdx.x;
@@ -345,11 +347,31 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
     }
     const int64_t first = off[0], last = off[nk];
     if (first >= last) return;
-    auto bag_of = [&](int64_t j) {  // off[lo] <= j < off[lo + 1]
-        int lo = 0, hi = nk;
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (off[mid] <= j) lo = mid; else hi = mid;
+    // A lookup's bag: the bag holding every 2^gsh-th lookup of the run is
+    // noted in LDS (at most kKeyHints notes), so a lookup's bag lies between
+    // two notes and the binary search over the staged offsets covers only
+    // those bags (usually one or two) instead of all nk.
+    int gsh = 5;
+    while (((last - first) >> gsh) >= kKeyHints) ++gsh;
+    const int nq = static_cast<int>((last - first - 1) >> gsh) + 1;  // notes at lookups first + (q << gsh) < last
+    for (int i = tid; i < nk; i += kThreads) {
+        // the noted lookups inside bag i (clamped, so malformed offsets of
+        // an unchecked call stay inside the notes)
+        const int64_t g = (int64_t(1) << gsh) - 1;
+        int64_t q0 = (off[i] - first + g) >> gsh, q1 = (off[i + 1] - first + g) >> gsh;
+        q0 = q0 < 0 ? 0 : q0;
+        q1 = q1 > nq ? nq : q1;
+        for (int64_t q = q0; q < q1; ++q) hint[q] = static_cast<uint8_t>(i);
+    }
+    __syncthreads();
+    static_assert(kKeyBags <= 256, "bag notes are 8-bit");
+    auto bag_of = [&](int64_t j) {  // the last bag lo with off[lo] <= j: off[lo] <= j < off[lo + 1]
+        const int q = static_cast<int>((j - first) >> gsh);
+        int lo = hint[q];
+        int hi = q + 1 < nq ? hint[q + 1] : nk - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (off[mid] <= j) lo = mid; else hi = mid - 1;
         }
         return lo;
     };
