@@ -278,6 +278,15 @@ __device__ inline int packed_shift(int64_t rows, int pbits) {
 // run's lookups fall in a few consecutive tiles, counted in LDS for the first
 // kKeyTiles of them (global atomics beyond) and added to `hist` at the end.
 constexpr int kKeyTiles = 8;
+// What the keys kernel needs of a lookup's bag, read as one 32-byte record.
+struct alignas(16) KeyBag {
+    int64_t tile_off;  // kTile * (the table's first tile) - (its first position)
+    int64_t rows;      // R_t of the bag's table
+    uint32_t b;        // batch row
+    uint32_t kf;       // mask of the table's key field
+    int32_t ps;        // shift of the key field in packed records, or -1
+    uint32_t buf;      // buffer the bag's table starts its sort in
+};
 constexpr int kKeyHints = 2048;  // keys kernel: bag hints per run (one per 2^gsh lookups)
 template <typename V, typename IT>
 __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restrict__ meta,
@@ -292,12 +301,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
                                                         uint32_t mask0, uint32_t *__restrict__ hist, int pbits,
                                                         int32_t *status) {
     __shared__ int64_t off[kKeyBags + 1];
-    __shared__ int64_t bag_rows[kKeyBags];  // R_t of each bag's table
-    __shared__ int64_t bag_tile[kKeyBags];  // kTile * (the table's first tile) - (its first position)
-    __shared__ uint32_t bag_b[kKeyBags];    // batch row of each bag
-    __shared__ uint8_t bag_buf[kKeyBags];   // buffer the bag's table starts its sort in
-    __shared__ int8_t bag_ps[kKeyBags];     // shift of the key field in packed records, or -1
-    __shared__ uint32_t bag_kf[kKeyBags];   // mask of the table's key field
+    __shared__ KeyBag bags[kKeyBags];
     __shared__ uint32_t h0[kKeyTiles * kBuckets];  // first-pass digit counts of the run's first tiles
     __shared__ uint8_t hint[kKeyHints];            // bag holding every 2^gsh-th lookup of the run
     __shared__ int64_t tile_lo;
@@ -312,14 +316,13 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
     // table and batch row once per bag, not per lookup
     for (int i = tid; i < nk; i += kThreads) {
         const int64_t t = (k0 + i) / B;
-        bag_b[i] = static_cast<uint32_t>(k0 + i - t * B);
-        bag_rows[i] = meta[t].rows;
-        bag_buf[i] = static_cast<uint8_t>((passes - meta[t].sort_passes) & 1);
-        bag_ps[i] = static_cast<int8_t>(sizeof(V) == 4 ? packed_shift(meta[t].rows, pbits) : -1);
-        bag_kf[i] = 0xffffffffu >> (32 - table_key_bits(meta[t].rows));
-        // position j of the bag's table lies in tile (bag_tile + j) / kTile
+        const int64_t rows = meta[t].rows;
+        // position j of the bag's table lies in tile (tile_off + j) / kTile
         const Range r = ranges[t];
-        bag_tile[i] = r.tile_base * kTile - r.start;
+        bags[i] = KeyBag{r.tile_base * kTile - r.start, rows, static_cast<uint32_t>(k0 + i - t * B),
+                         0xffffffffu >> (32 - table_key_bits(rows)),
+                         sizeof(V) == 4 ? packed_shift(rows, pbits) : -1,
+                         static_cast<uint32_t>((passes - meta[t].sort_passes) & 1)};
     }
     __syncthreads();
     if (inv_len) {
@@ -375,7 +378,7 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         }
         return lo;
     };
-    if (tid == 0) tile_lo = (bag_tile[bag_of(first)] + first) / kTile;
+    if (tid == 0) tile_lo = (bags[bag_of(first)].tile_off + first) / kTile;
     __syncthreads();
     const int64_t t_lo = tile_lo;
     // kKeyAhead rounds of the run's lookups at a time: their index (and
@@ -393,22 +396,23 @@ __global__ __launch_bounds__(kThreads) void keys_kernel(const TableMeta *__restr
         for (int r = 0; r < kKeyAhead; ++r) {
             const int64_t j = j0 + static_cast<int64_t>(r) * kThreads;
             if (j >= last) break;
-            const int lo = bag_of(j);
-            const uint32_t b = bag_b[lo];
+            const KeyBag bg = bags[bag_of(j)];
+            const uint32_t b = bg.b;
             const int64_t idx = ids[r];
             uint32_t key = static_cast<uint32_t>(idx);
-            if (check && (idx < 0 || idx >= bag_rows[lo])) {
+            if (check && (idx < 0 || idx >= bg.rows)) {
                 key = kSentinel;
                 atomicOr(status, TBE_STATUS_INDEX_OOB);
             }
-            const bool second = bag_buf[lo] != 0;
+            const bool second = bg.buf != 0;
             uint32_t *const keys = second ? keys1 : keys0;
             V *const vals = second ? vals1 : vals0;
-            const int ps = bag_ps[lo];
+            const int ps = bg.ps;
             // the record's key word: the key, or key field and batch row packed
-            const uint32_t rec = ps >= 0 ? ((key & bag_kf[lo]) << ps) | b : key;
+            const uint32_t rec = ps >= 0 ? ((key & bg.kf) << ps) | b : key;
             keys[j] = rec;
-            const int64_t tj = (bag_tile[lo] + j) / kTile;  // the lookup's tile
+            // the lookup's tile (tile_off + j >= 0)
+            const int64_t tj = static_cast<int64_t>(static_cast<uint64_t>(bg.tile_off + j) / kTile);
             const uint32_t d = (rec >> (ps > 0 ? ps : 0)) & mask0;
             if (tj - t_lo < kKeyTiles) atomicAdd(&h0[(tj - t_lo) * kBuckets + d], 1u);
             else atomicAdd(&hist[tj * kBuckets + d], 1u);
