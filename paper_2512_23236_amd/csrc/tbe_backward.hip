@@ -589,9 +589,8 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
     const uint32_t *__restrict__ prefix, const uint32_t *__restrict__ totals, const TableMeta *__restrict__ meta,
     const Range *__restrict__ ranges, int T, const Ctl *__restrict__ ctl, int pass, int passes, int shift,
     int nbits, int pbits) {
-    __shared__ uint32_t cnt[kScWaves][kBuckets];  // per-wave digit counts, then wave offsets
-    __shared__ uint32_t tstart[kBuckets];       // first tile-local slot of each digit
-    __shared__ uint32_t goff[kBuckets];         // first global slot of each digit for this tile
+    __shared__ uint32_t cnt[kScWaves][kBuckets];  // per-wave digit counts, then each wave's first tile slot
+    __shared__ uint32_t gdelta[kBuckets];       // global slot of a digit's key minus its tile slot
     __shared__ uint32_t sk[kTile];
     __shared__ V sv[kTile];
     __shared__ uint32_t lds[kScWaves];
@@ -656,25 +655,27 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
         // thread d < kBuckets: digit d (the other threads join the scans with 0)
         const int d = tid;
         const bool dig = d < kBuckets;
-        uint32_t run = 0;
+        uint32_t run = 0, before[kScWaves];  // digit d's keys of the earlier waves
         if (dig) {
 #pragma unroll
             for (int w = 0; w < kScWaves; ++w) {
-                const uint32_t c = cnt[w][d];
-                cnt[w][d] = run;
-                run += c;
+                before[w] = run;
+                run += cnt[w][d];
             }
         }
         uint32_t tot;
-        const uint32_t ts = scatter_scan(run, lds, &tot);
+        const uint32_t ts = scatter_scan(run, lds, &tot);  // digit d's first tile slot
         // first global slot of digit d for this tile: the table's first
         // position, the table's keys of smaller digits, then this digit's keys
         // in the table's earlier tiles
         const uint32_t below =
             scatter_scan(dig ? totals[static_cast<int64_t>(ti.t) * kBuckets + d] : 0u, lds, &tot);
         if (dig) {
-            tstart[d] = ts;
-            goff[d] = static_cast<uint32_t>(ranges[ti.t].start) + below + prefix[tile * kBuckets + d];
+#pragma unroll
+            for (int w = 0; w < kScWaves; ++w) cnt[w][d] = ts + before[w];
+            // a tile slot i of digit d goes to global slot gdelta[d] + i (the
+            // global slot is never below the tile slot)
+            gdelta[d] = static_cast<uint32_t>(ranges[ti.t].start) + below + prefix[tile * kBuckets + d] - ts;
         }
     }
     __syncthreads();
@@ -683,7 +684,7 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
         const int64_t pos = wbase + r * 64 + lane;
         if (pos < ti.p_hi) {
             const uint32_t d = digit_of(key[r], shift, mask);
-            const uint32_t slot = tstart[d] + cnt[wave][d] + rank[r];
+            const uint32_t slot = cnt[wave][d] + rank[r];
             sk[slot] = key[r];
             if (!packed) sv[slot] = val[r];
         }
@@ -693,7 +694,7 @@ __global__ __launch_bounds__(kScThreads) void radix_scatter_kernel(
     for (int i = tid; i < n; i += kScThreads) {
         const uint32_t k = sk[i];
         const uint32_t d = digit_of(k, shift, mask);
-        const int64_t dst = static_cast<int64_t>(goff[d]) + (i - static_cast<int64_t>(tstart[d]));
+        const int64_t dst = static_cast<int64_t>(gdelta[d]) + i;
         if (!packed) {
             keys_out[dst] = k;
             vals_out[dst] = sv[i];
